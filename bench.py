@@ -1,0 +1,271 @@
+"""Benchmark of the Sirius hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Workload (headline): one Llama-3-8B FFN layer (d_model 4096, d_ff 14336, bf16
+neuron-major weights ~ N(0, 0.02)), batch-1 decode with per-token threshold
+sparsity calibrated to 50% from 256 seeded N(0, 1) inputs. Eight copies of the
+layer (2.8 GB) are rotated so that the 256 MB last-level cache cannot serve the
+weights between steps.
+
+One step is one pass over every row of the hot path, each on its own synthetic
+batch, all inputs resident in HBM:
+  cats      sparse FFN decode, one token            (gate GEMV + SiLU + threshold +
+                                                     compaction, sparse up/down, reduce)
+  rmsnorm   RMSNorm of the layer output             (stack glue)
+  griffin   prompt top-k select + condensation      (512-token prompt, k = 7168)
+  condensed condensed-weight FFN decode, one token
+  dense     dense FFN decode, one token
+  dense16   the full model's 16-token FFN pass
+  verify    correction check over logits [8, 16, 128256]
+The printed value is the sparse FFN decode time per token (rows.cats); the
+roofline object is for the sparse path's dominant kernel (cats_gate), timed
+by the library's per-kernel HIP events over the timed region.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+D_MODEL, D_FF = 4096, 14336
+NCOPY = 8
+N_DECODE = 64
+PROMPT_T = 512
+VERIFY_B, VERIFY_K, VERIFY_V = 8, 16, 128256
+N_LOGIT_BUFS = 4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2409_03856_amd as sr
+    from synth import decode_inputs, calibration_inputs, griffin_prompt, verify_inputs
+
+    assert torch.cuda.is_available()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    sr.lib()
+
+    # ------------------------------------------------------------------ setup (untimed)
+    log("setup: filling weights")
+    layers = []
+    for c in range(NCOPY):
+        ws = []
+        for m in range(3):
+            w = torch.empty((D_FF, D_MODEL), dtype=torch.bfloat16, device=dev)
+            sr.sirius_fill_normal_bf16(w, seed=1000 + 3 * c + m, mean=0.0, std=0.02)
+            ws.append(w)
+        layers.append(ws)
+    x_cal = torch.from_numpy(calibration_inputs(1, 256, D_MODEL)).to(dev)
+    t_dev = [sr.sirius_cats_calibrate(x_cal, layers[c][0], 0.5) for c in range(NCOPY)]
+    thresholds = [float(t.item()) for t in t_dev]
+    xs = torch.from_numpy(decode_inputs(2, N_DECODE, D_MODEL)).to(dev)
+    x16 = torch.from_numpy(decode_inputs(3, VERIFY_K, D_MODEL)).to(dev)
+    prompt = torch.from_numpy(griffin_prompt(4, PROMPT_T, D_MODEL).view(np.int16)).view(torch.bfloat16).to(dev)
+    k_keep = D_FF // 2
+    log("setup: prompt top-k per copy")
+    cond = [sr.sirius_griffin_select(prompt, *layers[c], k_keep, want_scores=False)[2:] for c in range(NCOPY)]
+    log("setup: logits")
+    logits, drafted = [], []
+    for i in range(N_LOGIT_BUFS):
+        lg, dr = verify_inputs(10 + i, VERIFY_B, VERIFY_K, VERIFY_V, 3.0)
+        logits.append(torch.from_numpy(lg).to(dev))
+        drafted.append(torch.from_numpy(dr).to(dev))
+
+    y = torch.empty((1, D_MODEL), dtype=torch.float32, device=dev)
+    hn = torch.empty_like(y)
+    yc = torch.empty_like(y)
+    yd = torch.empty_like(y)
+    y16 = torch.empty((VERIFY_K, D_MODEL), dtype=torch.float32, device=dev)
+    act_idx = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
+    cnt_log = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
+    g_sel = torch.empty(k_keep, dtype=torch.int32, device=dev)
+    g_c = [torch.empty((k_keep, D_MODEL), dtype=torch.bfloat16, device=dev) for _ in range(3)]
+    acc = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
+    nxt = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
+
+    rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify"]
+    stream = torch.cuda.current_stream()
+
+    def step(s, ev=None):
+        c = s % NCOPY
+
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+
+        mark(0)
+        sr.sirius_ffn_cats(xs[s % N_DECODE: s % N_DECODE + 1], *layers[c], thresholds[c], y=y,
+                           active_idx=act_idx, active_cnt=cnt_log[s:s + 1])
+        mark(1)
+        sr.sirius_rmsnorm(y, 1e-5, out=hn)
+        mark(2)
+        c2 = (c + 2) % NCOPY
+        sr.sirius_griffin_select(prompt, *layers[c2], k_keep, want_scores=False, sel_idx=g_sel,
+                                 w_gate_c=g_c[0], w_up_c=g_c[1], w_down_c=g_c[2])
+        mark(3)
+        sr.sirius_ffn_condensed(xs[(s + 1) % N_DECODE:(s + 1) % N_DECODE + 1], *cond[(c + 4) % NCOPY], y=yc)
+        mark(4)
+        sr.sirius_ffn_dense(xs[(s + 2) % N_DECODE:(s + 2) % N_DECODE + 1], *layers[(c + 6) % NCOPY], y=yd)
+        mark(5)
+        sr.sirius_ffn_dense(x16, *layers[(c + 3) % NCOPY], y=y16)
+        mark(6)
+        sr.sirius_verify_accept(logits[s % N_LOGIT_BUFS], drafted[s % N_LOGIT_BUFS], 0.1, 1.0,
+                                accept_len=acc, next_token=nxt, want_p=False)
+        mark(7)
+
+    log("warmup")
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+
+    # ------------------------------------------------------------------ timed region
+    sr.sirius_profile_reset()
+    sr.sirius_profile_enable(True)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(rows) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sr.sirius_profile_enable(False)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    row_ms = {r: [] for r in rows}
+    for i in range(args.steps):
+        for j, r in enumerate(rows):
+            row_ms[r].append(evs[i][j].elapsed_time(evs[i][j + 1]))
+    kern = {}
+    for name in ["cats_gate", "ffn_down", "ffn_reduce", "verify_stats", "verify_scan", "griffin_z",
+                 "griffin_score", "griffin_pick", "condense", "select_hist", "select_pick", "select_init",
+                 "rmsnorm"]:
+        tot, n = sr.sirius_profile_query(name)
+        if n:
+            kern[name] = {"avg_us": round(tot * 1e3 / n, 3), "launches": n}
+    sr.sirius_profile_reset()
+
+    counts = cnt_log[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64)
+    mean_active = float(counts.mean())
+    # algorithmic bytes (what the method must move), per launch
+    gate_bytes = D_FF * D_MODEL * 2 + mean_active * D_MODEL * 2 + D_MODEL * 4
+    cats_bytes = D_FF * D_MODEL * 2 + 2 * mean_active * D_MODEL * 2 + 2 * D_MODEL * 4
+    dense_bytes = 3 * D_FF * D_MODEL * 2 + 2 * D_MODEL * 4
+    cond_bytes = 3 * k_keep * D_MODEL * 2 + 2 * D_MODEL * 4
+    verify_bytes = VERIFY_B * VERIFY_K * VERIFY_V * 4
+    griffin_bytes = 2 * D_FF * D_MODEL * 2 + PROMPT_T * D_MODEL * 2 + 6 * k_keep * D_MODEL * 2
+    row_bytes = {"cats": cats_bytes, "rmsnorm": 2 * D_MODEL * 4, "griffin": griffin_bytes,
+                 "condensed": cond_bytes, "dense": dense_bytes, "dense16": dense_bytes + 2 * VERIFY_K * D_MODEL * 4,
+                 "verify": verify_bytes}
+
+    def med(v):
+        return float(np.median(np.asarray(v)))
+
+    rows_out = {}
+    for r in rows:
+        us = med(row_ms[r]) * 1e3
+        gbps = row_bytes[r] / (us * 1e-6) / 1e9
+        rows_out[r] = {"us": round(us, 2), "alg_bytes": int(row_bytes[r]), "gbps": round(gbps, 1),
+                       "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
+    cats_us = float(np.mean(row_ms["cats"])) * 1e3
+    gate_us = kern["cats_gate"]["avg_us"]
+    gate_gbps = gate_bytes / (gate_us * 1e-6) / 1e9
+
+    out = {
+        "metric": "sparse-FFN decode µs/token & achieved HBM GB/s vs peak; 8B & 70B FFN shapes",
+        "value": round(cats_us, 3),
+        "unit": "us/token",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "llama3-8b-ffn-layer: CATS threshold decode, batch 1, 50% target sparsity",
+            "d_model": D_MODEL, "d_ff": D_FF, "batch": 1, "weights": "bf16 N(0,0.02) neuron-major",
+            "layer_copies_rotated": NCOPY, "mean_active_neurons": round(mean_active, 1),
+            "realized_sparsity": round(1.0 - mean_active / D_FF, 4),
+            "cats_hbm_gbps": round(cats_bytes / (cats_us * 1e-6) / 1e9, 1),
+        },
+        "roofline": {
+            "kernel": "cats_gate",
+            "bound": "hbm",
+            "achieved": round(gate_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(gate_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "alg_bytes_per_launch": int(gate_bytes),
+            "avg_launch_us": gate_us,
+        },
+        "rows": rows_out,
+        "kernels": kern,
+    }
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layers[0], thresholds[0], xs, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(layer, t, xs, budget_s):
+    """The fp64 oracle's threshold-sparse decode of the same layer on the host cores."""
+    import numpy as np
+    import torch
+    import oracle
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    log("cpu baseline: widening weights (not timed)")
+    w = [oracle.widen_bf16(m.view(torch.int16).cpu().numpy().view(np.uint16)) for m in layer]
+    x_host = xs.cpu().numpy()
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.ffn_cats(x_host[n % x_host.shape[0]:n % x_host.shape[0] + 1], *w, t)
+        n += 1
+        el = time.perf_counter() - t0
+        if (el >= budget_s and n >= 3) or n >= 400:
+            break
+    return {"value": round(el / n * 1e6, 1), "unit": "us/token", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} batch-1 decode tokens of the 8B FFN layer (fp64 NumPy, weights widened beforehand, "
+                      f"untimed) in {el:.1f} s; affinity {len(os.sched_getaffinity(0))} cpus"}
+
+
+if __name__ == "__main__":
+    main()

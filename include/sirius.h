@@ -1,0 +1,226 @@
+/*
+ * sirius.h -- C ABI of the MI355X (gfx950) library for the hot path of
+ * Sirius, "Contextual Sparsity with Correction for Efficient LLMs"
+ * (arXiv 2409.03856).
+ *
+ * The path has two halves:
+ *   1. the contextual-sparse SwiGLU FFN decode step the sparse model runs on
+ *      every token (Sec. 2.1: fine-grained per-token sparsity, FSparse, after
+ *      CATS; coarse-grained prompt-fixed sparsity, CSparse, after Griffin);
+ *   2. the full model's correction check of a chunk of drafted tokens
+ *      (Algorithm 1; Sec. 4 "How to correct"): likelihood of each drafted
+ *      token, first rejection below a threshold, the full model's own token
+ *      at that position.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor arguments are DEVICE pointers owned by the caller, contiguous,
+ *    row-major. The library never frees or retains them.
+ *  - Weights are bfloat16 passed as uint16_t bit patterns. All three FFN
+ *    matrices are NEURON-MAJOR [d_ff, d_model]: row i of W_gate and W_up are
+ *    neuron i's input weights, row i of W_down its output weights. Rows
+ *    must be 16-byte aligned (d_model % 8 == 0 and 16-byte aligned bases).
+ *  - Activations x, y, residuals are fp32 [B, d_model]. Accumulation is fp32.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Every call only
+ *    enqueues work on that stream and returns; nothing synchronizes.
+ *  - `ws` is a caller-owned device workspace of at least
+ *    sirius_workspace_size(op, ...) bytes, 256-byte aligned. Its contents on
+ *    entry are ignored; calls that share one workspace must be ordered on
+ *    one stream.
+ *  - Return value: SIRIUS_OK (0) on success, else a negative code. Arguments
+ *    are validated on the host BEFORE anything is enqueued, so a failing
+ *    call has launched nothing. sirius_last_error() returns a message for
+ *    the calling thread's most recent failure.
+ *  - B == 0 (empty batch) is a valid no-op that returns SIRIUS_OK.
+ *  - Limits of this build: 8 <= d_model <= 8192, 1 <= d_ff <= 65536,
+ *    B <= 64 for the FFN entry points.
+ */
+#ifndef SIRIUS_H
+#define SIRIUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SIRIUS_OK 0
+#define SIRIUS_EINVAL (-1)    /* null pointer, bad size, bad scalar */
+#define SIRIUS_EWORKSPACE (-2) /* ws_bytes smaller than sirius_workspace_size() */
+#define SIRIUS_EHIP (-3)      /* the HIP runtime refused a launch */
+
+/* Operation codes for sirius_workspace_size(). */
+#define SIRIUS_OP_FFN_DENSE 0
+#define SIRIUS_OP_FFN_CATS 1
+#define SIRIUS_OP_GRIFFIN_SELECT 2
+#define SIRIUS_OP_FFN_CONDENSED 3
+#define SIRIUS_OP_VERIFY 4
+#define SIRIUS_OP_CATS_CALIBRATE 5
+
+/*
+ * Dense SwiGLU FFN (the full model, sparsity 0):
+ *   y[b] = resid[b] + sum_i SiLU(W_gate[i].xn[b]) * (W_up[i].xn[b]) * W_down[i]
+ * where xn = RMSNorm(x) with unit weight when norm_eps >= 0, else xn = x.
+ * The FFN form is the Llama SwiGLU MLP the paper sparsifies (Sec. 2.1);
+ * the full model's parallel pass over a drafted chunk (Algorithm 1, Sec.
+ * 2.2) is this call with B = chunk length.
+ *   x      [B, d_model] fp32 input (read only).
+ *   resid  [B, d_model] fp32 added to the output, or NULL. May alias y.
+ *   y      [B, d_model] fp32 output. May alias resid, must not alias x
+ *          unless resid == x == y (in-place residual layer).
+ * For B >= 8 the gate and up products run on MFMA with x rounded to bf16
+ * and the intermediate h rounded to bf16 for the down product (fp32
+ * accumulation); for B < 8 x stays fp32.
+ * Errors: SIRIUS_EINVAL for null pointers (resid may be NULL), d_model not
+ * a multiple of 8 or outside [8, 8192], d_ff < 1, B < 0 or B > 64.
+ */
+int sirius_ffn_dense(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                     const uint16_t* w_down, int d_model, int d_ff, float norm_eps,
+                     const float* resid, float* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Fine-grained (per-token) contextual sparsity, FSparse after CATS
+ * (Sec. 2.1; Sec. 3 FSparse description: the gate stays dense, up and down
+ * are sparse). For each token b:
+ *   a_bi = SiLU(W_gate[i].xn[b]);  A_b = { i : |a_bi| > t }  (strict;
+ *   t < 0 keeps every neuron, t = +inf none)
+ *   y[b] = resid[b] + sum_{i in A_b} a_bi * (W_up[i].xn[b]) * W_down[i]
+ * Only rows of W_up and W_down in the union of the A_b are read.
+ *   active_idx [B, d_ff] int32 out: A_b in ascending order in
+ *              active_idx[b*d_ff .. b*d_ff + active_cnt[b]); the rest of the
+ *              row is left untouched. May be NULL together with active_cnt.
+ *   active_cnt [B] int32 out: |A_b|.
+ * The gate dot products, SiLU and the comparison are fp32 from the fp32
+ * input (x is never rounded to bf16 here), for every B.
+ * Errors: as sirius_ffn_dense, plus SIRIUS_EINVAL for NaN t or for exactly
+ * one of active_idx / active_cnt being NULL.
+ */
+int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                    const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                    const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Threshold calibration for sirius_ffn_cats: the nearest-rank q-quantile of
+ * the pooled |SiLU(W_gate[i].x_cal[n])| over N calibration inputs and all
+ * d_ff neurons (with the M = N*d_ff values sorted ascending, the value at
+ * rank ceil(q*M)). Dropping values <= t then removes a fraction q on the
+ * calibration set. The paper fixes FSparse sparsity levels (50% by
+ * default, Sec. 3) without printing how CATS sets its threshold; this is
+ * the plain quantile rule.
+ *   x_cal [N, d_model] fp32; t_out: ONE float in device memory. q is a double
+ *   so that ceil(q*M) is the exact nearest rank (a float q such as 0.4f
+ *   would move the rank by one when q*M is an integer).
+ * Errors: SIRIUS_EINVAL for null pointers, N < 1, q outside (0, 1].
+ */
+int sirius_cats_calibrate(const float* x_cal, int N, const uint16_t* w_gate, int d_model,
+                          int d_ff, double q, float* t_out, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/*
+ * Coarse-grained (prompt-fixed) contextual sparsity, CSparse after Griffin
+ * (Sec. 2.1; Appendix A.1): one neuron set per prompt, used for every
+ * generated token, sparsifying the whole MLP including the gate.
+ *   z_ti = SiLU(x_t.W_gate[i]) * (x_t.W_up[i])   over the T prompt tokens
+ *   s_i  = sqrt(sum_t z_ti^2)                     (normalize_tokens = 0)
+ *   s_i  = sqrt(sum_t (z_ti / ||z_t||)^2)          (normalize_tokens = 1)
+ * keeps the k neurons of largest s (equal scores: lower index first) and
+ * copies their rows of all three matrices into the condensed matrices.
+ *   x_prompt [T, d_model] bf16 bits; products are exact and accumulate in
+ *            fp32 on MFMA.
+ *   sel_idx  [k] int32 out, ascending.
+ *   scores   [d_ff] fp32 out (s), or NULL.
+ *   w_*_c    [k, d_model] bf16 out: row j = row sel_idx[j] of w_*.
+ * Errors: SIRIUS_EINVAL for null pointers (scores may be NULL), T < 1,
+ * k < 1 or k > d_ff, d_model/d_ff limits as above.
+ */
+int sirius_griffin_select(const uint16_t* x_prompt, int T, const uint16_t* w_gate,
+                          const uint16_t* w_up, const uint16_t* w_down, int d_model, int d_ff,
+                          int k, int normalize_tokens, int32_t* sel_idx, float* scores,
+                          uint16_t* w_gate_c, uint16_t* w_up_c, uint16_t* w_down_c, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/*
+ * Decode with condensed weights (the CSparse model's FFN): the dense SwiGLU
+ * FFN over the k selected neurons. Same arguments and rules as
+ * sirius_ffn_dense with d_ff = k.
+ */
+int sirius_ffn_condensed(const float* x, int B, const uint16_t* w_gate_c, const uint16_t* w_up_c,
+                         const uint16_t* w_down_c, int d_model, int k, float norm_eps,
+                         const float* resid, float* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Correction check of a drafted chunk (Algorithm 1; Sec. 4 "How to
+ * correct"). Row j of logits is the full model's distribution at drafted
+ * position j (the caller aligns rows to drafted tokens):
+ *   q_bj = softmax(logits[b, j, :] / temperature)[drafted[b, j]]
+ *          (0 when drafted[b, j] is outside [0, V))
+ *   accept_len[b] = first j with q_bj < r (strict), else K
+ *   next_token[b] = argmax_v logits[b, accept_len[b], v]  if accept_len < K
+ *                 = argmax_v logits[b, K, v]              if all accepted and R == K+1
+ *                 = -1                                    otherwise
+ * Argmax is over the raw logits; ties go to the lowest index. The paper
+ * samples the corrected token; the argmax is its deterministic form.
+ *   logits  [B, R, V] fp32, R = K (no bonus row) or K + 1.
+ *   drafted [B, K] int32.
+ *   p_draft [B, K] fp32 out (q), or NULL.
+ * Errors: SIRIUS_EINVAL for null pointers (p_draft may be NULL), K < 1,
+ * V < 1, R not in {K, K+1}, NaN r, temperature not > 0.
+ */
+int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
+                         float r, float temperature, int32_t* accept_len, int32_t* next_token,
+                         float* p_draft, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * RMSNorm with unit weight, the layer-stack glue around the FFN:
+ *   out[b] = h[b] / sqrt(mean(h[b]^2) + eps). out may alias h.
+ * Errors: SIRIUS_EINVAL for null pointers, d_model < 1, eps < 0.
+ */
+int sirius_rmsnorm(const float* h, int B, int d_model, float eps, float* out, void* stream);
+
+/*
+ * Seeded N(mean, std^2) bf16 fill, for building large synthetic weight
+ * stacks directly in HBM. Counter-based (Philox4x32-10, Salmon et al., SC
+ * 2011) with a Box-Muller transform: element e depends only on (seed, e).
+ * Errors: SIRIUS_EINVAL for a null pointer or std < 0.
+ */
+int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, float std,
+                            void* stream);
+
+/*
+ * Per-kernel timing, for measurement. While enabled, every kernel the library
+ * launches is bracketed by a pair of HIP events recorded on the stream the
+ * kernel runs on (a small launch overhead per kernel). sirius_profile_query
+ * waits for the recorded events of one kernel name and returns the summed
+ * duration in milliseconds and the number of launches (0 and 0 for an
+ * unknown name). Kernel names: "cats_gate", "ffn_down", "ffn_reduce",
+ * "ffn_mfma_gate_up", "verify_stats", "verify_scan", "griffin_z",
+ * "griffin_rownorm", "griffin_score", "select_init", "select_hist",
+ * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal".
+ * sirius_profile_reset drops every record (it waits for pending events).
+ * Errors: SIRIUS_EINVAL for NULL arguments, SIRIUS_EHIP if an event fails.
+ */
+int sirius_profile_enable(int on);
+int sirius_profile_reset(void);
+int sirius_profile_query(const char* kernel, double* total_ms, int64_t* launches);
+
+/* Workspace bytes needed by an operation (SIRIUS_OP_*). Arguments:
+ *   FFN_DENSE / FFN_CATS / FFN_CONDENSED: B, d_model, d_ff (= k), unused, unused
+ *   CATS_CALIBRATE: N, d_model, d_ff, unused, unused
+ *   GRIFFIN_SELECT: unused, d_model, d_ff, T, unused
+ *   VERIFY: B, unused, unused, V, R (rows per batch entry)
+ * Returns 0 for an unknown op or invalid sizes. */
+size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, int K_or_R);
+
+/* Message for the calling thread's most recent failure ("" if none). */
+const char* sirius_last_error(void);
+
+/* Library version string. */
+const char* sirius_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SIRIUS_H */

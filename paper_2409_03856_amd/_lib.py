@@ -1,0 +1,306 @@
+"""ctypes binding of libsirius.so (the C ABI declared in include/sirius.h).
+
+Argument marshalling only: every function here checks shapes and dtypes,
+turns torch tensors into device pointers, passes torch's current HIP stream,
+and calls the C entry point of the same name. All computation happens in the
+library's HIP kernels; there is no fallback path. If the library has not been
+built, loading it raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsirius.so")
+
+SIRIUS_OK = 0
+SIRIUS_EINVAL = -1
+SIRIUS_EWORKSPACE = -2
+SIRIUS_EHIP = -3
+
+OP_FFN_DENSE = 0
+OP_FFN_CATS = 1
+OP_GRIFFIN_SELECT = 2
+OP_FFN_CONDENSED = 3
+OP_VERIFY = 4
+OP_CATS_CALIBRATE = 5
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+_Z = ctypes.c_size_t
+
+# name -> (restype, argtypes), in the order of include/sirius.h
+SIGNATURES = {
+    "sirius_ffn_dense": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
+    "sirius_ffn_cats": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "sirius_cats_calibrate": (_I, [_P, _I, _P, _I, _I, ctypes.c_double, _P, _P, _Z, _P]),
+    "sirius_griffin_select": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
+    "sirius_ffn_condensed": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
+    "sirius_verify_accept": (_I, [_P, _I, _I, _I, _I, _P, _F, _F, _P, _P, _P, _P, _Z, _P]),
+    "sirius_rmsnorm": (_I, [_P, _I, _I, _F, _P, _P]),
+    "sirius_fill_normal_bf16": (_I, [_P, _Z, ctypes.c_uint64, _F, _F, _P]),
+    "sirius_profile_enable": (_I, [_I]),
+    "sirius_profile_reset": (_I, []),
+    "sirius_profile_query": (_I, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
+    "sirius_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "sirius_last_error": (ctypes.c_char_p, []),
+    "sirius_version": (ctypes.c_char_p, []),
+}
+
+_lock = threading.Lock()
+_lib = None
+
+
+class SiriusError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libsirius error {code}: {msg}")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsirius.so (built in-tree); raises if it is missing."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    f"{LIB_PATH} is not built; run `python -m paper_2409_03856_amd.build` "
+                    "(there is no CPU fallback)")
+            handle = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in SIGNATURES.items():
+                fn = getattr(handle, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = handle
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != SIRIUS_OK:
+        raise SiriusError(rc, lib().sirius_last_error().decode())
+
+
+# ---------------------------------------------------------------- torch glue
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+def _dev_check(*ts):
+    for t in ts:
+        if t is not None:
+            _need(t.is_cuda, "tensors must live on the GPU")
+            _need(t.is_contiguous(), "tensors must be contiguous")
+
+
+_ws_cache: dict = {}
+
+
+def workspace(op: int, a: int, b: int, c: int, d: int = 0, e: int = 0, device=None):
+    """Device workspace for an operation (cached per device; grows as needed)."""
+    torch = _torch()
+    n = int(lib().sirius_workspace_size(op, a, b, c, d, e))
+    if n == 0:
+        raise ValueError("invalid sizes for the workspace query")
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    key = (dev.index, op)
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < n:
+        buf = torch.empty(n, dtype=torch.uint8, device=dev)
+        _ws_cache[key] = buf
+    return buf
+
+
+def _w_dims(w_gate, w_up, w_down):
+    torch = _torch()
+    for w in (w_gate, w_up, w_down):
+        _need(w.dtype in (torch.bfloat16, torch.int16, torch.uint16), "weights must be bf16 (or 16-bit bits)")
+        _need(w.dim() == 2 and w.shape == w_gate.shape, "weights must share one [d_ff, d_model] shape")
+    return int(w_gate.shape[1]), int(w_gate.shape[0])
+
+
+# ---------------------------------------------------------------- entry points
+
+def sirius_ffn_dense(x, w_gate, w_up, w_down, *, norm_eps=-1.0, resid=None, y=None, ws=None, stream=None):
+    torch = _torch()
+    d, f = _w_dims(w_gate, w_up, w_down)
+    _need(x.dtype == torch.float32 and x.dim() == 2 and x.shape[1] == d, "x must be fp32 [B, d_model]")
+    bsz = int(x.shape[0])
+    if y is None:
+        y = torch.empty_like(x)
+    _dev_check(x, w_gate, w_up, w_down, resid, y)
+    if ws is None:
+        ws = workspace(OP_FFN_DENSE, max(bsz, 1), d, f, device=x.device)
+    _check(lib().sirius_ffn_dense(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f,
+                                  float(norm_eps), _ptr(resid), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+    return y
+
+
+def sirius_ffn_condensed(x, w_gate_c, w_up_c, w_down_c, *, norm_eps=-1.0, resid=None, y=None, ws=None,
+                         stream=None):
+    torch = _torch()
+    d, k = _w_dims(w_gate_c, w_up_c, w_down_c)
+    _need(x.dtype == torch.float32 and x.dim() == 2 and x.shape[1] == d, "x must be fp32 [B, d_model]")
+    bsz = int(x.shape[0])
+    if y is None:
+        y = torch.empty_like(x)
+    _dev_check(x, w_gate_c, w_up_c, w_down_c, resid, y)
+    if ws is None:
+        ws = workspace(OP_FFN_CONDENSED, max(bsz, 1), d, k, device=x.device)
+    _check(lib().sirius_ffn_condensed(_ptr(x), bsz, _ptr(w_gate_c), _ptr(w_up_c), _ptr(w_down_c), d, k,
+                                      float(norm_eps), _ptr(resid), _ptr(y), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return y
+
+
+def sirius_ffn_cats(x, w_gate, w_up, w_down, t, *, norm_eps=-1.0, resid=None, y=None, active_idx=None,
+                    active_cnt=None, want_active=True, ws=None, stream=None):
+    """Returns (y, active_idx [B, d_ff] int32, active_cnt [B] int32); the lists are None when
+    want_active is False and none were passed."""
+    torch = _torch()
+    d, f = _w_dims(w_gate, w_up, w_down)
+    _need(x.dtype == torch.float32 and x.dim() == 2 and x.shape[1] == d, "x must be fp32 [B, d_model]")
+    bsz = int(x.shape[0])
+    if y is None:
+        y = torch.empty_like(x)
+    if want_active and active_idx is None:
+        active_idx = torch.empty((bsz, f), dtype=torch.int32, device=x.device)
+        active_cnt = torch.empty((bsz,), dtype=torch.int32, device=x.device)
+    _dev_check(x, w_gate, w_up, w_down, resid, y, active_idx, active_cnt)
+    if ws is None:
+        ws = workspace(OP_FFN_CATS, max(bsz, 1), d, f, device=x.device)
+    _check(lib().sirius_ffn_cats(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, float(t),
+                                 float(norm_eps), _ptr(resid), _ptr(y), _ptr(active_idx), _ptr(active_cnt),
+                                 _ptr(ws), ws.numel(), _stream(stream)))
+    return y, active_idx, active_cnt
+
+
+def sirius_cats_calibrate(x_cal, w_gate, q, *, t_out=None, ws=None, stream=None):
+    """Returns a 1-element fp32 device tensor holding the threshold."""
+    torch = _torch()
+    f, d = int(w_gate.shape[0]), int(w_gate.shape[1])
+    _need(x_cal.dtype == torch.float32 and x_cal.dim() == 2 and x_cal.shape[1] == d, "x_cal must be fp32 [N, d]")
+    n = int(x_cal.shape[0])
+    if t_out is None:
+        t_out = torch.empty(1, dtype=torch.float32, device=x_cal.device)
+    _dev_check(x_cal, w_gate, t_out)
+    if ws is None:
+        ws = workspace(OP_CATS_CALIBRATE, n, d, f, device=x_cal.device)
+    _check(lib().sirius_cats_calibrate(_ptr(x_cal), n, _ptr(w_gate), d, f, float(q), _ptr(t_out), _ptr(ws),
+                                       ws.numel(), _stream(stream)))
+    return t_out
+
+
+def sirius_griffin_select(x_prompt, w_gate, w_up, w_down, k, *, normalize_tokens=False, sel_idx=None,
+                          scores=None, want_scores=True, w_gate_c=None, w_up_c=None, w_down_c=None, ws=None,
+                          stream=None):
+    """Returns (sel_idx [k] int32, scores [d_ff] fp32 or None, w_gate_c, w_up_c, w_down_c)."""
+    torch = _torch()
+    d, f = _w_dims(w_gate, w_up, w_down)
+    _need(x_prompt.dim() == 2 and x_prompt.shape[1] == d and x_prompt.element_size() == 2,
+          "x_prompt must be bf16 [T, d_model]")
+    t_n = int(x_prompt.shape[0])
+    k = int(k)
+    dev = x_prompt.device
+    if sel_idx is None:
+        sel_idx = torch.empty(k, dtype=torch.int32, device=dev)
+    if want_scores and scores is None:
+        scores = torch.empty(f, dtype=torch.float32, device=dev)
+    if w_gate_c is None:
+        w_gate_c = torch.empty((k, d), dtype=w_gate.dtype, device=dev)
+        w_up_c = torch.empty((k, d), dtype=w_up.dtype, device=dev)
+        w_down_c = torch.empty((k, d), dtype=w_down.dtype, device=dev)
+    _dev_check(x_prompt, w_gate, w_up, w_down, sel_idx, scores, w_gate_c, w_up_c, w_down_c)
+    if ws is None:
+        ws = workspace(OP_GRIFFIN_SELECT, 0, d, f, t_n, device=dev)
+    _check(lib().sirius_griffin_select(_ptr(x_prompt), t_n, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, k,
+                                       1 if normalize_tokens else 0, _ptr(sel_idx), _ptr(scores), _ptr(w_gate_c),
+                                       _ptr(w_up_c), _ptr(w_down_c), _ptr(ws), ws.numel(), _stream(stream)))
+    return sel_idx, scores, w_gate_c, w_up_c, w_down_c
+
+
+def sirius_verify_accept(logits, drafted, r, temperature=1.0, *, accept_len=None, next_token=None,
+                         p_draft=None, want_p=True, ws=None, stream=None):
+    """logits [B, R, V] fp32 (R = K or K + 1), drafted [B, K] int32.
+    Returns (accept_len [B] int32, next_token [B] int32, p_draft [B, K] fp32 or None)."""
+    torch = _torch()
+    _need(logits.dtype == torch.float32 and logits.dim() == 3, "logits must be fp32 [B, R, V]")
+    _need(drafted.dtype == torch.int32 and drafted.dim() == 2 and drafted.shape[0] == logits.shape[0],
+          "drafted must be int32 [B, K]")
+    bsz, rows, vocab = (int(s) for s in logits.shape)
+    k = int(drafted.shape[1])
+    dev = logits.device
+    if accept_len is None:
+        accept_len = torch.empty(bsz, dtype=torch.int32, device=dev)
+        next_token = torch.empty(bsz, dtype=torch.int32, device=dev)
+    if want_p and p_draft is None:
+        p_draft = torch.empty((bsz, k), dtype=torch.float32, device=dev)
+    _dev_check(logits, drafted, accept_len, next_token, p_draft)
+    if ws is None:
+        ws = workspace(OP_VERIFY, max(bsz, 1), 0, 0, vocab, rows, device=dev)
+    _check(lib().sirius_verify_accept(_ptr(logits), bsz, k, rows, vocab, _ptr(drafted), float(r),
+                                      float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(p_draft),
+                                      _ptr(ws), ws.numel(), _stream(stream)))
+    return accept_len, next_token, p_draft
+
+
+def sirius_rmsnorm(h, eps=1e-5, *, out=None, stream=None):
+    torch = _torch()
+    _need(h.dtype == torch.float32 and h.dim() == 2, "h must be fp32 [B, d_model]")
+    if out is None:
+        out = torch.empty_like(h)
+    _dev_check(h, out)
+    _check(lib().sirius_rmsnorm(_ptr(h), int(h.shape[0]), int(h.shape[1]), float(eps), _ptr(out), _stream(stream)))
+    return out
+
+
+def sirius_fill_normal_bf16(out, seed, mean=0.0, std=1.0, *, stream=None):
+    _dev_check(out)
+    _need(out.element_size() == 2, "out must be a 16-bit (bf16) tensor")
+    _check(lib().sirius_fill_normal_bf16(_ptr(out), out.numel(), int(seed) & 0xFFFFFFFFFFFFFFFF, float(mean),
+                                         float(std), _stream(stream)))
+    return out
+
+
+def sirius_profile_enable(on: bool = True) -> None:
+    _check(lib().sirius_profile_enable(1 if on else 0))
+
+
+def sirius_profile_reset() -> None:
+    _check(lib().sirius_profile_reset())
+
+
+def sirius_profile_query(kernel: str):
+    """(total milliseconds, launches) recorded for one kernel name since the last reset."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(lib().sirius_profile_query(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, int(n.value)
+
+
+def sirius_workspace_size(op, a, b, c, d=0, e=0):
+    return int(lib().sirius_workspace_size(op, a, b, c, d, e))
+
+
+def sirius_version() -> str:
+    return lib().sirius_version().decode()

@@ -1,0 +1,270 @@
+// C ABI of libsirius: host-side argument validation, workspace checks and dispatch to the
+// gfx950 kernels. Nothing is enqueued unless every argument check passes.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/sirius.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return SIRIUS_OK;
+  return fail(SIRIUS_EHIP, "%s: HIP error %d (%s)", what, (int)e, hipGetErrorString(e));
+}
+
+constexpr int kMaxDModel = 8192;
+constexpr int kMaxDFF = 65536;
+constexpr int kMaxBatch = 64;
+constexpr int kMaxVerifyRows = 1024;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_ffn_dims(const char* fn, int B, int d_model, int d_ff) {
+  if (B < 0 || B > kMaxBatch) return fail(SIRIUS_EINVAL, "%s: B=%d outside [0, %d]", fn, B, kMaxBatch);
+  if (d_model < 8 || d_model > kMaxDModel || (d_model % 8) != 0)
+    return fail(SIRIUS_EINVAL, "%s: d_model=%d must be a multiple of 8 in [8, %d]", fn, d_model, kMaxDModel);
+  if (d_ff < 1 || d_ff > kMaxDFF)
+    return fail(SIRIUS_EINVAL, "%s: d_ff=%d outside [1, %d]", fn, d_ff, kMaxDFF);
+  return SIRIUS_OK;
+}
+
+int check_ptrs(const char* fn, std::initializer_list<std::pair<const void*, const char*>> ptrs) {
+  for (auto& p : ptrs) {
+    if (p.first == nullptr) return fail(SIRIUS_EINVAL, "%s: %s is NULL", fn, p.second);
+    if (!aligned16(p.first)) return fail(SIRIUS_EINVAL, "%s: %s is not 16-byte aligned", fn, p.second);
+  }
+  return SIRIUS_OK;
+}
+
+bool dims_ok(int d_model, int d_ff) {
+  return d_model >= 8 && d_model <= kMaxDModel && (d_model % 8) == 0 && d_ff >= 1 && d_ff <= kMaxDFF;
+}
+
+size_t ffn_ws(int B, int d, int F) {
+  if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
+  return sirius::gemv_layout(std::max(B, 1), d, F).total;
+}
+
+// Dense / condensed / sparse FFN through the small-batch kernels, batch in LDS-sized chunks.
+int run_ffn_gemv(const char* fn, const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                 const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                 const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
+                 hipStream_t s) {
+  const sirius::GemvLayout L = sirius::gemv_layout(B, d, F);
+  for (int b0 = 0; b0 < B; b0 += L.bc) {
+    const int nb = std::min(L.bc, B - b0);
+    hipError_t e = sirius::launch_ffn_gemv(
+        x + (size_t)b0 * d, nb, wg, wu, wd, d, F, mode, t, norm_eps,
+        resid ? resid + (size_t)b0 * d : nullptr, y + (size_t)b0 * d,
+        active_idx ? active_idx + (size_t)b0 * F : nullptr, active_cnt ? active_cnt + b0 : nullptr,
+        static_cast<char*>(ws), L, s);
+    if (e != hipSuccess) return hip_status(e, fn);
+  }
+  return SIRIUS_OK;
+}
+
+int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                   const uint16_t* wd, int d, int F, float norm_eps, const float* resid, float* y,
+                   void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_ffn_dims(fn, B, d, F);
+  if (rc) return rc;
+  if ((rc = check_ptrs(fn, {{x, "x"}, {wg, "w_gate"}, {wu, "w_up"}, {wd, "w_down"}, {y, "y"}, {ws, "ws"}})))
+    return rc;
+  if (resid != nullptr && !aligned16(resid)) return fail(SIRIUS_EINVAL, "%s: resid is not 16-byte aligned", fn);
+  if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
+  if (B == 0) return SIRIUS_OK;
+  const size_t need = ffn_ws(B, d, F);
+  if (ws_bytes < need)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (B >= sirius::kMfmaMinBatch) {
+    const sirius::MfmaLayout L = sirius::mfma_layout(B, d, F);
+    return hip_status(sirius::launch_ffn_mfma(x, B, wg, wu, wd, d, F, norm_eps, resid, y,
+                                              static_cast<char*>(ws), L, s),
+                      fn);
+  }
+  return run_ffn_gemv(fn, x, B, wg, wu, wd, d, F, /*mode=*/0, 0.f, norm_eps, resid, y, nullptr,
+                      nullptr, ws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sirius_last_error(void) { return g_last_error.c_str(); }
+
+const char* sirius_version(void) { return "sirius-mi355x 0.1 (gfx950)"; }
+
+size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, int K_or_R) {
+  switch (op) {
+    case SIRIUS_OP_FFN_DENSE:
+    case SIRIUS_OP_FFN_CONDENSED:
+      if (B < 0 || B > kMaxBatch || !dims_ok(d_model, d_ff)) return 0;
+      return ffn_ws(B, d_model, d_ff);
+    case SIRIUS_OP_FFN_CATS:
+      if (B < 0 || B > kMaxBatch || !dims_ok(d_model, d_ff)) return 0;
+      return sirius::gemv_layout(std::max(B, 1), d_model, d_ff).total;
+    case SIRIUS_OP_CATS_CALIBRATE:
+      if (B < 1 || !dims_ok(d_model, d_ff)) return 0;
+      return (((size_t)B * d_ff * sizeof(float) + 255) & ~size_t(255)) + sirius::select_ws_bytes();
+    case SIRIUS_OP_GRIFFIN_SELECT:
+      if (T_or_V < 1 || !dims_ok(d_model, d_ff)) return 0;
+      return sirius::griffin_layout(T_or_V, d_model, d_ff).total;
+    case SIRIUS_OP_VERIFY:
+      if (B < 0 || T_or_V < 1 || K_or_R < 1 || K_or_R > kMaxVerifyRows) return 0;
+      return sirius::verify_layout(std::max(B, 1), K_or_R, T_or_V).total;
+    default:
+      return 0;
+  }
+}
+
+int sirius_ffn_dense(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                     const uint16_t* w_down, int d_model, int d_ff, float norm_eps,
+                     const float* resid, float* y, void* ws, size_t ws_bytes, void* stream) {
+  return ffn_dense_impl("sirius_ffn_dense", x, B, w_gate, w_up, w_down, d_model, d_ff, norm_eps,
+                        resid, y, ws, ws_bytes, stream);
+}
+
+int sirius_ffn_condensed(const float* x, int B, const uint16_t* w_gate_c, const uint16_t* w_up_c,
+                         const uint16_t* w_down_c, int d_model, int k, float norm_eps,
+                         const float* resid, float* y, void* ws, size_t ws_bytes, void* stream) {
+  return ffn_dense_impl("sirius_ffn_condensed", x, B, w_gate_c, w_up_c, w_down_c, d_model, k,
+                        norm_eps, resid, y, ws, ws_bytes, stream);
+}
+
+int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                    const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                    const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                    void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_ffn_cats";
+  int rc = check_ffn_dims(fn, B, d_model, d_ff);
+  if (rc) return rc;
+  if ((rc = check_ptrs(fn, {{x, "x"}, {w_gate, "w_gate"}, {w_up, "w_up"}, {w_down, "w_down"}, {y, "y"}, {ws, "ws"}})))
+    return rc;
+  if (resid != nullptr && !aligned16(resid)) return fail(SIRIUS_EINVAL, "%s: resid is not 16-byte aligned", fn);
+  if ((active_idx == nullptr) != (active_cnt == nullptr))
+    return fail(SIRIUS_EINVAL, "%s: active_idx and active_cnt must both be given or both be NULL", fn);
+  if (std::isnan(t)) return fail(SIRIUS_EINVAL, "%s: threshold t is NaN", fn);
+  if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
+  if (B == 0) return SIRIUS_OK;
+  const size_t need = sirius::gemv_layout(B, d_model, d_ff).total;
+  if (ws_bytes < need)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, /*mode=*/1, t, norm_eps, resid,
+                      y, active_idx, active_cnt, ws, static_cast<hipStream_t>(stream));
+}
+
+int sirius_cats_calibrate(const float* x_cal, int N, const uint16_t* w_gate, int d_model, int d_ff,
+                          double q, float* t_out, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_cats_calibrate";
+  if (N < 1) return fail(SIRIUS_EINVAL, "%s: N=%d must be >= 1", fn, N);
+  int rc = check_ffn_dims(fn, 1, d_model, d_ff);
+  if (rc) return rc;
+  if ((rc = check_ptrs(fn, {{x_cal, "x_cal"}, {w_gate, "w_gate"}, {ws, "ws"}}))) return rc;
+  if (t_out == nullptr) return fail(SIRIUS_EINVAL, "%s: t_out is NULL", fn);
+  if (!(q > 0.0 && q <= 1.0)) return fail(SIRIUS_EINVAL, "%s: q=%g outside (0, 1]", fn, q);
+  const size_t M = (size_t)N * d_ff;
+  if (M > (size_t)INT32_MAX) return fail(SIRIUS_EINVAL, "%s: N*d_ff too large", fn);
+  const size_t need = sirius_workspace_size(SIRIUS_OP_CATS_CALIBRATE, N, d_model, d_ff, 0, 0);
+  if (ws_bytes < need)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  // nearest rank r = ceil(q*M) (1-based, ascending) == the (M - r + 1)-th largest
+  long long r = (long long)std::ceil(q * (double)M);
+  r = std::min<long long>(std::max<long long>(r, 1), (long long)M);
+  const int k = (int)((long long)M - r + 1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* absact = static_cast<float*>(ws);
+  char* sel_ws = static_cast<char*>(ws) + ((M * sizeof(float) + 255) & ~size_t(255));
+  hipError_t e = sirius::launch_gate_absact(x_cal, N, w_gate, d_model, d_ff, absact, s);
+  if (e != hipSuccess) return hip_status(e, fn);
+  return hip_status(sirius::launch_select_kth_largest(absact, (int)M, k, t_out, sel_ws, s), fn);
+}
+
+int sirius_griffin_select(const uint16_t* x_prompt, int T, const uint16_t* w_gate,
+                          const uint16_t* w_up, const uint16_t* w_down, int d_model, int d_ff,
+                          int k, int normalize_tokens, int32_t* sel_idx, float* scores,
+                          uint16_t* w_gate_c, uint16_t* w_up_c, uint16_t* w_down_c, void* ws,
+                          size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_griffin_select";
+  if (T < 1) return fail(SIRIUS_EINVAL, "%s: T=%d must be >= 1", fn, T);
+  int rc = check_ffn_dims(fn, 1, d_model, d_ff);
+  if (rc) return rc;
+  if (k < 1 || k > d_ff) return fail(SIRIUS_EINVAL, "%s: k=%d outside [1, d_ff=%d]", fn, k, d_ff);
+  if ((rc = check_ptrs(fn, {{x_prompt, "x_prompt"}, {w_gate, "w_gate"}, {w_up, "w_up"}, {w_down, "w_down"},
+                            {sel_idx, "sel_idx"}, {w_gate_c, "w_gate_c"}, {w_up_c, "w_up_c"},
+                            {w_down_c, "w_down_c"}, {ws, "ws"}})))
+    return rc;
+  if ((size_t)T * d_ff > (size_t)INT32_MAX) return fail(SIRIUS_EINVAL, "%s: T*d_ff too large", fn);
+  const sirius::GriffinLayout L = sirius::griffin_layout(T, d_model, d_ff);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_griffin(x_prompt, T, w_gate, w_up, w_down, d_model, d_ff, k,
+                                           normalize_tokens ? 1 : 0, sel_idx, scores, w_gate_c,
+                                           w_up_c, w_down_c, static_cast<char*>(ws), L,
+                                           static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
+                         float r, float temperature, int32_t* accept_len, int32_t* next_token,
+                         float* p_draft, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_verify_accept";
+  if (B < 0) return fail(SIRIUS_EINVAL, "%s: B=%d < 0", fn, B);
+  if (K < 1) return fail(SIRIUS_EINVAL, "%s: K=%d must be >= 1", fn, K);
+  if (R != K && R != K + 1) return fail(SIRIUS_EINVAL, "%s: R=%d must be K or K+1 (K=%d)", fn, R, K);
+  if (R > kMaxVerifyRows) return fail(SIRIUS_EINVAL, "%s: R=%d above %d", fn, R, kMaxVerifyRows);
+  if (V < 1) return fail(SIRIUS_EINVAL, "%s: V=%d must be >= 1", fn, V);
+  if (std::isnan(r)) return fail(SIRIUS_EINVAL, "%s: r is NaN", fn);
+  if (!(temperature > 0.f) || std::isinf(temperature))
+    return fail(SIRIUS_EINVAL, "%s: temperature=%g must be finite and > 0", fn, (double)temperature);
+  if (logits == nullptr || drafted == nullptr || accept_len == nullptr || next_token == nullptr || ws == nullptr)
+    return fail(SIRIUS_EINVAL, "%s: a required pointer is NULL", fn);
+  if (!aligned16(logits)) return fail(SIRIUS_EINVAL, "%s: logits is not 16-byte aligned", fn);
+  if (B == 0) return SIRIUS_OK;
+  if ((size_t)B * R * V > ((size_t)1 << 40)) return fail(SIRIUS_EINVAL, "%s: logits too large", fn);
+  const sirius::VerifyLayout L = sirius::verify_layout(B, R, V);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_verify(logits, B, K, R, V, drafted, r, temperature, accept_len,
+                                          next_token, p_draft, static_cast<char*>(ws), L,
+                                          static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_rmsnorm(const float* h, int B, int d_model, float eps, float* out, void* stream) {
+  const char* fn = "sirius_rmsnorm";
+  if (h == nullptr || out == nullptr) return fail(SIRIUS_EINVAL, "%s: NULL pointer", fn);
+  if (B < 0 || d_model < 1) return fail(SIRIUS_EINVAL, "%s: bad sizes B=%d d_model=%d", fn, B, d_model);
+  if (!(eps >= 0.f)) return fail(SIRIUS_EINVAL, "%s: eps must be >= 0", fn);
+  if (B == 0) return SIRIUS_OK;
+  return hip_status(sirius::launch_rmsnorm(h, B, d_model, eps, out, static_cast<hipStream_t>(stream)), fn);
+}
+
+int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, float std,
+                            void* stream) {
+  const char* fn = "sirius_fill_normal_bf16";
+  if (out == nullptr) return fail(SIRIUS_EINVAL, "%s: out is NULL", fn);
+  if (!(std >= 0.f) || std::isinf(std) || !std::isfinite(mean))
+    return fail(SIRIUS_EINVAL, "%s: need finite mean and std >= 0", fn);
+  if (n == 0) return SIRIUS_OK;
+  return hip_status(sirius::launch_fill_normal_bf16(out, n, seed, mean, std, static_cast<hipStream_t>(stream)), fn);
+}
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// Internal launchers of libsirius (not part of the C ABI). Every launcher
+// only enqueues kernels on `stream`; the C-ABI layer validates arguments
+// before calling any of them.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sirius {
+
+// ---- small-batch FFN (gate GEMV + SiLU + threshold + compaction, sparse down, reduce)
+struct GemvLayout {
+  int bc;       // batch rows handled per pass (x staged in LDS needs bc*d*4 <= 64 KiB)
+  int ntiles;   // gate row tiles
+  int cs, gr;   // down-projection grid: column slices x row ranges
+  size_t uidx, h, ucnt, bidx, bcnt, part, total;  // workspace byte offsets / size
+};
+GemvLayout gemv_layout(int B, int d, int F);
+
+// mode 0: dense (every neuron), 1: threshold sparsity. x/y/resid/active_* already offset
+// to the chunk; B <= layout.bc.
+hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                           const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                           char* ws, const GemvLayout& L, hipStream_t stream);
+
+// Gate activations |SiLU(W_gate x)| for N inputs into absact [N, F] (calibration).
+hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, int F,
+                              float* absact, hipStream_t stream);
+
+// ---- multi-token FFN on MFMA (B >= kMfmaMinBatch)
+constexpr int kMfmaMinBatch = 1 << 20;  // multi-token MFMA path not enabled yet
+struct MfmaLayout {
+  int mpad;     // batch padded to the MFMA M tile
+  int cs, gr;   // down grid
+  size_t xb, h, part, total;
+};
+MfmaLayout mfma_layout(int B, int d, int F);
+hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, int d, int F, float norm_eps, const float* resid,
+                           float* y, char* ws, const MfmaLayout& L, hipStream_t stream);
+
+// ---- radix select of the k-th largest non-negative float (ties resolved by index)
+hipError_t launch_select_kth_largest(const float* v, int n, int k, float* out_value,
+                                     char* ws, hipStream_t stream);
+size_t select_ws_bytes();
+
+// ---- Griffin
+struct GriffinLayout {
+  size_t z, rownorm, select, kth, scores, total;
+};
+GriffinLayout griffin_layout(int T, int d, int F);
+hipError_t launch_griffin(const uint16_t* xp, int T, const uint16_t* wg, const uint16_t* wu,
+                          const uint16_t* wd, int d, int F, int k, int normalize,
+                          int32_t* sel, float* scores_out, uint16_t* wgc, uint16_t* wuc,
+                          uint16_t* wdc, char* ws, const GriffinLayout& L, hipStream_t stream);
+
+// ---- verify
+struct VerifyLayout {
+  int splits;
+  size_t part, total;
+};
+VerifyLayout verify_layout(int B, int R, int V);
+hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
+                         float r, float temperature, int32_t* accept_len, int32_t* next_token,
+                         float* p_draft, char* ws, const VerifyLayout& L, hipStream_t stream);
+
+// ---- glue
+hipError_t launch_rmsnorm(const float* h, int B, int d, float eps, float* out, hipStream_t stream);
+hipError_t launch_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, float std,
+                                   hipStream_t stream);
+
+}  // namespace sirius

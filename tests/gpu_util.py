@@ -1,0 +1,94 @@
+"""Helpers for the GPU parity tests: upload seeded inputs, parity checks against the oracle.
+
+Tolerances (see the design notes for their derivation):
+  * active-neuron sets: bit-exact outside a guard band |(|a| - t)| <= 1e-3;
+  * FFN outputs on the fp32-input paths: max-abs error <= 1e-4 x RMS of the
+    oracle output (fp32 accumulation of bf16 x fp32 products); the stated
+    bound of the method, 2e-2 x RMS, is asserted as well;
+  * FFN outputs on the MFMA path (x and h rounded to bf16): <= 2e-2 x RMS;
+  * acceptance lengths: bit-exact outside a guard band |q - r| <= 1e-5 r.
+"""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+
+FP32_PATH_TOL = 1e-4
+METHOD_TOL = 2e-2
+CATS_BAND = 1e-3
+VERIFY_BAND = 1e-5
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev_bf16(bits: np.ndarray):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.bfloat16).cuda()
+
+
+def dev_f32(a: np.ndarray):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def dev_i32(a: np.ndarray):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+def host(t) -> np.ndarray:
+    import torch
+    torch.cuda.synchronize()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def rel_err(got, want) -> float:
+    want = np.asarray(want, dtype=np.float64)
+    rms = float(np.sqrt(np.mean(want * want)))
+    return float(np.max(np.abs(np.asarray(got, dtype=np.float64) - want))) / max(rms, 1e-300)
+
+
+def check_cats_sets(x_in, wg, t, idx, cnt, band=CATS_BAND):
+    """GPU sets equal the oracle's outside the guard band. Returns (gpu_sets, boundary_count)."""
+    sets_o, a = oracle.cats_active_sets(x_in, wg, t)
+    gpu_sets = []
+    n_boundary = 0
+    for b in range(len(sets_o)):
+        g = idx[b, : int(cnt[b])].astype(np.int64)
+        assert np.all(np.diff(g) > 0), "active list must be strictly ascending"
+        near = np.abs(np.abs(a[b]) - t) <= band
+        n_boundary += int(near.sum())
+        sym = np.setxor1d(g, sets_o[b])
+        assert np.all(near[sym]), f"token {b}: {int((~near[sym]).sum())} set mismatches outside the band"
+        gpu_sets.append(g)
+    return gpu_sets, n_boundary
+
+
+def check_ffn(y_gpu, y_ref, resid=None, tol=FP32_PATH_TOL):
+    y_gpu = np.asarray(y_gpu, dtype=np.float64)
+    if resid is not None:
+        y_gpu = y_gpu - np.asarray(resid, dtype=np.float64)
+    e = rel_err(y_gpu, y_ref)
+    assert e <= METHOD_TOL, f"max-abs error {e:.3e} x RMS exceeds the method bound"
+    assert e <= tol, f"max-abs error {e:.3e} x RMS exceeds {tol:.1e}"
+    return e
+
+
+def verify_boundary_rows(q_oracle, acc_oracle, r, band=VERIFY_BAND):
+    """Rows where some q_j (j <= accept_len) lies within the guard band of r."""
+    rows = []
+    for b in range(q_oracle.shape[0]):
+        jmax = min(int(acc_oracle[b]), q_oracle.shape[1] - 1)
+        if np.any(np.abs(q_oracle[b, : jmax + 1] - r) <= band * abs(r)):
+            rows.append(b)
+    return rows

@@ -1,0 +1,152 @@
+"""The C-ABI library loads, exports every entry point of include/sirius.h, and
+rejects bad arguments on the host before touching the GPU (no compute calls here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sirius.h")
+
+pytestmark = pytest.mark.skipif(
+    not os.path.exists(os.path.join(ROOT, "paper_2409_03856_amd", "libsirius.so")),
+    reason="libsirius.so not built (run __graft_entry__.build())")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sirius_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2409_03856_amd import _lib
+    return _lib.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_binding_covers_the_header():
+    from paper_2409_03856_amd import _lib
+    assert sorted(_lib.SIGNATURES) == _declared()
+
+
+def test_version_and_empty_error(L):
+    assert b"gfx950" in L.sirius_version()
+
+
+FAKE = ctypes.c_void_p(1 << 20)  # non-null, 16-byte aligned; never dereferenced by these calls
+
+
+def _err(L):
+    return L.sirius_last_error().decode()
+
+
+def test_ffn_argument_errors(L):
+    big = 1 << 30
+    # d_model not a multiple of 8
+    rc = L.sirius_ffn_dense(FAKE, 1, FAKE, FAKE, FAKE, 100, 64, -1.0, None, FAKE, FAKE, big, None)
+    assert rc == -1 and "d_model" in _err(L)
+    # d_model above the limit, d_ff zero, negative batch, batch above the limit
+    assert L.sirius_ffn_dense(FAKE, 1, FAKE, FAKE, FAKE, 16384, 64, -1.0, None, FAKE, FAKE, big, None) == -1
+    assert L.sirius_ffn_dense(FAKE, 1, FAKE, FAKE, FAKE, 64, 0, -1.0, None, FAKE, FAKE, big, None) == -1
+    assert L.sirius_ffn_dense(FAKE, -1, FAKE, FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE, big, None) == -1
+    assert L.sirius_ffn_dense(FAKE, 65, FAKE, FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE, big, None) == -1
+    # null and misaligned pointers
+    rc = L.sirius_ffn_dense(None, 1, FAKE, FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE, big, None)
+    assert rc == -1 and "x is NULL" in _err(L)
+    rc = L.sirius_ffn_dense(FAKE, 1, ctypes.c_void_p((1 << 20) + 2), FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE,
+                            big, None)
+    assert rc == -1 and "aligned" in _err(L)
+    # workspace too small
+    rc = L.sirius_ffn_dense(FAKE, 1, FAKE, FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE, 16, None)
+    assert rc == -2 and "workspace" in _err(L)
+    # an empty batch is a no-op
+    assert L.sirius_ffn_dense(FAKE, 0, FAKE, FAKE, FAKE, 64, 64, -1.0, None, FAKE, FAKE, 0, None) == 0
+
+
+def test_cats_argument_errors(L):
+    big = 1 << 30
+    nan = float("nan")
+    rc = L.sirius_ffn_cats(FAKE, 1, FAKE, FAKE, FAKE, 64, 64, nan, -1.0, None, FAKE, FAKE, FAKE, FAKE, big, None)
+    assert rc == -1 and "NaN" in _err(L)
+    rc = L.sirius_ffn_cats(FAKE, 1, FAKE, FAKE, FAKE, 64, 64, 0.1, -1.0, None, FAKE, FAKE, None, FAKE, big, None)
+    assert rc == -1 and "active_idx" in _err(L)
+    rc = L.sirius_ffn_cats(FAKE, 1, FAKE, FAKE, FAKE, 64, 64, 0.1, -1.0, None, FAKE, None, None, FAKE, 8, None)
+    assert rc == -2
+    assert L.sirius_ffn_cats(FAKE, 0, FAKE, FAKE, FAKE, 64, 64, 0.1, -1.0, None, FAKE, None, None, FAKE, 0, None) == 0
+    rc = L.sirius_cats_calibrate(FAKE, 4, FAKE, 64, 64, 0.0, FAKE, FAKE, big, None)
+    assert rc == -1 and "q=" in _err(L)
+    rc = L.sirius_cats_calibrate(FAKE, 0, FAKE, 64, 64, 0.5, FAKE, FAKE, big, None)
+    assert rc == -1
+
+
+def test_griffin_argument_errors(L):
+    big = 1 << 30
+    args = [FAKE, 8, FAKE, FAKE, FAKE, 64, 100, 50, 0, FAKE, None, FAKE, FAKE, FAKE, FAKE, big, None]
+    bad_k = list(args)
+    bad_k[7] = 101
+    assert L.sirius_griffin_select(*bad_k) == -1 and "k=" in _err(L)
+    bad_k[7] = 0
+    assert L.sirius_griffin_select(*bad_k) == -1
+    bad_t = list(args)
+    bad_t[1] = 0
+    assert L.sirius_griffin_select(*bad_t) == -1
+    small = list(args)
+    small[15] = 64
+    assert L.sirius_griffin_select(*small) == -2
+
+
+def test_verify_argument_errors(L):
+    big = 1 << 30
+    nan = float("nan")
+    base = [FAKE, 2, 4, 4, 100, FAKE, 0.1, 1.0, FAKE, FAKE, None, FAKE, big, None]
+
+    def call(**kw):
+        a = list(base)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.sirius_verify_accept(*a)
+
+    assert call(a2=0) == -1            # K < 1
+    assert call(a3=6) == -1            # R not in {K, K+1}
+    assert call(a4=0) == -1            # V < 1
+    assert call(a6=nan) == -1          # NaN r
+    assert call(a7=0.0) == -1          # temperature 0
+    assert call(a7=-1.0) == -1
+    assert call(a7=float("inf")) == -1
+    assert call(a5=None) == -1         # drafted NULL
+    assert call(a12=16) == -2          # workspace too small
+    assert call(a1=0) == 0             # empty batch
+
+
+def test_glue_argument_errors(L):
+    assert L.sirius_rmsnorm(None, 1, 64, 1e-5, FAKE, None) == -1
+    assert L.sirius_rmsnorm(FAKE, 1, 64, -1.0, FAKE, None) == -1
+    assert L.sirius_rmsnorm(FAKE, 0, 64, 1e-5, FAKE, None) == 0
+    assert L.sirius_fill_normal_bf16(None, 10, 1, 0.0, 1.0, None) == -1
+    assert L.sirius_fill_normal_bf16(FAKE, 10, 1, 0.0, -1.0, None) == -1
+    assert L.sirius_fill_normal_bf16(FAKE, 0, 1, 0.0, 1.0, None) == 0
+
+
+def test_workspace_sizes(L):
+    f = L.sirius_workspace_size
+    assert f(99, 1, 64, 64, 0, 0) == 0
+    assert f(0, 1, 100, 64, 0, 0) == 0
+    s1 = f(1, 1, 4096, 14336, 0, 0)
+    s4 = f(1, 4, 4096, 14336, 0, 0)
+    assert 0 < s1 < s4 < (64 << 20)
+    assert f(4, 8, 0, 0, 128256, 16) > 0
+    assert f(4, 8, 0, 0, 128256, 2000) == 0
+    g = f(2, 0, 4096, 14336, 512, 0)
+    assert g >= 512 * 14336 * 4
+    c = f(5, 256, 4096, 14336, 0, 0)
+    assert c >= 256 * 14336 * 4
