@@ -7,7 +7,7 @@
 #include <cstdio>
 #include <string>
 
-#include "../../include/sirius.h"
+#include "sirius.h"
 #include "kernels.h"
 
 namespace {
@@ -57,9 +57,11 @@ bool dims_ok(int d_model, int d_ff) {
   return d_model >= 8 && d_model <= kMaxDModel && (d_model % 8) == 0 && d_ff >= 1 && d_ff <= kMaxDFF;
 }
 
+size_t gemv_ws(int B, int d, int F) { return sirius::gemv_layout(std::max(B, 1), d, F).total; }
+
 size_t ffn_ws(int B, int d, int F) {
   if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
-  return sirius::gemv_layout(std::max(B, 1), d, F).total;
+  return gemv_ws(B, d, F);
 }
 
 // Dense / condensed / sparse FFN through the small-batch kernels, batch in LDS-sized chunks.
@@ -120,7 +122,7 @@ size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, i
       return ffn_ws(B, d_model, d_ff);
     case SIRIUS_OP_FFN_CATS:
       if (B < 0 || B > kMaxBatch || !dims_ok(d_model, d_ff)) return 0;
-      return sirius::gemv_layout(std::max(B, 1), d_model, d_ff).total;
+      return gemv_ws(B, d_model, d_ff);
     case SIRIUS_OP_CATS_CALIBRATE:
       if (B < 1 || !dims_ok(d_model, d_ff)) return 0;
       return (((size_t)B * d_ff * sizeof(float) + 255) & ~size_t(255)) + sirius::select_ws_bytes();
@@ -164,7 +166,7 @@ int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_
   if (std::isnan(t)) return fail(SIRIUS_EINVAL, "%s: threshold t is NaN", fn);
   if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
   if (B == 0) return SIRIUS_OK;
-  const size_t need = sirius::gemv_layout(B, d_model, d_ff).total;
+  const size_t need = gemv_ws(B, d_model, d_ff);
   if (ws_bytes < need)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
   return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, /*mode=*/1, t, norm_eps, resid,

@@ -49,6 +49,23 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* s_tmp, int* 
   return off + incl - v;
 }
 
+// Last-arrival detection without waiting: an epoch-tagged arrival counter in the caller's
+// workspace. The 64-bit word holds (epoch << 16) | count. A workgroup arriving with a
+// word of another epoch (stale contents from an earlier call, or never written) restarts
+// the count at 1, so the workspace needs no initialisation; the epoch is unique per
+// launch. Returns this workgroup's arrival index (0-based). Nobody spins: only the last
+// arrival (index n-1) does extra work, after an acquire fence.
+__device__ __forceinline__ int arrive_count(unsigned long long* ctr, unsigned long long tag) {
+  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (;;) {
+    const bool same = (old & ~0xFFFFull) == tag;
+    const unsigned long long want = same ? old + 1ull : tag + 1ull;
+    if (__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_ACQ_REL, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      return same ? (int)(old & 0xFFFFull) : 0;
+  }
+}
+
 // Byte offsets inside a caller workspace: every region starts 256-byte aligned.
 struct Carve {
   size_t off = 0;

