@@ -43,6 +43,7 @@ constexpr int kDownUnroll = 16;             // full-row chunks in flight per dow
 constexpr int kRangeCap = 1024;             // kept rows resolved per pass in down_kernel
 constexpr int kDownBlocks = 512;            // target workgroups of down_kernel
 constexpr int kListBlocks = 16;             // workgroups copying each token's active list
+constexpr int kMaxSegs = 4096;              // row segments a down launch can take (d_ff / 16)
 constexpr int kXLdsFloats = 32768;          // fp32 x staged in LDS: 128 KiB (LDS is 160 KiB)
 
 constexpr int kModeDense = 0, kModeSparse = 1, kModeAbsAct = 2;
@@ -243,9 +244,9 @@ __global__ __launch_bounds__(256) void gate_kernel(
 template <int BM>
 __global__ __launch_bounds__(256) void down_kernel(
     const uint4* __restrict__ wd, int d, int B, const int32_t* __restrict__ uidx,
-    const float* __restrict__ hbuf, const int32_t* __restrict__ ucnt, int ntiles, int rmax, int gr,
-    float* __restrict__ part) {
-  __shared__ int s_pref[kGateSegs + 1];
+    const float* __restrict__ hbuf, int hstride, const int32_t* __restrict__ ucnt, int ntiles,
+    int rmax, int gr, float* __restrict__ part) {
+  __shared__ int s_pref[kMaxSegs + 1];
   __shared__ int s_row[kRangeCap];
   __shared__ float s_h[kRangeCap * BM];
   __shared__ float4 s_red[kDownWaves][kWave * 2];
@@ -311,7 +312,7 @@ __global__ __launch_bounds__(256) void down_kernel(
         pv[u] = ok ? p - base : -1;
         rv[u] = ok ? uidx[slot] : 0;
 #pragma unroll
-        for (int b = 0; b < BM; ++b) hv[u][b] = (ok && b < B) ? hbuf[slot * B + b] : 0.f;
+        for (int b = 0; b < BM; ++b) hv[u][b] = (ok && b < B) ? hbuf[slot * hstride + b] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -567,33 +568,50 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
   if (e != hipSuccess) return e;
 
   float* part = reinterpret_cast<float*>(ws + L.part);
-  const dim3 dgrid(L.cs, L.gr);
-  const uint4* wd4 = reinterpret_cast<const uint4*>(wd);
   {
     ProfScope prof(mode == kModeSparse ? "cats_down" : "dense_down", stream);
-#define SIRIUS_DOWN(BMV)                                                                           \
-  case BMV:                                                                                        \
-    down_kernel<BMV><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, ucnt, L.ntiles, L.rmax,     \
-                                                L.gr, part);                                       \
-    break;
-    switch (bm) {
-      SIRIUS_DOWN(1)
-      SIRIUS_DOWN(2)
-      SIRIUS_DOWN(4)
-      SIRIUS_DOWN(8)
-      default:
-        return hipErrorInvalidValue;
-    }
-#undef SIRIUS_DOWN
+    if ((e = launch_down(B, d, L.ntiles, L.rmax, L.gr, wd, uidx, hbuf, B, ucnt, part, stream)) !=
+        hipSuccess)
+      return e;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-
   const int n = B * d;
   const int nred = ceil_div(n, 4 * kWave);
   ProfScope prof(mode == kModeSparse ? "cats_reduce" : "dense_reduce", stream);
-  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(part, L.gr, n, resid, y, nred, B, F,
-                                                             L.ntiles, L.rmax, bidx, bcnt,
-                                                             active_idx, active_cnt);
+  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
+      part, L.gr, n, resid, y, nred, B, F, L.ntiles, L.rmax, bidx, bcnt, active_idx, active_cnt);
+  return hipGetLastError();
+}
+
+hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t* wd,
+                       const int32_t* uidx, const float* hbuf, int hstride, const int32_t* ucnt,
+                       float* part, hipStream_t stream) {
+  if (B < 1 || B > 16 || nseg > kMaxSegs) return hipErrorInvalidValue;
+  const dim3 dgrid(ceil_div(d / 8, kWave), gr);
+  const uint4* wd4 = reinterpret_cast<const uint4*>(wd);
+#define SIRIUS_DOWN(BMV)                                                                     \
+  case BMV:                                                                                  \
+    down_kernel<BMV><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, hstride, ucnt, nseg, \
+                                                rmax, gr, part);                             \
+    break;
+  switch (pow2_at_least(B, 16)) {
+    SIRIUS_DOWN(1)
+    SIRIUS_DOWN(2)
+    SIRIUS_DOWN(4)
+    SIRIUS_DOWN(8)
+    SIRIUS_DOWN(16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef SIRIUS_DOWN
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* resid, float* y,
+                         hipStream_t stream) {
+  const int n = B * d;
+  const int nred = ceil_div(n, 4 * kWave);
+  reduce_kernel<<<nred, 256, 0, stream>>>(part, gr, n, resid, y, nred, B, 0, 0, 0, nullptr,
+                                          nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 

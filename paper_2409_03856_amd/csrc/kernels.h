@@ -30,12 +30,23 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
 hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, int F,
                               float* absact, hipStream_t stream);
 
+// Row-split down projection over compacted neuron lists: nseg segments of up to rmax rows
+// (uidx[seg*rmax + k], count ucnt[seg]), h values at hbuf[slot*hstride + b] for b < B <= 16,
+// partial sums into part[gr][B][d].
+hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t* wd,
+                       const int32_t* uidx, const float* hbuf, int hstride, const int32_t* ucnt,
+                       float* part, hipStream_t stream);
+// y[b] = sum_r part[r][b] (+ resid[b]) in a fixed order.
+hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* resid, float* y,
+                         hipStream_t stream);
+
 // ---- multi-token FFN on MFMA (B >= kMfmaMinBatch)
-constexpr int kMfmaMinBatch = 1 << 20;  // multi-token MFMA path not enabled yet
+constexpr int kMfmaMinBatch = 8;
 struct MfmaLayout {
   int mpad;     // batch padded to the MFMA M tile
+  int ntiles;   // neuron tiles of 16
   int cs, gr;   // down grid
-  size_t xb, h, part, total;
+  size_t xn, uidx, h, ucnt, part, total;  // workspace byte offsets / size
 };
 MfmaLayout mfma_layout(int B, int d, int F);
 hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint16_t* wu,

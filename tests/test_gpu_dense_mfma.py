@@ -1,0 +1,106 @@
+"""GPU parity: the multi-token dense FFN (batch >= 8, gate/up products on MFMA) vs the fp64 oracle.
+
+This path is the full model's parallel pass over a drafted chunk (the chunk of
+tokens the full model checks at once). The gate and up products take the
+normalised input rounded to bf16, so the precision-matched reference is the
+oracle's dense FFN on that rounded input: the MFMA products are exact and
+accumulate in fp32, and h and the down product are fp32, so the fp32-path
+tolerance applies to it. Against the unrounded input the stated bound of the
+method holds as well.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import ffn_weights, decode_inputs, griffin_prompt, bf16_bits, TINY, LLAMA3_8B
+from gpu_util import say, dev_bf16, dev_f32, host, check_ffn, rel_err, FP32_PATH_TOL, METHOD_TOL
+
+pytestmark = pytest.mark.gpu
+
+# With RMSNorm the GPU rounds its fp32 normalised input to bf16; where that fp32 value and the
+# fp64 one straddle a bf16 rounding boundary the two roundings differ by one bf16 ulp (2^-8
+# relative) in that element, which moves a gate/up sum by ~2^-8 / sqrt(d) of its size.
+NORM_ROUNDING_TOL = 5e-4
+
+
+@pytest.fixture(scope="module")
+def sr():
+    import paper_2409_03856_amd as sr
+    sr.lib()
+    return sr
+
+
+def _layer(seed, d, f, std):
+    wg, wu, wd = ffn_weights(seed, d, f, std)
+    return (wg, wu, wd), tuple(dev_bf16(w) for w in (wg, wu, wd))
+
+
+def _rounded(x):
+    return oracle.widen_bf16(bf16_bits(np.asarray(x, dtype=np.float32)))
+
+
+@pytest.mark.parametrize("d,f,bsz", [(256, 688, 8), (264, 1000, 9), (256, 688, 16), (512, 97, 17),
+                                     (4096, 40, 33), (8, 1, 8), (264, 1000, 64), (520, 33, 48)])
+def test_ragged_batches(sr, d, f, bsz):
+    say(f"dense mfma d={d} f={f} B={bsz}")
+    (wg, wu, wd), W = _layer(500 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
+    x = decode_inputs(40 + bsz, bsz, d)
+    y = host(sr.sirius_ffn_dense(dev_f32(x), *W))
+    check_ffn(y, oracle.ffn_dense(_rounded(x), wg, wu, wd), tol=FP32_PATH_TOL)
+    e = rel_err(y, oracle.ffn_dense(x, wg, wu, wd))
+    say(f"  error vs unrounded input: {e:.2e} x RMS")
+    assert e <= METHOD_TOL
+
+
+@pytest.mark.parametrize("bsz", [8, 24])
+def test_norm_and_residual(sr, bsz):
+    d, f = 264, 1000
+    say(f"dense mfma norm+resid B={bsz}")
+    (wg, wu, wd), W = _layer(600 + bsz, d, f, 1.0 / np.sqrt(d))
+    x = decode_inputs(60 + bsz, bsz, d) * 3.0
+    res = decode_inputs(61 + bsz, bsz, d)
+    y = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res)))
+    xn = oracle.rmsnorm(x, 1e-5)
+    check_ffn(y, oracle.ffn_dense(_rounded(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
+    assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
+
+
+def test_run_twice_bitwise_and_in_place(sr):
+    import torch
+    d, f, bsz = TINY.d_model, TINY.d_ff, 16
+    (wg, wu, wd), W = _layer(700, d, f, TINY.weight_std)
+    x = decode_inputs(700, bsz, d)
+    a = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(x)))
+    b = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(x)))
+    assert np.array_equal(a, b)
+    h = dev_f32(x)
+    sr.sirius_ffn_dense(h, *W, norm_eps=1e-5, resid=h, y=h)  # residual layer in place
+    torch.cuda.synchronize()
+    assert np.array_equal(host(h), a)
+
+
+def test_condensed_batch(sr):
+    """Condensed decode of 12 tokens equals the FFN restricted to the selected neurons."""
+    d, f, k, bsz = 256, 688, 300, 12
+    say(f"condensed mfma B={bsz}")
+    (wg, wu, wd), W = _layer(800, d, f, TINY.weight_std)
+    sel, _, wgc, wuc, wdc = sr.sirius_griffin_select(dev_bf16(griffin_prompt(800, 32, d)), *W, k)
+    sel = host(sel).astype(np.int64)
+    x = decode_inputs(800, bsz, d)
+    y = host(sr.sirius_ffn_condensed(dev_f32(x), wgc, wuc, wdc))
+    check_ffn(y, oracle.ffn_masked(_rounded(x), wg, wu, wd, [sel] * bsz), tol=FP32_PATH_TOL)
+
+
+def test_llama3_8b_verify_chunk(sr):
+    """The full model's 16-token pass over one Llama-3-8B-shaped FFN layer."""
+    d, f, bsz = LLAMA3_8B.d_model, LLAMA3_8B.d_ff, 16
+    say("8B dense mfma B=16")
+    (wg, wu, wd), W = _layer(900, d, f, LLAMA3_8B.weight_std)
+    x = decode_inputs(900, bsz, d)
+    res = decode_inputs(901, bsz, d)
+    y = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res)))
+    xn = oracle.rmsnorm(x, 1e-5)
+    e = check_ffn(y, oracle.ffn_dense(_rounded(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
+    say(f"  error vs precision-matched oracle: {e:.2e} x RMS")
+    assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
