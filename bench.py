@@ -1,6 +1,6 @@
 """Benchmark of the Sirius hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--copy-mib N]
 
 Workload (headline): one Llama-3-8B FFN layer (d_model 4096, d_ff 14336, bf16
 neuron-major weights ~ N(0, 0.02)), batch-1 decode with per-token threshold
@@ -22,7 +22,10 @@ The printed value is the sparse FFN decode time per token (rows.cats, from
 row-boundary HIP events in the timed region). The roofline object is for the
 sparse path's dominant kernel (cats_gate: the gate GEMV plus the kept up rows),
 timed by the library's per-kernel HIP events in a second pass of the same K
-steps right after the timed region.
+steps right after the timed region. Its `traffic` is the HBM byte count per
+launch from the committed rocprofv3 counter summary under profiles/, reported
+only while that summary's kernel-source digest matches the current sources
+(`--copy-mib` adds the plain copy whose counters scale FETCH_SIZE/WRITE_SIZE).
 """
 
 from __future__ import annotations
@@ -57,7 +60,40 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--copy-mib", type=int, default=0,
+                   help="after setup, run one plain device-to-device copy of this many MiB (the reference "
+                        "kernel that scales the HBM byte counters)")
     return p.parse_args()
+
+
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "cats_gate_llama3-8b_b1_hbm_counters.md")
+GATE_SOURCES = [os.path.join(ROOT, "paper_2409_03856_amd", "csrc", f) for f in ("ffn_gemv.hip", "common.h")]
+
+
+def gate_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GATE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counted_traffic():
+    """HBM bytes per cats_gate launch from the committed counter summary, or None when that
+    summary is missing or was taken on a different kernel source."""
+    try:
+        kv = {}
+        with open(COUNTERS_FILE) as fh:
+            for line in fh:
+                if line.startswith("    ") and " = " in line:
+                    k, v = line.strip().split(" = ", 1)
+                    kv[k] = v
+        if kv.get("kernel_source_sha256") != gate_source_digest():
+            return None
+        return int(float(kv["traffic_bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def main():
@@ -102,6 +138,13 @@ def main():
         lg, dr = verify_inputs(10 + i, VERIFY_B, VERIFY_K, VERIFY_V, 3.0)
         logits.append(torch.from_numpy(lg).to(dev))
         drafted.append(torch.from_numpy(dr).to(dev))
+
+    if args.copy_mib > 0:
+        src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     y = torch.empty((1, D_MODEL), dtype=torch.float32, device=dev)
     hn = torch.empty_like(y)
@@ -238,7 +281,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": counted_traffic(),
             "alg_bytes_per_launch": int(dom_bytes),
             "avg_launch_us": dom_us,
             "timing": "library per-kernel HIP events on the launch stream, separate K-step pass",

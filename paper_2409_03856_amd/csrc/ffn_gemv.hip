@@ -40,7 +40,9 @@ constexpr int kGateSegs = 1024;             // gate workgroups: four per CU on a
 constexpr int kMaxSeg = 256;                // rows per gate workgroup at most (d_ff <= 65536)
 constexpr int kDownWaves = 4;
 constexpr int kDownUnroll = 16;             // full-row chunks in flight per down wave
-constexpr int kRangeCap = 1024;             // kept rows resolved per pass in down_kernel
+// kept rows resolved per pass in down_kernel (h staged for BM tokens: <= 16 KiB of LDS)
+template <int BM>
+constexpr int range_cap() { return BM >= 8 ? 256 : 1024; }
 constexpr int kDownBlocks = 512;            // target workgroups of down_kernel
 constexpr int kListBlocks = 16;             // workgroups copying each token's active list
 constexpr int kMaxSegs = 4096;              // row segments a down launch can take (d_ff / 16)
@@ -247,6 +249,7 @@ __global__ __launch_bounds__(256) void down_kernel(
     const float* __restrict__ hbuf, int hstride, const int32_t* __restrict__ ucnt, int ntiles,
     int rmax, int gr, float* __restrict__ part) {
   __shared__ int s_pref[kMaxSegs + 1];
+  constexpr int kRangeCap = range_cap<BM>();
   __shared__ int s_row[kRangeCap];
   __shared__ float s_h[kRangeCap * BM];
   __shared__ float4 s_red[kDownWaves][kWave * 2];

@@ -5,10 +5,8 @@
 //  mfma_gate_up_kernel  h[m, n] = SiLU(x_m . W_gate[n]) * (x_m . W_up[n]) with
 //                       v_mfma_f32_16x16x32_bf16 (x rounded to bf16, exact products,
 //                       fp32 accumulation). A wave owns 16 neurons and streams their
-//                       W_gate and W_up rows: each lane reads 128 contiguous bytes of one
-//                       row per 256-wide K block, i.e. the K order inside a block is
-//                       permuted, identically for both operands (the sum does not care), so
-//                       weight rows are read in full cache lines. Two waves split the K
+//                       W_gate and W_up rows straight into MFMA operand registers, 256 K
+//                       elements per block and 8 MFMA steps per block. Two waves split the K
 //                       blocks of one neuron tile and are summed in a fixed order. h is
 //                       written in the compacted-list layout of the small-batch path (every
 //                       neuron kept, tiles of 16), so the same row-split down projection and
@@ -68,18 +66,20 @@ __global__ __launch_bounds__(256) void mfma_gate_up_kernel(
   }
   const int nblk = (d + kKBlock - 1) / kKBlock;
   for (int blk = khalf; blk < nblk; blk += 2) {
-    const int kb = blk * kKBlock + 64 * grp;  // this lane's 64 contiguous K elements
+    // step i covers K elements [32 i, 32 i + 32) of the block, lane group grp the 8 at 8 grp:
+    // the four lanes of a row read 64 contiguous bytes, steps 2j and 2j+1 a full 128-byte line
+    const int kb = blk * kKBlock + 8 * grp;
     uint4 g8[8], u8[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int k = kb + 8 * i;
+      const int k = kb + 32 * i;
       const bool ok = rv && k < d;
       g8[i] = ok ? *reinterpret_cast<const uint4*>(wgr + k) : make_uint4(0u, 0u, 0u, 0u);
       u8[i] = ok ? *reinterpret_cast<const uint4*>(wur + k) : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int k = kb + 8 * i;
+      const int k = kb + 32 * i;
       const bf16x8_t bg = __builtin_bit_cast(bf16x8_t, g8[i]);
       const bf16x8_t bu = __builtin_bit_cast(bf16x8_t, u8[i]);
 #pragma unroll
