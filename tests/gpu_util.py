@@ -5,7 +5,9 @@ Tolerances (see the design notes for their derivation):
   * FFN outputs on the fp32-input paths: max-abs error <= 1e-4 x RMS of the
     oracle output (fp32 accumulation of bf16 x fp32 products); the stated
     bound of the method, 2e-2 x RMS, is asserted as well;
-  * FFN outputs on the MFMA path (x and h rounded to bf16): <= 2e-2 x RMS;
+  * FFN outputs on the MFMA path (batch >= 8; the normalised input rounded to bf16):
+    <= 1e-4 x RMS against the oracle on the rounded input (5e-4 with RMSNorm, see
+    NORM_ROUNDING_TOL), and the method bound against the unrounded input;
   * acceptance lengths: bit-exact outside a guard band |q - r| <= 1e-5 r.
 """
 
@@ -19,6 +21,11 @@ import oracle
 
 FP32_PATH_TOL = 1e-4
 METHOD_TOL = 2e-2
+# With RMSNorm the GPU rounds its fp32 normalised input to bf16; where that fp32 value and the
+# fp64 one straddle a bf16 rounding boundary the two roundings differ by one bf16 ulp (2^-8
+# relative) in that element, which moves a gate/up sum by ~2^-8 / sqrt(d) of its size.
+NORM_ROUNDING_TOL = 5e-4
+MFMA_MIN_BATCH = 8
 CATS_BAND = 1e-3
 VERIFY_BAND = 1e-5
 
@@ -50,6 +57,12 @@ def host(t) -> np.ndarray:
     if t.dtype == torch.bfloat16:
         return t.view(torch.int16).cpu().numpy().view(np.uint16)
     return t.cpu().numpy()
+
+
+def rounded_bf16(x) -> np.ndarray:
+    """x rounded to bf16 (nearest even) and widened back: the MFMA path's input precision."""
+    from synth import bf16_bits
+    return oracle.widen_bf16(bf16_bits(np.asarray(x, dtype=np.float32)))
 
 
 def rel_err(got, want) -> float:

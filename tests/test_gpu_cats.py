@@ -40,7 +40,8 @@ def test_tiny_config_sixteen_tokens(sr):
 
 
 @pytest.mark.parametrize("d,f,bsz", [(264, 1000, 1), (264, 1000, 3), (256, 688, 16), (512, 97, 5),
-                                     (4096, 33, 4), (4096, 40, 5), (8, 1, 2)])
+                                     (4096, 33, 4), (4096, 40, 5), (8, 1, 2),
+                                     (8192, 300, 2)])
 def test_ragged_shapes_norm_resid(sr, d, f, bsz):
     say(f"cats ragged d={d} f={f} B={bsz}")
     (wg, wu, wd), W = _layer(200 + d + f + bsz, d, f, 1.0 / np.sqrt(d))

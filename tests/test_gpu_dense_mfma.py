@@ -13,15 +13,11 @@ import numpy as np
 import pytest
 
 import oracle
-from synth import ffn_weights, decode_inputs, griffin_prompt, bf16_bits, TINY, LLAMA3_8B
-from gpu_util import say, dev_bf16, dev_f32, host, check_ffn, rel_err, FP32_PATH_TOL, METHOD_TOL
+from synth import ffn_weights, decode_inputs, griffin_prompt, TINY, LLAMA3_8B
+from gpu_util import (say, dev_bf16, dev_f32, host, check_ffn, rel_err, rounded_bf16,
+                      FP32_PATH_TOL, METHOD_TOL, NORM_ROUNDING_TOL)
 
 pytestmark = pytest.mark.gpu
-
-# With RMSNorm the GPU rounds its fp32 normalised input to bf16; where that fp32 value and the
-# fp64 one straddle a bf16 rounding boundary the two roundings differ by one bf16 ulp (2^-8
-# relative) in that element, which moves a gate/up sum by ~2^-8 / sqrt(d) of its size.
-NORM_ROUNDING_TOL = 5e-4
 
 
 @pytest.fixture(scope="module")
@@ -36,18 +32,15 @@ def _layer(seed, d, f, std):
     return (wg, wu, wd), tuple(dev_bf16(w) for w in (wg, wu, wd))
 
 
-def _rounded(x):
-    return oracle.widen_bf16(bf16_bits(np.asarray(x, dtype=np.float32)))
-
-
 @pytest.mark.parametrize("d,f,bsz", [(256, 688, 8), (264, 1000, 9), (256, 688, 16), (512, 97, 17),
-                                     (4096, 40, 33), (8, 1, 8), (264, 1000, 64), (520, 33, 48)])
+                                     (4096, 40, 33), (8, 1, 8), (264, 1000, 64), (520, 33, 48),
+                                     (8192, 100, 16)])
 def test_ragged_batches(sr, d, f, bsz):
     say(f"dense mfma d={d} f={f} B={bsz}")
     (wg, wu, wd), W = _layer(500 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
     x = decode_inputs(40 + bsz, bsz, d)
     y = host(sr.sirius_ffn_dense(dev_f32(x), *W))
-    check_ffn(y, oracle.ffn_dense(_rounded(x), wg, wu, wd), tol=FP32_PATH_TOL)
+    check_ffn(y, oracle.ffn_dense(rounded_bf16(x), wg, wu, wd), tol=FP32_PATH_TOL)
     e = rel_err(y, oracle.ffn_dense(x, wg, wu, wd))
     say(f"  error vs unrounded input: {e:.2e} x RMS")
     assert e <= METHOD_TOL
@@ -62,7 +55,7 @@ def test_norm_and_residual(sr, bsz):
     res = decode_inputs(61 + bsz, bsz, d)
     y = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res)))
     xn = oracle.rmsnorm(x, 1e-5)
-    check_ffn(y, oracle.ffn_dense(_rounded(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
+    check_ffn(y, oracle.ffn_dense(rounded_bf16(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
     assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
 
 
@@ -89,7 +82,7 @@ def test_condensed_batch(sr):
     sel = host(sel).astype(np.int64)
     x = decode_inputs(800, bsz, d)
     y = host(sr.sirius_ffn_condensed(dev_f32(x), wgc, wuc, wdc))
-    check_ffn(y, oracle.ffn_masked(_rounded(x), wg, wu, wd, [sel] * bsz), tol=FP32_PATH_TOL)
+    check_ffn(y, oracle.ffn_masked(rounded_bf16(x), wg, wu, wd, [sel] * bsz), tol=FP32_PATH_TOL)
 
 
 def test_llama3_8b_verify_chunk(sr):
@@ -101,6 +94,6 @@ def test_llama3_8b_verify_chunk(sr):
     res = decode_inputs(901, bsz, d)
     y = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res)))
     xn = oracle.rmsnorm(x, 1e-5)
-    e = check_ffn(y, oracle.ffn_dense(_rounded(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
+    e = check_ffn(y, oracle.ffn_dense(rounded_bf16(xn), wg, wu, wd), resid=res, tol=NORM_ROUNDING_TOL)
     say(f"  error vs precision-matched oracle: {e:.2e} x RMS")
     assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
