@@ -20,12 +20,14 @@ batch, all inputs resident in HBM:
   verify    correction check over logits [8, 16, 128256]
 The printed value is the sparse FFN decode time per token (rows.cats, from
 row-boundary HIP events in the timed region). The roofline object is for the
-sparse path's dominant kernel (cats_gate: the gate GEMV plus the kept up rows),
-timed by the library's per-kernel HIP events in a second pass of the same K
-steps right after the timed region. Its `traffic` is the HBM byte count per
-launch from the committed rocprofv3 counter summary under profiles/, reported
-only while that summary's kernel-source digest matches the current sources
-(`--copy-mib` adds the plain copy whose counters scale FETCH_SIZE/WRITE_SIZE).
+sparse path's dominant kernel (cats_decode: gate GEMV, threshold, compaction,
+kept up rows and kept down rows in one pass; the other launch is the small
+fixed-order reduce), timed by the library's per-kernel HIP events in a second
+pass of the same K steps right after the timed region. Its `traffic` is the
+HBM byte count per launch from the committed rocprofv3 counter summary under
+profiles/, reported only while that summary's kernel-source digest matches the
+current sources (`--copy-mib` adds the plain copy whose counters scale
+FETCH_SIZE/WRITE_SIZE).
 """
 
 from __future__ import annotations
@@ -66,21 +68,22 @@ def parse():
     return p.parse_args()
 
 
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "cats_gate_llama3-8b_b1_hbm_counters.md")
-GATE_SOURCES = [os.path.join(ROOT, "paper_2409_03856_amd", "csrc", f) for f in ("ffn_gemv.hip", "common.h")]
+DOM_KERNEL = "cats_decode"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "cats_decode_llama3-8b_b1_hbm_counters.md")
+DOM_SOURCES = [os.path.join(ROOT, "paper_2409_03856_amd", "csrc", f) for f in ("ffn_decode.hip", "common.h")]
 
 
-def gate_source_digest() -> str:
+def dom_source_digest() -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in GATE_SOURCES:
+    for f in DOM_SOURCES:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
 def counted_traffic():
-    """HBM bytes per cats_gate launch from the committed counter summary, or None when that
+    """HBM bytes per dominant-kernel launch from the committed counter summary, or None when that
     summary is missing or was taken on a different kernel source."""
     try:
         kv = {}
@@ -89,7 +92,7 @@ def counted_traffic():
                 if line.startswith("    ") and " = " in line:
                     k, v = line.strip().split(" = ", 1)
                     kv[k] = v
-        if kv.get("kernel_source_sha256") != gate_source_digest():
+        if kv.get("kernel_source_sha256") != dom_source_digest():
             return None
         return int(float(kv["traffic_bytes_per_launch"]))
     except (OSError, KeyError, ValueError):
@@ -218,7 +221,8 @@ def main():
     torch.cuda.synchronize()
     sr.sirius_profile_enable(False)
     kern = {}
-    for name in ["cats_gate", "cats_down", "cats_reduce", "dense_gate", "dense_down", "dense_reduce", "ffn_mfma_gate_up", "ffn_mfma_down",
+    for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_gate_up", "ffn_mfma_down",
+                 "ffn_mfma_reduce",
                  "verify_stats", "verify_scan", "griffin_z", "griffin_score", "griffin_pick", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:
         tot, n = sr.sirius_profile_query(name)
@@ -249,9 +253,9 @@ def main():
                        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
 
     cats_us = float(np.mean(row_ms["cats"])) * 1e3
-    dom = "cats_gate"  # gate GEMV + up rows of the kept neurons: 3/4 of the sparse step's bytes
+    dom = DOM_KERNEL  # everything but the final reduce
     dom_us = kern[dom]["avg_us"]
-    dom_bytes = D_FF * D_MODEL * 2 + mean_active * D_MODEL * 2 + D_MODEL * 4
+    dom_bytes = D_FF * D_MODEL * 2 + 2 * mean_active * D_MODEL * 2 + D_MODEL * 4
     dom_gbps = dom_bytes / (dom_us * 1e-6) / 1e9
 
     out = {

@@ -57,7 +57,11 @@ bool dims_ok(int d_model, int d_ff) {
   return d_model >= 8 && d_model <= kMaxDModel && (d_model % 8) == 0 && d_ff >= 1 && d_ff <= kMaxDFF;
 }
 
-size_t gemv_ws(int B, int d, int F) { return sirius::gemv_layout(std::max(B, 1), d, F).total; }
+// B == 1 runs the one-pass decode kernel; larger batches the small-batch kernels.
+size_t gemv_ws(int B, int d, int F) {
+  if (B <= 1) return sirius::decode1_layout(d, F).total;
+  return sirius::gemv_layout(B, d, F).total;
+}
 
 size_t ffn_ws(int B, int d, int F) {
   if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
@@ -69,6 +73,12 @@ int run_ffn_gemv(const char* fn, const float* x, int B, const uint16_t* wg, cons
                  const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                  const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
                  hipStream_t s) {
+  if (B == 1) {
+    const sirius::Decode1Layout L1 = sirius::decode1_layout(d, F);
+    hipError_t e = sirius::launch_ffn_decode1(x, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
+                                              active_idx, active_cnt, static_cast<char*>(ws), L1, s);
+    return e == hipSuccess ? SIRIUS_OK : hip_status(e, fn);
+  }
   const sirius::GemvLayout L = sirius::gemv_layout(B, d, F);
   for (int b0 = 0; b0 < B; b0 += L.bc) {
     const int nb = std::min(L.bc, B - b0);

@@ -1,29 +1,32 @@
-// Small-batch SwiGLU FFN decode on gfx950: dense and per-token threshold sparsity
-// (FSparse after CATS: the gate is read whole, up and down only for kept neurons).
+// Small-batch SwiGLU FFN decode on gfx950, dense and per-token threshold sparsity (FSparse
+// after CATS: the gate is read whole, up and down only for neurons some token keeps), and
+// the calibration pass. Threshold-sparse calls with 2 or more tokens run here in chunks of up
+// to 8 tokens, dense and condensed calls with 2 to 7 tokens; batch 1 runs the one-pass
+// kernel of ffn_decode.hip, and dense calls with 8 or more tokens the MFMA kernel of
+// ffn_mfma.hip, which reuses the down and reduce kernels below.
 //
-// Three kernels per call, HBM-bound (one bf16 weight per two flops). No grid-wide barrier,
-// atomics or fences: on this part a dependent kernel boundary costs several microseconds,
-// and in-kernel cross-workgroup synchronisation (grid barriers, release fences) costs far
-// more, so workgroups hand results to each other only through kernel boundaries.
+// Three kernels per call, HBM-bound (one bf16 weight per two flops per token). No grid-wide
+// barrier, atomics or fences: workgroups hand results to each other only through kernel
+// boundaries, and every sum has a fixed order (bitwise reproducible).
 //
-//  gate_kernel   a workgroup owns a tile of 16 neuron rows, four per wave. Each wave first
-//                loads its four gate rows together (16-byte loads, 1 KiB per wave
-//                instruction), dots them with fp32 x staged in LDS (optionally RMS-
-//                normalised), reduces across the wave, applies SiLU and the threshold; then
-//                loads the W_up rows of the neurons some token keeps, together, and forms
-//                h_bi = a_bi * u_bi (0 for tokens that drop the neuron). A wave ballot +
-//                popcount compacts the tile's kept rows, in ascending order, into a per-tile
-//                list.
+//  gate_kernel   a workgroup owns one contiguous segment of neuron rows (1024 segments at
+//                most, four per CU). x (up to 8 tokens) is staged in LDS, optionally RMS-
+//                normalised; each wave streams gate rows two at a time (16-byte loads, 1 KiB
+//                per wave instruction), reduces across the wave, applies SiLU and the
+//                threshold per token; a block scan compacts the rows some token keeps, in
+//                ascending order; the W_up rows of those neurons are then streamed and
+//                h_bi = a_bi * u_bi (0 for tokens that drop the neuron) stored with the
+//                segment's kept list. Per-token lists go to a side buffer for the outputs.
 //  down_kernel   partial y over the kept rows only. Grid: (512-column slice) x (row range
-//                of the compacted kept list, split evenly by position, so every workgroup
-//                reads the same number of bytes whatever the sparsity pattern). A wave
-//                reads whole 1 KiB row chunks (16 rows in flight) and each lane
+//                of the concatenated kept lists, split evenly by position, so every
+//                workgroup reads the same number of bytes whatever the sparsity pattern).
+//                A wave reads whole 1 KiB row chunks (16 rows in flight) and each lane
 //                accumulates 8 output columns per token; the four waves are summed in a
 //                fixed order into one partial per workgroup. (Owning columns instead, to
 //                avoid partials, means 32-byte reads per row, and the per-CU limit on
 //                outstanding line requests then caps useful bandwidth near a quarter.)
-//  reduce_kernel y = resid + the row-range partials summed in order (bitwise reproducible);
-//                extra blocks build the per-token ascending active lists.
+//  reduce_kernel y = resid + the row-range partials summed in order; extra blocks build the
+//                per-token ascending active lists.
 
 
 
@@ -46,24 +49,12 @@ constexpr int range_cap() { return BM >= 8 ? 256 : 1024; }
 constexpr int kDownBlocks = 512;            // target workgroups of down_kernel
 constexpr int kListBlocks = 16;             // workgroups copying each token's active list
 constexpr int kMaxSegs = 4096;              // row segments a down launch can take (d_ff / 16)
+constexpr int kRedOut4 = 16;                // float4 outputs per reduce workgroup
+constexpr int kRedGroups = 256 / kRedOut4;  // partial-row groups per reduce workgroup
+constexpr int kRedUnroll = 8;               // partial rows in flight per reduce thread
 constexpr int kXLdsFloats = 32768;          // fp32 x staged in LDS: 128 KiB (LDS is 160 KiB)
 
 constexpr int kModeDense = 0, kModeSparse = 1, kModeAbsAct = 2;
-
-// Dot product of 8 bf16 weights (one 16-byte load) with 8 fp32 activations from LDS.
-__device__ __forceinline__ float dot8(uint4 w, const float* xp, float acc) {
-  const float4 a = *reinterpret_cast<const float4*>(xp);
-  const float4 b = *reinterpret_cast<const float4*>(xp + 4);
-  acc = fmaf(bf16_lo(w.x), a.x, acc);
-  acc = fmaf(bf16_hi(w.x), a.y, acc);
-  acc = fmaf(bf16_lo(w.y), a.z, acc);
-  acc = fmaf(bf16_hi(w.y), a.w, acc);
-  acc = fmaf(bf16_lo(w.z), b.x, acc);
-  acc = fmaf(bf16_hi(w.z), b.y, acc);
-  acc = fmaf(bf16_lo(w.w), b.z, acc);
-  acc = fmaf(bf16_hi(w.w), b.w, acc);
-  return acc;
-}
 
 template <int BM, int CPL, int MODE>
 __global__ __launch_bounds__(256) void gate_kernel(
@@ -139,7 +130,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
 #pragma unroll
       for (int q = 0; q < CPL; ++q) {
         const int c = lane + kWave * q;
-        w[r][q] = (j < nr && c < nch) ? wr[c] : make_uint4(0u, 0u, 0u, 0u);
+        w[r][q] = (j < nr && c < nch) ? ld_stream(wr + c) : make_uint4(0u, 0u, 0u, 0u);
       }
     }
 #pragma unroll
@@ -208,7 +199,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
 #pragma unroll
       for (int q = 0; q < CPL; ++q) {
         const int c = lane + kWave * q;
-        w[r][q] = (k < nkept && c < nch) ? ur[c] : make_uint4(0u, 0u, 0u, 0u);
+        w[r][q] = (k < nkept && c < nch) ? ld_stream(ur + c) : make_uint4(0u, 0u, 0u, 0u);
       }
     }
 #pragma unroll
@@ -334,7 +325,7 @@ __global__ __launch_bounds__(256) void down_kernel(
 #pragma unroll
       for (int u = 0; u < kDownUnroll; ++u) {
         const int i = i0 + u * kDownWaves;
-        w[u] = (i < n && cv) ? wd[(size_t)s_row[i] * nch + c] : make_uint4(0u, 0u, 0u, 0u);
+        w[u] = (i < n && cv) ? ld_stream(wd + (size_t)s_row[i] * nch + c) : make_uint4(0u, 0u, 0u, 0u);
       }
 #pragma unroll
       for (int u = 0; u < kDownUnroll; ++u) {
@@ -390,40 +381,44 @@ __global__ __launch_bounds__(256) void reduce_kernel(
     const float* __restrict__ part, int gr, int n, const float* resid, float* y, int nred, int B,
     int F, int ntiles, int rmax, const int32_t* __restrict__ bidx, const int32_t* __restrict__ bcnt,
     int32_t* __restrict__ active_idx, int32_t* __restrict__ active_cnt) {
-  __shared__ float4 s_red[4][kWave];
+  __shared__ float4 s_red[kRedGroups][kRedOut4];
   __shared__ int s_tmp[4];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int tid = threadIdx.x;
   if ((int)blockIdx.x < nred) {
-    // 64 float4 (256 outputs) per block; wave v sums ranges v, v + 4, ... with 8 loads in flight
-    const int o4 = blockIdx.x * kWave + lane;
+    // kRedOut4 float4 outputs per block; thread (o, g) sums partial rows g, g + 16, ... of
+    // output o with kRedUnroll loads in flight; the 16 groups are then added in order
+    const int o = tid % kRedOut4, g = tid / kRedOut4;
+    const int o4 = blockIdx.x * kRedOut4 + o;
     const bool ov = 4 * o4 < n;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     const float4* p4 = reinterpret_cast<const float4*>(part);
     const size_t stride4 = (size_t)(n >> 2);
-    for (int r0 = wave; r0 < gr; r0 += 8 * 4) {
-      float4 v[8];
+    for (int r0 = g; r0 < gr; r0 += kRedUnroll * kRedGroups) {
+      float4 v[kRedUnroll];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int r = r0 + 4 * u;
+      for (int u = 0; u < kRedUnroll; ++u) {
+        const int r = r0 + kRedGroups * u;
         v[u] = (ov && r < gr) ? p4[(size_t)r * stride4 + o4] : make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < kRedUnroll; ++u) {
         s.x += v[u].x;
         s.y += v[u].y;
         s.z += v[u].z;
         s.w += v[u].w;
       }
     }
-    s_red[wave][lane] = s;
+    s_red[g][o] = s;
     __syncthreads();
-    if (wave == 0 && ov) {
-      const float4 a = s_red[0][lane], b = s_red[1][lane], c = s_red[2][lane], e = s_red[3][lane];
-      float4 v;
-      v.x = ((a.x + b.x) + c.x) + e.x;
-      v.y = ((a.y + b.y) + c.y) + e.y;
-      v.z = ((a.z + b.z) + c.z) + e.z;
-      v.w = ((a.w + b.w) + c.w) + e.w;
+    if (tid < kRedOut4 && ov) {
+      float4 v = s_red[0][tid];
+      for (int q = 1; q < kRedGroups; ++q) {
+        const float4 a = s_red[q][tid];
+        v.x += a.x;
+        v.y += a.y;
+        v.z += a.z;
+        v.w += a.w;
+      }
       if (resid != nullptr) {
         const float4 rv = reinterpret_cast<const float4*>(resid)[o4];
         v.x = rv.x + v.x;
@@ -578,7 +573,7 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
       return e;
   }
   const int n = B * d;
-  const int nred = ceil_div(n, 4 * kWave);
+  const int nred = ceil_div(n, 4 * kRedOut4);
   ProfScope prof(mode == kModeSparse ? "cats_reduce" : "dense_reduce", stream);
   reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
       part, L.gr, n, resid, y, nred, B, F, L.ntiles, L.rmax, bidx, bcnt, active_idx, active_cnt);
@@ -610,11 +605,14 @@ hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t*
 }
 
 hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* resid, float* y,
-                         hipStream_t stream) {
+                         hipStream_t stream, int F, int nseg, int rmax, const int32_t* bidx,
+                         const int32_t* bcnt, int32_t* active_idx, int32_t* active_cnt) {
   const int n = B * d;
-  const int nred = ceil_div(n, 4 * kWave);
-  reduce_kernel<<<nred, 256, 0, stream>>>(part, gr, n, resid, y, nred, B, 0, 0, 0, nullptr,
-                                          nullptr, nullptr, nullptr);
+  const int nred = ceil_div(n, 4 * kRedOut4);
+  const bool lists = active_idx != nullptr;
+  if (lists && nseg > kGateSegs) return hipErrorInvalidValue;
+  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
+      part, gr, n, resid, y, nred, B, F, nseg, rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();
 }
 

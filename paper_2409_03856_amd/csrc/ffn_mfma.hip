@@ -74,8 +74,8 @@ __global__ __launch_bounds__(256) void mfma_gate_up_kernel(
     for (int i = 0; i < 8; ++i) {
       const int k = kb + 32 * i;
       const bool ok = rv && k < d;
-      g8[i] = ok ? *reinterpret_cast<const uint4*>(wgr + k) : make_uint4(0u, 0u, 0u, 0u);
-      u8[i] = ok ? *reinterpret_cast<const uint4*>(wur + k) : make_uint4(0u, 0u, 0u, 0u);
+      g8[i] = ok ? ld_stream(reinterpret_cast<const uint4*>(wgr + k)) : make_uint4(0u, 0u, 0u, 0u);
+      u8[i] = ok ? ld_stream(reinterpret_cast<const uint4*>(wur + k)) : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {

@@ -36,9 +36,26 @@ hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, 
 hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t* wd,
                        const int32_t* uidx, const float* hbuf, int hstride, const int32_t* ucnt,
                        float* part, hipStream_t stream);
-// y[b] = sum_r part[r][b] (+ resid[b]) in a fixed order.
+// y[b] = sum_r part[r][b] (+ resid[b]) in a fixed order. With active_idx, B * 16 more
+// workgroups concatenate token b's per-segment lists bidx[b][seg][0 .. bcnt[b][seg]) (nseg
+// segments of rmax slots, nseg <= 1024) into active_idx[b][*] and write active_cnt[b].
 hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* resid, float* y,
-                         hipStream_t stream);
+                         hipStream_t stream, int F = 0, int nseg = 0, int rmax = 0,
+                         const int32_t* bidx = nullptr, const int32_t* bcnt = nullptr,
+                         int32_t* active_idx = nullptr, int32_t* active_cnt = nullptr);
+
+// ---- batch-1 decode: gate, threshold, compaction, kept up rows and kept down rows of one
+// row segment per 1024-thread workgroup, then launch_reduce over the segment partials
+struct Decode1Layout {
+  int nseg, rmax;
+  size_t uidx, ucnt, part, total;
+};
+Decode1Layout decode1_layout(int d, int F);
+hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t* wu,
+                              const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                              const float* resid, float* y, int32_t* active_idx,
+                              int32_t* active_cnt, char* ws, const Decode1Layout& L,
+                              hipStream_t stream);
 
 // ---- multi-token FFN on MFMA (B >= kMfmaMinBatch)
 constexpr int kMfmaMinBatch = 8;

@@ -115,14 +115,14 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
     const int lo4 = lo >> 2, hi4 = (hi + 3) >> 2;  // hi is V or a multiple of 4
     int i = lo4 + tid;
     for (; i + 3 * kVerifyThreads < hi4; i += 4 * kVerifyThreads) {
-      const float4 v[4] = {L4[i], L4[i + kVerifyThreads], L4[i + 2 * kVerifyThreads],
-                           L4[i + 3 * kVerifyThreads]};
+      const float4 v[4] = {ld_stream(L4 + i), ld_stream(L4 + i + kVerifyThreads),
+                           ld_stream(L4 + i + 2 * kVerifyThreads), ld_stream(L4 + i + 3 * kVerifyThreads)};
       const int i0[4] = {4 * i, 4 * (i + kVerifyThreads), 4 * (i + 2 * kVerifyThreads),
                          4 * (i + 3 * kVerifyThreads)};
       stat_fold<4>(st, v, i0, c);
     }
     for (; i < hi4; i += kVerifyThreads) {
-      const float4 v[1] = {L4[i]};
+      const float4 v[1] = {ld_stream(L4 + i)};
       const int i0[1] = {4 * i};
       stat_fold<1>(st, v, i0, c);
     }

@@ -20,8 +20,8 @@ import pytest
 
 import oracle
 from synth import decode_inputs, calibration_inputs, griffin_prompt, LLAMA3_8B, LLAMA3_70B
-from gpu_util import (say, dev_f32, dev_bf16, host, check_cats_sets, check_ffn, rounded_bf16,
-                      FP32_PATH_TOL, NORM_ROUNDING_TOL, MFMA_MIN_BATCH)
+from gpu_util import (say, dev_f32, dev_bf16, host, check_cats_sets, check_ffn, check_ffn_rounded_norm,
+                      MFMA_MIN_BATCH)
 
 pytestmark = pytest.mark.gpu
 
@@ -159,11 +159,10 @@ def test_llama3_8b_condensed_stack(sr, stack8b, condensed8b, bsz):
         hwg, hwu, hwd = stack8b.host_layer(l)
         xn = oracle.rmsnorm(h_in, EPS)
         if bsz >= MFMA_MIN_BATCH:  # gate/up on MFMA from the bf16-rounded normalised input
-            ref, tol = oracle.ffn_masked(rounded_bf16(xn), hwg, hwu, hwd, [sels[l]] * bsz), NORM_ROUNDING_TOL
+            e, nb = check_ffn_rounded_norm(host(h), xn, hwg, hwu, hwd, sets=[sels[l]] * bsz, resid=h_in)
         else:
-            ref, tol = oracle.ffn_masked(xn, hwg, hwu, hwd, [sels[l]] * bsz), FP32_PATH_TOL
-        e = check_ffn(host(h), ref, resid=h_in, tol=tol)
-        say(f"  layer {l}: error {e:.2e} x RMS")
+            e, nb = check_ffn(host(h), oracle.ffn_masked(xn, hwg, hwu, hwd, [sels[l]] * bsz), resid=h_in), 0
+        say(f"  layer {l}: error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
     assert np.all(np.isfinite(host(h)))
 
 
@@ -180,9 +179,8 @@ def test_llama3_8b_dense_verify_chunk_stack(sr, stack8b):
         sr.sirius_ffn_dense(h, wg, wu, wd, norm_eps=EPS, resid=h, y=h)
         hwg, hwu, hwd = stack8b.host_layer(l)
         xn = oracle.rmsnorm(h_in, EPS)
-        e = check_ffn(host(h), oracle.ffn_dense(rounded_bf16(xn), hwg, hwu, hwd), resid=h_in,
-                      tol=NORM_ROUNDING_TOL)
-        say(f"  layer {l}: error {e:.2e} x RMS")
+        e, nb = check_ffn_rounded_norm(host(h), xn, hwg, hwu, hwd, resid=h_in)
+        say(f"  layer {l}: error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
 
 
 # --------------------------------------------------------------------------------------- 70B
