@@ -221,7 +221,7 @@ def main():
     torch.cuda.synchronize()
     sr.sirius_profile_enable(False)
     kern = {}
-    for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_gate_up", "ffn_mfma_down",
+    for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
                  "ffn_mfma_reduce",
                  "verify_stats", "verify_scan", "griffin_z", "griffin_score", "griffin_pick", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:

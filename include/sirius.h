@@ -69,9 +69,10 @@ extern "C" {
  *   resid  [B, d_model] fp32 added to the output, or NULL. May alias y.
  *   y      [B, d_model] fp32 output. May alias resid, must not alias x
  *          unless resid == x == y (in-place residual layer).
- * For B >= 8 the gate and up products run on MFMA with xn rounded to bf16
- * (exact products, fp32 accumulation); h and the down product stay fp32.
- * For B < 8 xn stays fp32 throughout.
+ * For B >= 8 both products run on MFMA: the gate and up products take xn
+ * rounded to bf16, the down product takes h as a pair of bf16 values
+ * (hi = bf16(h), lo = bf16(h - hi): about 16 significant bits); products
+ * are exact and accumulate in fp32. For B < 8 xn and h stay fp32.
  * Errors: SIRIUS_EINVAL for null pointers (resid may be NULL), d_model not
  * a multiple of 8 or outside [8, 8192], d_ff < 1, B < 0 or B > 64.
  */

@@ -1,19 +1,33 @@
-// Multi-token SwiGLU FFN gate/up products on MFMA (gfx950), for batches of 8..64 tokens:
-// the full model's parallel pass over a drafted chunk, and condensed / dense decode of
-// batched tokens.
+// Multi-token SwiGLU FFN on MFMA (gfx950), for batches of 8..64 tokens: the full model's
+// parallel pass over a drafted chunk, and condensed / dense decode of batched tokens. Both
+// products stream their weights once and stay HBM-bound at these batch sizes (16 tokens: two
+// flops per weight byte per token, against a bf16 MFMA ridge near 300), so the kernels are
+// organised around full-line weight reads, and v_mfma_f32_16x16x32_bf16 does the arithmetic.
 //
-//  mfma_gate_up_kernel  h[m, n] = SiLU(x_m . W_gate[n]) * (x_m . W_up[n]) with
-//                       v_mfma_f32_16x16x32_bf16 (x rounded to bf16, exact products,
-//                       fp32 accumulation). A wave owns 16 neurons and streams their
-//                       W_gate and W_up rows straight into MFMA operand registers, 256 K
-//                       elements per block and 8 MFMA steps per block. Two waves split the K
-//                       blocks of one neuron tile and are summed in a fixed order. h is
-//                       written in the compacted-list layout of the small-batch path (every
-//                       neuron kept, tiles of 16), so the same row-split down projection and
-//                       fixed-order reduce finish the FFN.
-//
-// The pass is HBM-bound (3 * d_ff * d_model * 2 bytes against ~6 * B * d_ff * d_model
-// flops), so MFMA is used for the contraction and nothing more elaborate is needed.
+//  prep_x_kernel   x -> RMSNorm (optional) -> bf16, zero-padded to a multiple of 16 rows.
+//  gate_up_kernel  H = SiLU(X W_gate^T) * (X W_up^T). A two-wave workgroup owns 8 neurons
+//                  (the MFMA tile's other 8 B-operand rows are zero), 7 workgroups per CU at
+//                  d_ff = 14336. Per 256-wide K block it stages the tile's gate and up rows and
+//                  the x rows in LDS with coalesced loads (512 contiguous bytes per row;
+//                  reading the MFMA operand layout straight from HBM gives only 64 contiguous
+//                  bytes per row per instruction and ran at about 3.6 TB/s), requests the next
+//                  block, and the two waves take alternate MFMA steps of the block, reading
+//                  operands with 16-byte LDS reads. (16-row tiles with wave-private staging,
+//                  deeper prefetch and staggered K starts measured the same or slower.) The
+//                  two waves' sums are added in a fixed order. h is stored as a pair of bf16
+//                  values, hi = bf16(h) and lo = bf16(h - hi), token-major [Mpad, F16]
+//                  (F16 = d_ff rounded up to 16, padding 0): the down product takes both,
+//                  which keeps about 16 significant bits of h.
+//  down_kernel     Y_partial = H W_down over one neuron range and one 64-column tile.
+//                  W_down is neuron-major (columns contiguous) but the MFMA B operand wants
+//                  eight consecutive neurons of one column per lane, so each 64-neuron x
+//                  64-column chunk is staged in LDS (rows padded to 136 bytes) and the
+//                  operand is gathered with 16-bit LDS reads; the four 8-row groups of a
+//                  gather fall 16 banks apart, so the gathers are conflict-free. The chunk's
+//                  hi/lo h fragments are staged in LDS as well and shared by the four waves
+//                  (one 16-column tile each). The next chunks' loads are kept in flight in
+//                  registers while the current chunk is multiplied.
+//  reduce_kernel   (ffn_gemv.hip) y = resid + the neuron-range partials in a fixed order.
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
@@ -24,39 +38,90 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 
-constexpr int kMTile = 16;      // MFMA M (tokens) and N (neurons) tile
-constexpr int kKBlock = 256;    // K elements per block: 4 lane groups x 64
-constexpr int kMaxMTiles = 4;   // batch <= 64
+constexpr int kMTile = 16;     // MFMA M (tokens) and N (neurons / columns) tile
+constexpr int kKBlock = 256;   // gate/up: K elements per block (8 MFMA steps of 32)
+constexpr int kMaxMTiles = 4;  // batch <= 64
+constexpr int kGuPitch = kKBlock * 2 + 16;  // bytes per staged gate/up row (528)
+constexpr int kGuRows = 8;  // neurons per gate/up workgroup (the MFMA tile's other 8 rows are 0)
+constexpr int kGuDepth = 1;  // K blocks in flight per gate/up workgroup
 
-// 8 fp32 -> 8 bf16 (round to nearest even), zero when out of range
-__device__ __forceinline__ bf16x8_t load_x8(const float* x, int m, int B, int d, int k) {
-  uint4 r = make_uint4(0u, 0u, 0u, 0u);
-  if (m < B && k < d) {
-    const float4 a = *reinterpret_cast<const float4*>(x + (size_t)m * d + k);
-    const float4 b = *reinterpret_cast<const float4*>(x + (size_t)m * d + k + 4);
-    r.x = f32_to_bf16(a.x) | (f32_to_bf16(a.y) << 16);
-    r.y = f32_to_bf16(a.z) | (f32_to_bf16(a.w) << 16);
-    r.z = f32_to_bf16(b.x) | (f32_to_bf16(b.y) << 16);
-    r.w = f32_to_bf16(b.z) | (f32_to_bf16(b.w) << 16);
+constexpr int kDnCols = 64;                // down: output columns per workgroup (4 waves x 16)
+constexpr int kDnChunk = 64;               // down: neurons per LDS chunk (2 MFMA steps)
+constexpr int kDnSteps = kDnChunk / 32;
+constexpr int kDnPitch = kDnCols * 2 + 8;  // bytes per staged W_down row (136)
+constexpr int kDnPrefetch = 4;             // chunks in flight per thread
+constexpr int kDnTarget = 1024;            // down workgroups to aim for
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// ---- x -> optional RMSNorm -> bf16 [Mpad][d]; one workgroup per padded row. Every thread
+// requests all of its (at most eight) 16-byte pieces of the row before using any of them.
+__global__ __launch_bounds__(256) void prep_x_kernel(const float* __restrict__ x, int B, int d,
+                                                     float norm_eps, uint16_t* __restrict__ xb) {
+  constexpr int kPer = 8;  // d_model <= 8192: 2048 float4 per row over 256 threads
+  __shared__ float s_w[4];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int m = blockIdx.x;
+  uint2* out = reinterpret_cast<uint2*>(xb + (size_t)m * d);
+  const int nv4 = d >> 2;
+  if (m >= B) {  // uniform over the block
+    for (int i = tid; i < nv4; i += 256) out[i] = make_uint2(0u, 0u);
+    return;
   }
-  return __builtin_bit_cast(bf16x8_t, r);
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)m * d);
+  float4 v[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = tid + 256 * u;
+    v[u] = (i < nv4) ? xr[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float inv = 1.0f;
+  if (norm_eps >= 0.f) {
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      ss = fmaf(v[u].x, v[u].x, ss);
+      ss = fmaf(v[u].y, v[u].y, ss);
+      ss = fmaf(v[u].z, v[u].z, ss);
+      ss = fmaf(v[u].w, v[u].w, ss);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) s_w[wave] = ss;
+    __syncthreads();
+    const float tot = ((s_w[0] + s_w[1]) + s_w[2]) + s_w[3];
+    inv = 1.0f / sqrtf(tot / (float)d + norm_eps);
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = tid + 256 * u;
+    if (i < nv4) {
+      float4 w = v[u];
+      if (norm_eps >= 0.f) {
+        w.x *= inv;
+        w.y *= inv;
+        w.z *= inv;
+        w.w *= inv;
+      }
+      out[i] = make_uint2(f32_to_bf16(w.x) | (f32_to_bf16(w.y) << 16),
+                          f32_to_bf16(w.z) | (f32_to_bf16(w.w) << 16));
+    }
+  }
 }
 
 template <int MT>
-__global__ __launch_bounds__(256) void mfma_gate_up_kernel(
-    const float* __restrict__ x, int B, const uint16_t* __restrict__ wg,
-    const uint16_t* __restrict__ wu, int d, int F, int32_t* __restrict__ uidx,
-    float* __restrict__ hbuf, int32_t* __restrict__ ucnt) {
-  __shared__ floatx4_t s_acc[2][MT][2][kWave];  // [neuron tile][m tile][gate/up][lane]
+__global__ __launch_bounds__(128) void gate_up_kernel(
+    const uint16_t* __restrict__ xb, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int F16, uint16_t* __restrict__ hhi,
+    uint16_t* __restrict__ hlo) {
+  // one K block at a time: the tile's gate and up rows and the x rows, padded to kGuPitch
+  __shared__ __attribute__((aligned(16))) unsigned char s_w[2][kGuRows * kGuPitch];
+  __shared__ __attribute__((aligned(16))) unsigned char s_x[MT * kMTile * kGuPitch];
+  __shared__ floatx4_t s_acc[MT][2][kWave];  // the second wave's sums: [m tile][gate/up][lane]
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int ntile = blockIdx.x * 2 + (wave >> 1);  // two neuron tiles per workgroup
-  const int khalf = wave & 1;                      // waves 0/1 and 2/3 split the K blocks
-  const int n0 = ntile * kMTile;
-  const int fr = lane & 15, grp = lane >> 4;  // fragment row, lane group
-  const int row = n0 + fr;
-  const bool rv = row < F;
-  const uint16_t* wgr = wg + (size_t)row * d;
-  const uint16_t* wur = wu + (size_t)row * d;
+  const int n0 = blockIdx.x * kGuRows;
+  const int fr = lane & 15, grp = lane >> 4;  // MFMA fragment row, lane group
+  const bool frv = fr < kGuRows;              // B-operand rows 8..15 of the tile stay zero
+  const int nch = d >> 3;
 
   floatx4_t accg[MT], accu[MT];
 #pragma unroll
@@ -64,61 +129,206 @@ __global__ __launch_bounds__(256) void mfma_gate_up_kernel(
     accg[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     accu[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   }
+  constexpr int kSteps = kKBlock / 32;
+  // staging of one block by the 128 threads, 16 bytes each per load: weight row r of the tile
+  // (gate for r < 8, up for r >= 8) or x row r - 16, K chunk tid % 32 of the block
+  constexpr int kRowsStaged = 2 * kGuRows + MT * kMTile;
+  constexpr int kLoads = kRowsStaged * (kKBlock / 8) / 128;
+  static_assert((kRowsStaged * (kKBlock / 8)) % 128 == 0, "whole loads per thread");
   const int nblk = (d + kKBlock - 1) / kKBlock;
-  for (int blk = khalf; blk < nblk; blk += 2) {
-    // step i covers K elements [32 i, 32 i + 32) of the block, lane group grp the 8 at 8 grp:
-    // the four lanes of a row read 64 contiguous bytes, steps 2j and 2j+1 a full 128-byte line
-    const int kb = blk * kKBlock + 8 * grp;
-    uint4 g8[8], u8[8];
+  const int schunk = tid & 31, srow0 = tid >> 5;  // 4 rows per load round
+  uint4 v[kGuDepth][kLoads];
+  auto load_block = [&](int blk, uint4(&vv)[kLoads]) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int k = kb + 32 * i;
-      const bool ok = rv && k < d;
-      g8[i] = ok ? ld_stream(reinterpret_cast<const uint4*>(wgr + k)) : make_uint4(0u, 0u, 0u, 0u);
-      u8[i] = ok ? ld_stream(reinterpret_cast<const uint4*>(wur + k)) : make_uint4(0u, 0u, 0u, 0u);
+    for (int q = 0; q < kLoads; ++q) {
+      const int r = srow0 + 4 * q;
+      const int c = blk * (kKBlock / 8) + schunk;
+      const bool cok = blk < nblk && c < nch;
+      if (r < 2 * kGuRows) {
+        const int row = n0 + (r & (kGuRows - 1));
+        const uint4* base = reinterpret_cast<const uint4*>(r < kGuRows ? wg : wu);
+        vv[q] = (cok && row < F) ? ld_stream(base + (size_t)row * nch + c) : make_uint4(0u, 0u, 0u, 0u);
+      } else {
+        const int m = r - 2 * kGuRows;
+        vv[q] = cok ? *(reinterpret_cast<const uint4*>(xb + (size_t)m * d) + c) : make_uint4(0u, 0u, 0u, 0u);
+      }
     }
+  };
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int k = kb + 32 * i;
-      const bf16x8_t bg = __builtin_bit_cast(bf16x8_t, g8[i]);
-      const bf16x8_t bu = __builtin_bit_cast(bf16x8_t, u8[i]);
+  for (int p = 0; p < kGuDepth; ++p) load_block(p, v[p]);
+  for (int b0 = 0; b0 < nblk; b0 += kGuDepth) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8_t a = load_x8(x, mt * kMTile + fr, B, d, k);
-        accg[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bg, accg[mt], 0, 0, 0);
-        accu[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bu, accu[mt], 0, 0, 0);
+    for (int p = 0; p < kGuDepth; ++p) {
+      const int blk = b0 + p;
+      if (blk >= nblk) break;  // uniform over the block
+      __syncthreads();  // both waves are done reading the previous block
+#pragma unroll
+      for (int q = 0; q < kLoads; ++q) {
+        const int r = srow0 + 4 * q;
+        unsigned char* dst = (r < 2 * kGuRows)
+                                 ? s_w[r / kGuRows] + (r & (kGuRows - 1)) * kGuPitch
+                                 : s_x + (r - 2 * kGuRows) * kGuPitch;
+        *reinterpret_cast<uint4*>(dst + 16 * schunk) = v[p][q];
+      }
+      __syncthreads();
+      load_block(blk + kGuDepth, v[p]);  // in flight while the next blocks are multiplied
+      // wave w takes MFMA steps w, w + 2, ... of the block
+#pragma unroll
+      for (int i2 = 0; i2 < kSteps / 2; ++i2) {
+        const int i = 2 * i2 + wave;
+        const int off = 2 * (32 * i + 8 * grp);
+        uint4 vg = *reinterpret_cast<const uint4*>(s_w[0] + (frv ? fr : 0) * kGuPitch + off);
+        uint4 vu = *reinterpret_cast<const uint4*>(s_w[1] + (frv ? fr : 0) * kGuPitch + off);
+        if (!frv) vg = vu = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const uint4 xa = *reinterpret_cast<const uint4*>(s_x + (mt * kMTile + fr) * kGuPitch + off);
+          accg[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xa), as_bf16x8(vg), accg[mt], 0, 0, 0);
+          accu[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xa), as_bf16x8(vu), accu[mt], 0, 0, 0);
+        }
       }
     }
   }
 
-  // fixed-order sum of the two K halves, then the epilogue on the first wave of each pair
-  const int pair = wave >> 1;
-  if (khalf == 1) {
+  // fixed-order sum of the two waves' steps, then the epilogue on the first wave
+  if (wave == 1) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      s_acc[pair][mt][0][lane] = accg[mt];
-      s_acc[pair][mt][1][lane] = accu[mt];
+      s_acc[mt][0][lane] = accg[mt];
+      s_acc[mt][1][lane] = accu[mt];
     }
   }
   __syncthreads();
-  if (khalf == 0 && n0 < F) {
-    // C layout: lane holds neuron n0 + lane % 16 and tokens 4 * (lane / 16) + r of each m tile
+  if (wave == 0 && frv) {
+    // C layout: lane holds tile row lane % 16 and tokens 4 (lane / 16) + r of each m tile.
+    // Rows past d_ff (up to F16) have zero weights and padded tokens zero inputs: h = 0.
     const int n = n0 + fr;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const floatx4_t og = s_acc[pair][mt][0][lane], ou = s_acc[pair][mt][1][lane];
+      const floatx4_t og = s_acc[mt][0][lane], ou = s_acc[mt][1][lane];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mt * kMTile + 4 * grp + r;
-        if (n < F && m < B) {
-          const float g = accg[mt][r] + og[r];
-          const float u = accu[mt][r] + ou[r];
-          hbuf[(size_t)n * B + m] = silu(g) * u;
+        const float g = accg[mt][r] + og[r];
+        const float u = accu[mt][r] + ou[r];
+        const float h = silu(g) * u;
+        const uint32_t hi = f32_to_bf16(h);
+        const float lo = h - __uint_as_float(hi << 16);
+        hhi[(size_t)m * F16 + n] = (uint16_t)hi;
+        hlo[(size_t)m * F16 + n] = (uint16_t)f32_to_bf16(lo);
+      }
+    }
+  }
+}
+
+// Y_partial[rho][m][c] = sum over the neurons n of range rho of H[m][n] * W_down[n][c]
+template <int MT>
+__global__ __launch_bounds__(256) void down_kernel(
+    const uint16_t* __restrict__ hhi, const uint16_t* __restrict__ hlo, int F16,
+    const uint16_t* __restrict__ wd, int d, int F, int B, int nchunk, float* __restrict__ part) {
+  constexpr int kHFrags = 2 * MT * kDnSteps * kWave;  // [hi/lo][m tile][step][lane]
+  constexpr int kHPerThread = kHFrags / 256;
+  static_assert(kHFrags % 256 == 0, "h fragments split evenly over the threads");
+  __shared__ __attribute__((aligned(16))) unsigned char s_w[kDnChunk * kDnPitch];
+  __shared__ uint4 s_h[kHFrags];
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int c0 = blockIdx.x * kDnCols, rho = blockIdx.y, gr = gridDim.y;
+  const int ch_lo = (int)(((long long)nchunk * rho) / gr);
+  const int ch_hi = (int)(((long long)nchunk * (rho + 1)) / gr);
+  const int nch = d >> 3;  // 16-byte chunks per W_down row
+
+  // weight staging: thread t loads rows t / 8 and t / 8 + 32 of a chunk, 16 bytes at
+  // column c0 + 8 (t % 8)
+  const int lr = tid >> 3, lc = tid & 7;
+  const int gcol = (c0 >> 3) + lc;
+  const bool colok = gcol < nch;
+  auto load_w = [&](int ch, uint4(&v)[2]) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int n = ch * kDnChunk + lr + 32 * q;
+      v[q] = (ch < ch_hi && colok && n < F)
+                 ? ld_stream(reinterpret_cast<const uint4*>(wd) + (size_t)n * nch + gcol)
+                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  // h fragment f = ((which * MT + mt) * kDnSteps + s) * 64 + l holds, for A-operand lane l
+  // (token mt * 16 + l % 16, neuron group l / 16), neurons 32 s + 8 (l / 16) .. + 7 of the chunk
+  auto load_h = [&](int ch, uint4(&v)[kHPerThread]) {
+#pragma unroll
+    for (int i = 0; i < kHPerThread; ++i) {
+      const int f = tid + 256 * i;
+      const int l = f % kWave, s = (f / kWave) % kDnSteps, mt = (f / (kWave * kDnSteps)) % MT;
+      const int which = f / (kWave * kDnSteps * MT);
+      const int k = ch * kDnChunk + 32 * s + 8 * (l >> 4);
+      const int m = mt * kMTile + (l & 15);
+      v[i] = (ch < ch_hi && k < F16)
+                 ? *reinterpret_cast<const uint4*>((which ? hlo : hhi) + (size_t)m * F16 + k)
+                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+
+  floatx4_t acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  uint4 wv[kDnPrefetch][2], hv[kDnPrefetch][kHPerThread];
+#pragma unroll
+  for (int p = 0; p < kDnPrefetch; ++p) {
+    load_w(ch_lo + p, wv[p]);
+    load_h(ch_lo + p, hv[p]);
+  }
+  const int nb = lane & 15, gq = lane >> 4;  // B operand: column 16 wave + nb, neuron group gq
+  for (int ch = ch_lo; ch < ch_hi; ch += kDnPrefetch) {
+#pragma unroll
+    for (int p = 0; p < kDnPrefetch; ++p) {
+      if (ch + p >= ch_hi) break;  // uniform over the block
+      __syncthreads();             // the previous chunk's readers are done with s_w / s_h
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        uint2* dst = reinterpret_cast<uint2*>(s_w + (lr + 32 * q) * kDnPitch + lc * 16);
+        dst[0] = make_uint2(wv[p][q].x, wv[p][q].y);
+        dst[1] = make_uint2(wv[p][q].z, wv[p][q].w);
+      }
+#pragma unroll
+      for (int i = 0; i < kHPerThread; ++i) s_h[tid + 256 * i] = hv[p][i];
+      __syncthreads();
+      // refill this slot with the chunk kDnPrefetch ahead
+      load_w(ch + p + kDnPrefetch, wv[p]);
+      load_h(ch + p + kDnPrefetch, hv[p]);
+#pragma unroll
+      for (int s = 0; s < kDnSteps; ++s) {
+        // B operand: rows 32 s + 8 gq + j (j = 0..7) of column 16 wave + nb, from LDS
+        const unsigned char* col = s_w + (32 * s + 8 * gq) * kDnPitch + (16 * wave + nb) * 2;
+        uint32_t bw[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t e0 = *reinterpret_cast<const uint16_t*>(col + (2 * j) * kDnPitch);
+          const uint32_t e1 = *reinterpret_cast<const uint16_t*>(col + (2 * j + 1) * kDnPitch);
+          bw[j] = e0 | (e1 << 16);
+        }
+        const bf16x8_t bop = as_bf16x8(make_uint4(bw[0], bw[1], bw[2], bw[3]));
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const bf16x8_t ahi = as_bf16x8(s_h[(mt * kDnSteps + s) * kWave + lane]);
+          const bf16x8_t alo = as_bf16x8(s_h[((MT + mt) * kDnSteps + s) * kWave + lane]);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bop, acc[mt], 0, 0, 0);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bop, acc[mt], 0, 0, 0);
         }
       }
     }
-    if (lane < kMTile && n0 + lane < F) uidx[n0 + lane] = n0 + lane;
-    if (lane == 0) ucnt[ntile] = min(kMTile, F - n0);
+  }
+
+  // C layout: lane holds column c0 + 16 wave + lane % 16 and tokens 4 (lane / 16) + r
+  const int c = c0 + 16 * wave + nb;
+  if (c < d) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mt * kMTile + 4 * gq + r;
+        if (m < B) part[((size_t)rho * B + m) * d + c] = acc[mt][r];
+      }
   }
 }
 
@@ -128,14 +338,15 @@ MfmaLayout mfma_layout(int B, int d, int F) {
   MfmaLayout L{};
   L.mpad = ceil_div(B, kMTile) * kMTile;
   L.ntiles = ceil_div(F, kMTile);
-  L.cs = ceil_div(d / 8, kWave);
-  L.gr = std::max(1, std::min(512 / L.cs, ceil_div(F, 32)));
+  L.f16 = L.ntiles * kMTile;
+  L.cs = ceil_div(d, kDnCols);
+  L.nchunk = ceil_div(F, kDnChunk);
+  L.gr = std::max(1, std::min(L.nchunk, kDnTarget / L.cs));
   Carve c;
-  L.xn = c.take((size_t)B * d * 4);
-  L.uidx = c.take((size_t)L.ntiles * kMTile * 4);
-  L.h = c.take((size_t)L.ntiles * kMTile * B * 4);
-  L.ucnt = c.take((size_t)L.ntiles * 4);
-  L.part = c.take((size_t)L.gr * std::min(B, 16) * d * 4);  // one 16-token down chunk
+  L.xb = c.take((size_t)L.mpad * d * 2);
+  L.hhi = c.take((size_t)L.mpad * L.f16 * 2);
+  L.hlo = c.take((size_t)L.mpad * L.f16 * 2);
+  L.part = c.take((size_t)L.gr * B * d * 4);
   L.total = c.off;
   return L;
 }
@@ -143,46 +354,57 @@ MfmaLayout mfma_layout(int B, int d, int F) {
 hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, int d, int F, float norm_eps, const float* resid,
                            float* y, char* ws, const MfmaLayout& L, hipStream_t stream) {
-  if (B < 1 || B > kMaxMTiles * kMTile) return hipErrorInvalidValue;
+  if (B < 1 || B > kMaxMTiles * kMTile || L.mpad != ceil_div(B, kMTile) * kMTile)
+    return hipErrorInvalidValue;
   hipError_t e;
-  const float* xin = x;
-  if (norm_eps >= 0.f) {  // RMSNorm once into the workspace, then the unnormalised path
-    float* xn = reinterpret_cast<float*>(ws + L.xn);
-    if ((e = launch_rmsnorm(x, B, d, norm_eps, xn, stream)) != hipSuccess) return e;
-    xin = xn;
-  }
-  int32_t* uidx = reinterpret_cast<int32_t*>(ws + L.uidx);
-  float* hbuf = reinterpret_cast<float*>(ws + L.h);
-  int32_t* ucnt = reinterpret_cast<int32_t*>(ws + L.ucnt);
-  const dim3 grid(ceil_div(L.ntiles, 2));
+  uint16_t* xb = reinterpret_cast<uint16_t*>(ws + L.xb);
+  uint16_t* hhi = reinterpret_cast<uint16_t*>(ws + L.hhi);
+  uint16_t* hlo = reinterpret_cast<uint16_t*>(ws + L.hlo);
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  const int mt = L.mpad / kMTile;
   {
-    ProfScope prof("ffn_mfma_gate_up", stream);
-    switch (ceil_div(B, kMTile)) {
-      case 1: mfma_gate_up_kernel<1><<<grid, 256, 0, stream>>>(xin, B, wg, wu, d, F, uidx, hbuf, ucnt); break;
-      case 2: mfma_gate_up_kernel<2><<<grid, 256, 0, stream>>>(xin, B, wg, wu, d, F, uidx, hbuf, ucnt); break;
-      case 3: mfma_gate_up_kernel<3><<<grid, 256, 0, stream>>>(xin, B, wg, wu, d, F, uidx, hbuf, ucnt); break;
-      case 4: mfma_gate_up_kernel<4><<<grid, 256, 0, stream>>>(xin, B, wg, wu, d, F, uidx, hbuf, ucnt); break;
-      default: return hipErrorInvalidValue;
-    }
+    ProfScope prof("ffn_mfma_prep", stream);
+    prep_x_kernel<<<L.mpad, 256, 0, stream>>>(x, B, d, norm_eps, xb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  // down projection and reduce in token chunks of at most 16 (the row-split down kernel keeps
-  // 8 output columns per token per lane in registers)
-  float* part = reinterpret_cast<float*>(ws + L.part);
-  for (int b0 = 0; b0 < B; b0 += 16) {
-    const int nb = std::min(16, B - b0);
-    {
-      ProfScope prof("ffn_mfma_down", stream);
-      if ((e = launch_down(nb, d, L.ntiles, kMTile, L.gr, wd, uidx, hbuf + b0, B, ucnt, part,
-                           stream)) != hipSuccess)
-        return e;
+  {
+    ProfScope prof("ffn_mfma_gate_up", stream);
+    const dim3 grid(L.f16 / kGuRows);  // every row below F16 is written (0 past d_ff)
+#define SIRIUS_GU(MTV)                                                                       \
+  case MTV:                                                                                  \
+    gate_up_kernel<MTV><<<grid, 128, 0, stream>>>(xb, wg, wu, d, F, L.f16, hhi, hlo);        \
+    break;
+    switch (mt) {
+      SIRIUS_GU(1)
+      SIRIUS_GU(2)
+      SIRIUS_GU(3)
+      SIRIUS_GU(4)
+      default:
+        return hipErrorInvalidValue;
     }
-    ProfScope prof("ffn_mfma_reduce", stream);
-    if ((e = launch_reduce(part, L.gr, nb, d, resid ? resid + (size_t)b0 * d : nullptr,
-                           y + (size_t)b0 * d, stream)) != hipSuccess)
-      return e;
+#undef SIRIUS_GU
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return hipSuccess;
+  {
+    ProfScope prof("ffn_mfma_down", stream);
+    const dim3 grid(L.cs, L.gr);
+#define SIRIUS_DN(MTV)                                                                        \
+  case MTV:                                                                                   \
+    down_kernel<MTV><<<grid, 256, 0, stream>>>(hhi, hlo, L.f16, wd, d, F, B, L.nchunk, part); \
+    break;
+    switch (mt) {
+      SIRIUS_DN(1)
+      SIRIUS_DN(2)
+      SIRIUS_DN(3)
+      SIRIUS_DN(4)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef SIRIUS_DN
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  ProfScope prof("ffn_mfma_reduce", stream);
+  return launch_reduce(part, L.gr, B, d, resid, y, stream);
 }
 
 }  // namespace sirius

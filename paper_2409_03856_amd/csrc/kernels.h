@@ -60,10 +60,11 @@ hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t
 // ---- multi-token FFN on MFMA (B >= kMfmaMinBatch)
 constexpr int kMfmaMinBatch = 8;
 struct MfmaLayout {
-  int mpad;     // batch padded to the MFMA M tile
-  int ntiles;   // neuron tiles of 16
-  int cs, gr;   // down grid
-  size_t xn, uidx, h, ucnt, part, total;  // workspace byte offsets / size
+  int mpad;          // batch padded to the MFMA M tile
+  int ntiles, f16;   // neuron tiles of 16, d_ff rounded up to 16
+  int cs, gr;        // down grid: 64-column tiles x neuron ranges
+  int nchunk;        // 64-neuron chunks of the down product
+  size_t xb, hhi, hlo, part, total;  // workspace byte offsets / size
 };
 MfmaLayout mfma_layout(int B, int d, int F);
 hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint16_t* wu,

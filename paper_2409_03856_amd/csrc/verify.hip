@@ -6,6 +6,8 @@
 //                      exp((L - max) / T) in fp64, and the first argmax. Wave
 //                      shuffles and a fixed-order merge of the four waves give
 //                      one partial per (row, segment).
+//                      The workgroup whose segment holds the row's drafted token
+//                      also records that token's logit.
 // verify_scan_kernel   one workgroup per batch entry: merges the segments of
 //                      each row in segment order, forms q_j = softmax(L_j/T)
 //                      [drafted_j], finds the first j with q_j < r, and picks
@@ -26,6 +28,8 @@ constexpr int kVerifyThreads = 256;
 constexpr int kMinSegment = 2048;    // logits per workgroup at least
 constexpr int kTargetBlocks = 2048;  // enough workgroups to cover 256 CUs several times
 constexpr int kMaxRows = 1024;       // R limit of the scan kernel
+constexpr int kChunk = 8;            // float4 loads in flight per stats thread
+constexpr int kScanBatch = 16;       // split partials loaded together per scan thread
 
 struct Stat {
   float m;    // running max of the raw logits
@@ -94,14 +98,20 @@ __device__ __forceinline__ void stat_fold1(Stat& st, float v, int i, float c) {
 }
 
 __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
-    const float* __restrict__ logits, int V, int seg, float c, float* __restrict__ pm,
-    double* __restrict__ ps, float* __restrict__ pbv, int* __restrict__ pbi) {
+    const float* __restrict__ logits, int V, int seg, float c, const int32_t* __restrict__ drafted,
+    int K, int R, float* __restrict__ pm, double* __restrict__ ps, float* __restrict__ pbv,
+    int* __restrict__ pbi, float* __restrict__ pd) {
   __shared__ Stat s_w[kVerifyThreads / kWave];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int split = blockIdx.x, row = blockIdx.y, splits = gridDim.x;
   const int lo = split * seg;
   const int hi = min(V, lo + seg);
   const float* L = logits + (size_t)row * V;
+  // the drafted token of this row, if it falls in this segment: its logit goes to pd
+  const int j = row % R;
+  const int tok = (j < K) ? drafted[(size_t)(row / R) * K + j] : -1;
+  const bool mine = tok >= lo && tok < hi;
+  const float lt = (mine && tid == 0) ? L[tok] : -INFINITY;
 
   Stat st;
   st.m = -INFINITY;
@@ -110,21 +120,21 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
   st.bi = 0x7fffffff;
 
   if ((V & 3) == 0) {
-    // 16-byte loads; seg is a multiple of 4 so lo is 16-byte aligned.
+    // 16-byte loads, kChunk per thread in flight; seg is a multiple of 4 so lo is 16-byte
+    // aligned. Groups of 4 logits in a chunk are folded with one rescale per chunk.
     const float4* L4 = reinterpret_cast<const float4*>(L);
     const int lo4 = lo >> 2, hi4 = (hi + 3) >> 2;  // hi is V or a multiple of 4
-    int i = lo4 + tid;
-    for (; i + 3 * kVerifyThreads < hi4; i += 4 * kVerifyThreads) {
-      const float4 v[4] = {ld_stream(L4 + i), ld_stream(L4 + i + kVerifyThreads),
-                           ld_stream(L4 + i + 2 * kVerifyThreads), ld_stream(L4 + i + 3 * kVerifyThreads)};
-      const int i0[4] = {4 * i, 4 * (i + kVerifyThreads), 4 * (i + 2 * kVerifyThreads),
-                         4 * (i + 3 * kVerifyThreads)};
-      stat_fold<4>(st, v, i0, c);
-    }
-    for (; i < hi4; i += kVerifyThreads) {
-      const float4 v[1] = {ld_stream(L4 + i)};
-      const int i0[1] = {4 * i};
-      stat_fold<1>(st, v, i0, c);
+    for (int i = lo4 + tid; i < hi4; i += kChunk * kVerifyThreads) {
+      float4 v[kChunk];
+      int i0[kChunk];
+#pragma unroll
+      for (int g = 0; g < kChunk; ++g) {
+        const int k = i + g * kVerifyThreads;
+        // past the segment: -inf logits change neither the max, the sum nor the argmax
+        v[g] = (k < hi4) ? ld_stream(L4 + k) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        i0[g] = 4 * k;
+      }
+      stat_fold<kChunk>(st, v, i0, c);
     }
   } else {
     for (int i = lo + tid; i < hi; i += kVerifyThreads) stat_fold1(st, L[i], i, c);
@@ -146,40 +156,55 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
     ps[o] = a.s;
     pbv[o] = a.bv;
     pbi[o] = a.bi;
+    pd[o] = lt;
   }
 }
 
 __global__ __launch_bounds__(256) void verify_scan_kernel(
     const float* __restrict__ logits, int K, int R, int V, const int32_t* __restrict__ drafted,
     float r, float c, int splits, const float* __restrict__ pm, const double* __restrict__ ps,
-    const float* __restrict__ pbv, const int* __restrict__ pbi, int32_t* __restrict__ accept_len,
+    const float* __restrict__ pbv, const int* __restrict__ pbi, const float* __restrict__ pd,
+    int32_t* __restrict__ accept_len,
     int32_t* __restrict__ next_token, float* __restrict__ p_draft) {
   __shared__ float s_q[kMaxRows];
   __shared__ int s_amax[kMaxRows];
   const int b = blockIdx.x;
   for (int j = threadIdx.x; j < R; j += blockDim.x) {
     const size_t row = (size_t)b * R + j;
+    // merge the row's split partials in split order, kScanBatch loads in flight; the split
+    // holding the drafted token recorded its logit (-inf elsewhere, and everywhere for an id
+    // outside [0, V), which then gets q = 0)
+    float lt = -INFINITY;
     Stat a;
-    a.m = pm[row * splits];
-    a.s = ps[row * splits];
-    a.bv = pbv[row * splits];
-    a.bi = pbi[row * splits];
-    for (int sp = 1; sp < splits; ++sp) {
-      Stat o;
-      o.m = pm[row * splits + sp];
-      o.s = ps[row * splits + sp];
-      o.bv = pbv[row * splits + sp];
-      o.bi = pbi[row * splits + sp];
-      stat_merge(a, o, c);
+    a.m = -INFINITY;
+    a.s = 0.0;
+    a.bv = -INFINITY;
+    a.bi = 0x7fffffff;
+    for (int s0 = 0; s0 < splits; s0 += kScanBatch) {
+      Stat o[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const int sp = s0 + u;
+        if (sp < splits) {
+          const size_t i = row * splits + sp;
+          o[u].m = pm[i];
+          o[u].s = ps[i];
+          o[u].bv = pbv[i];
+          o[u].bi = pbi[i];
+          lt = fmaxf(lt, pd[i]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        if (s0 + u < splits) {
+          if (s0 + u == 0) a = o[u];
+          else stat_merge(a, o[u], c);
+        }
+      }
     }
     s_amax[j] = a.bi;
     if (j < K) {
-      const int tok = drafted[(size_t)b * K + j];
-      float q = 0.f;
-      if (tok >= 0 && tok < V) {
-        const float lt = logits[row * V + tok];
-        q = (float)((double)exp2f((lt - a.m) * c) / a.s);
-      }
+      const float q = (lt > -INFINITY) ? (float)((double)exp2f((lt - a.m) * c) / a.s) : 0.f;
       s_q[j] = q;
       if (p_draft != nullptr) p_draft[(size_t)b * K + j] = q;
     }
@@ -208,7 +233,7 @@ VerifyLayout verify_layout(int B, int R, int V) {
   L.splits = splits;
   const size_t n = (size_t)rows * splits;
   Carve c;
-  L.part = c.take(n * (sizeof(float) * 2 + sizeof(double) + sizeof(int)));
+  L.part = c.take(n * (sizeof(float) * 3 + sizeof(double) + sizeof(int)));
   L.total = c.off;
   return L;
 }
@@ -226,18 +251,19 @@ hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const 
   float* pm = reinterpret_cast<float*>(p + n * sizeof(double));
   float* pbv = pm + n;
   int* pbi = reinterpret_cast<int*>(pbv + n);
+  float* pd = reinterpret_cast<float*>(pbi + n);
   // exp((L - m) / T) = exp2((L - m) * log2(e) / T); the factor is formed in double.
   const float c = (float)(1.4426950408889634 / (double)temperature);
   {
     ProfScope prof("verify_stats", stream);
-    verify_stats_kernel<<<dim3(splits, B * R), kVerifyThreads, 0, stream>>>(logits, V, seg, c, pm,
-                                                                            ps, pbv, pbi);
+    verify_stats_kernel<<<dim3(splits, B * R), kVerifyThreads, 0, stream>>>(
+        logits, V, seg, c, drafted, K, R, pm, ps, pbv, pbi, pd);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   ProfScope prof("verify_scan", stream);
   verify_scan_kernel<<<B, 256, 0, stream>>>(logits, K, R, V, drafted, r, c, splits, pm, ps, pbv,
-                                            pbi, accept_len, next_token, p_draft);
+                                            pbi, pd, accept_len, next_token, p_draft);
   return hipGetLastError();
 }
 

@@ -4,9 +4,9 @@ This path is the full model's parallel pass over a drafted chunk (the chunk of
 tokens the full model checks at once). The gate and up products take the
 normalised input rounded to bf16, so the precision-matched reference is the
 oracle's dense FFN on that rounded input: the MFMA products are exact and
-accumulate in fp32, and h and the down product are fp32, so the fp32-path
-tolerance applies to it. Against the unrounded input the stated bound of the
-method holds as well.
+accumulate in fp32, and h enters the down product as a bf16 pair (hi + lo,
+relative error below 2^-17), so the fp32-path tolerance applies to it. Against
+the unrounded input the stated bound of the method holds as well.
 """
 
 import numpy as np

@@ -17,7 +17,7 @@ def sr():
     return sr
 
 
-@pytest.mark.parametrize("bsz,d", [(1, 4096), (3, 264), (16, 8192), (2, 1)])
+@pytest.mark.parametrize("bsz,d", [(1, 4096), (3, 264), (16, 8192), (2, 1), (2, 1001)])
 def test_rmsnorm(sr, bsz, d):
     h = decode_inputs(bsz + d, bsz, d) * 5.0
     out = host(sr.sirius_rmsnorm(dev_f32(h), 1e-5))
