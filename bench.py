@@ -223,7 +223,7 @@ def main():
     kern = {}
     for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
                  "ffn_mfma_reduce",
-                 "verify_stats", "verify_scan", "griffin_z", "griffin_score", "griffin_pick", "condense",
+                 "verify_stats", "verify_scan", "griffin_z", "griffin_topk", "griffin_score", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:
         tot, n = sr.sirius_profile_query(name)
         if n:

@@ -78,7 +78,7 @@ size_t select_ws_bytes();
 
 // ---- Griffin
 struct GriffinLayout {
-  size_t z, rownorm, select, kth, scores, total;
+  size_t z, rownorm, part, scores, total;  // z is used by the normalised variant only
 };
 GriffinLayout griffin_layout(int T, int d, int F);
 hipError_t launch_griffin(const uint16_t* xp, int T, const uint16_t* wg, const uint16_t* wu,
