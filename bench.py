@@ -18,6 +18,8 @@ batch, all inputs resident in HBM:
   dense     dense FFN decode, one token
   dense16   the full model's 16-token FFN pass
   verify    correction check over logits [8, 16, 128256]
+  cats70b   sparse FFN decode, one token, one Llama-3-70B FFN layer (d_model 8192,
+            d_ff 28672, 50% calibrated), four rotated copies (5.6 GB)
 The printed value is the sparse FFN decode time per token (rows.cats, from
 row-boundary HIP events in the timed region). The roofline object is for the
 sparse path's dominant kernel (cats_decode: gate GEMV, threshold, compaction,
@@ -44,6 +46,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 D_MODEL, D_FF = 4096, 14336
+D70, F70, NCOPY70 = 8192, 28672, 4
 NCOPY = 8
 N_DECODE = 64
 PROMPT_T = 512
@@ -135,6 +138,19 @@ def main():
     k_keep = D_FF // 2
     log("setup: prompt top-k per copy")
     cond = [sr.sirius_griffin_select(prompt, *layers[c], k_keep, want_scores=False)[2:] for c in range(NCOPY)]
+    log("setup: 70B layers")
+    layers70 = []
+    for c in range(NCOPY70):
+        ws = []
+        for m in range(3):
+            w = torch.empty((F70, D70), dtype=torch.bfloat16, device=dev)
+            sr.sirius_fill_normal_bf16(w, 5000 + 3 * c + m, mean=0.0, std=0.02)
+            ws.append(w)
+        layers70.append(ws)
+    x_cal70 = torch.from_numpy(calibration_inputs(5, 256, D70)).to(dev)
+    t70 = [float(sr.sirius_cats_calibrate(x_cal70, layers70[c][0], 0.5).item()) for c in range(NCOPY70)]
+    del x_cal70
+    xs70 = torch.from_numpy(decode_inputs(6, N_DECODE, D70)).to(dev)
     log("setup: logits")
     logits, drafted = [], []
     for i in range(N_LOGIT_BUFS):
@@ -156,15 +172,18 @@ def main():
     y16 = torch.empty((VERIFY_K, D_MODEL), dtype=torch.float32, device=dev)
     act_idx = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
     cnt_log = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
+    y70 = torch.empty((1, D70), dtype=torch.float32, device=dev)
+    act70 = torch.empty((1, F70), dtype=torch.int32, device=dev)
+    cnt70 = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
     g_sel = torch.empty(k_keep, dtype=torch.int32, device=dev)
     g_c = [torch.empty((k_keep, D_MODEL), dtype=torch.bfloat16, device=dev) for _ in range(3)]
     acc = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
     nxt = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
 
-    rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify"]
+    rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "cats70b"]
     stream = torch.cuda.current_stream()
 
-    def step(s, ev=None):
+    def step(s, ev=None, with70=True):
         c = s % NCOPY
 
         def mark(i):
@@ -190,6 +209,12 @@ def main():
         sr.sirius_verify_accept(logits[s % N_LOGIT_BUFS], drafted[s % N_LOGIT_BUFS], 0.1, 1.0,
                                 accept_len=acc, next_token=nxt, want_p=False)
         mark(7)
+        if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
+            return
+        c70 = s % NCOPY70
+        sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
+                           active_idx=act70, active_cnt=cnt70[s:s + 1])
+        mark(8)
 
     log("warmup")
     for s in range(args.warmup):
@@ -217,7 +242,7 @@ def main():
     sr.sirius_profile_reset()
     sr.sirius_profile_enable(True)
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(args.warmup + i, with70=False)
     torch.cuda.synchronize()
     sr.sirius_profile_enable(False)
     kern = {}
@@ -232,15 +257,17 @@ def main():
 
     counts = cnt_log[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64)
     mean_active = float(counts.mean())
+    mean_active70 = float(cnt70[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64).mean())
     # algorithmic bytes (what the method must move), per launch
     cats_bytes = D_FF * D_MODEL * 2 + 2 * mean_active * D_MODEL * 2 + 2 * D_MODEL * 4
     dense_bytes = 3 * D_FF * D_MODEL * 2 + 2 * D_MODEL * 4
     cond_bytes = 3 * k_keep * D_MODEL * 2 + 2 * D_MODEL * 4
     verify_bytes = VERIFY_B * VERIFY_K * VERIFY_V * 4
     griffin_bytes = 2 * D_FF * D_MODEL * 2 + PROMPT_T * D_MODEL * 2 + 6 * k_keep * D_MODEL * 2
+    cats70_bytes = F70 * D70 * 2 + 2 * mean_active70 * D70 * 2 + 2 * D70 * 4
     row_bytes = {"cats": cats_bytes, "rmsnorm": 2 * D_MODEL * 4, "griffin": griffin_bytes,
                  "condensed": cond_bytes, "dense": dense_bytes, "dense16": dense_bytes + 2 * VERIFY_K * D_MODEL * 4,
-                 "verify": verify_bytes}
+                 "verify": verify_bytes, "cats70b": cats70_bytes}
 
     def med(v):
         return float(np.median(np.asarray(v)))
@@ -277,6 +304,9 @@ def main():
             "layer_copies_rotated": NCOPY, "mean_active_neurons": round(mean_active, 1),
             "realized_sparsity": round(1.0 - mean_active / D_FF, 4),
             "cats_hbm_gbps": round(cats_bytes / (cats_us * 1e-6) / 1e9, 1),
+            "llama3_70b_layer": {"d_model": D70, "d_ff": F70, "layer_copies_rotated": NCOPY70,
+                                 "mean_active_neurons": round(mean_active70, 1),
+                                 "realized_sparsity": round(1.0 - mean_active70 / F70, 4)},
         },
         "roofline": {
             "kernel": dom,
