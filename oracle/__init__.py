@@ -8,6 +8,9 @@ A plain, slow, float64 NumPy statement of what the GPU library computes:
   * verify   -- the full model's likelihood check of drafted tokens:
                 per-row softmax probability of the drafted token, first
                 rejection below threshold r, corrected (argmax) token;
+  * tree     -- the pruned tree drafting step (fixed treewidth, cumulative
+                log-likelihood ranking) and the verification of a drafted tree
+                (longest advance over its complete paths), Sec. 4;
   * apu      -- the efficiency bookkeeping of Sec. 2.2 and Sec. 2.3
                 (APU, effective density, speculative-decoding AAL).
 
@@ -40,4 +43,5 @@ from .ffn import (  # noqa: F401
     stack_layer,
 )
 from .verify import softmax_row_stats, verify_accept  # noqa: F401
+from .tree import log_softmax, tree_build_step, tree_paths, tree_verify  # noqa: F401
 from .apu import sd_aal, apu, effective_density  # noqa: F401
