@@ -18,6 +18,8 @@ batch, all inputs resident in HBM:
   dense     dense FFN decode, one token
   dense16   the full model's 16-token FFN pass
   verify    correction check over logits [8, 16, 128256]
+  tree_build one drafting step of a width-4 tree: logits [4, 128256] at the current leaves
+  tree_verify verification of a 16-step, width-4 tree with bonus rows: logits [68, 128256]
   cats70b   sparse FFN decode, one token, one Llama-3-70B FFN layer (d_model 8192,
             d_ff 28672, 50% calibrated), four rotated copies (5.6 GB)
 The printed value is the sparse FFN decode time per token (rows.cats, from
@@ -51,6 +53,7 @@ NCOPY = 8
 N_DECODE = 64
 PROMPT_T = 512
 VERIFY_B, VERIFY_K, VERIFY_V = 8, 16, 128256
+TREE_K, TREE_W = 16, 4
 N_LOGIT_BUFS = 4
 
 
@@ -112,7 +115,8 @@ def main():
     import numpy as np
     import torch
     import paper_2409_03856_amd as sr
-    from synth import decode_inputs, calibration_inputs, griffin_prompt, verify_inputs
+    from synth import (decode_inputs, calibration_inputs, griffin_prompt, verify_inputs, tree_build_inputs,
+                       tree_verify_inputs)
 
     assert torch.cuda.is_available()
     dev = torch.device("cuda", 0)
@@ -157,6 +161,16 @@ def main():
         lg, dr = verify_inputs(10 + i, VERIFY_B, VERIFY_K, VERIFY_V, 3.0)
         logits.append(torch.from_numpy(lg).to(dev))
         drafted.append(torch.from_numpy(dr).to(dev))
+    log("setup: trees")
+    tb_logits, tb_cum, tv_logits, tv_tok, tv_par = [], [], [], [], []
+    for i in range(N_LOGIT_BUFS):
+        lg, cum = tree_build_inputs(20 + i, 1, TREE_W, VERIFY_V, 3.0)
+        tb_logits.append(torch.from_numpy(lg).to(dev))
+        tb_cum.append(torch.from_numpy(cum).to(dev))
+        lg, tk, pa = tree_verify_inputs(30 + i, 1, TREE_K, TREE_W, VERIFY_V, 3.0, bonus=True)
+        tv_logits.append(torch.from_numpy(lg).to(dev))
+        tv_tok.append(torch.from_numpy(tk).to(dev))
+        tv_par.append(torch.from_numpy(pa).to(dev))
 
     if args.copy_mib > 0:
         src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.float32, device=dev)
@@ -179,8 +193,11 @@ def main():
     g_c = [torch.empty((k_keep, D_MODEL), dtype=torch.bfloat16, device=dev) for _ in range(3)]
     acc = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
     nxt = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
+    tb_out = [torch.empty((1, TREE_W), dtype=dt, device=dev) for dt in (torch.int32, torch.int32, torch.float32)]
+    tv_out = [torch.empty(1, dtype=torch.int32, device=dev) for _ in range(3)]
 
-    rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "cats70b"]
+    rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "tree_build", "tree_verify",
+            "cats70b"]
     stream = torch.cuda.current_stream()
 
     def step(s, ev=None, with70=True):
@@ -209,12 +226,19 @@ def main():
         sr.sirius_verify_accept(logits[s % N_LOGIT_BUFS], drafted[s % N_LOGIT_BUFS], 0.1, 1.0,
                                 accept_len=acc, next_token=nxt, want_p=False)
         mark(7)
+        b = s % N_LOGIT_BUFS
+        sr.sirius_tree_build_step(tb_logits[b], TREE_W, tb_cum[b], 1.0, tokens=tb_out[0], parents=tb_out[1],
+                                  cum_ll_out=tb_out[2])
+        mark(8)
+        sr.sirius_tree_verify(tv_logits[b], tv_tok[b], tv_par[b], 0.1, 1.0, bonus=True, best_leaf=tv_out[0],
+                              accept_len=tv_out[1], next_token=tv_out[2], want_q=False)
+        mark(9)
         if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
             return
         c70 = s % NCOPY70
         sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
                            active_idx=act70, active_cnt=cnt70[s:s + 1])
-        mark(8)
+        mark(10)
 
     log("warmup")
     for s in range(args.warmup):
@@ -248,7 +272,7 @@ def main():
     kern = {}
     for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
                  "ffn_mfma_reduce",
-                 "verify_stats", "verify_scan", "griffin_z", "griffin_topk", "griffin_score", "condense",
+                 "verify_stats", "verify_scan", "tree_topw", "tree_select", "tree_stats", "tree_scan", "griffin_z", "griffin_topk", "griffin_score", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:
         tot, n = sr.sirius_profile_query(name)
         if n:
@@ -267,7 +291,9 @@ def main():
     cats70_bytes = F70 * D70 * 2 + 2 * mean_active70 * D70 * 2 + 2 * D70 * 4
     row_bytes = {"cats": cats_bytes, "rmsnorm": 2 * D_MODEL * 4, "griffin": griffin_bytes,
                  "condensed": cond_bytes, "dense": dense_bytes, "dense16": dense_bytes + 2 * VERIFY_K * D_MODEL * 4,
-                 "verify": verify_bytes, "cats70b": cats70_bytes}
+                 "verify": verify_bytes, "tree_build": TREE_W * VERIFY_V * 4 + 2 * TREE_W * 4,
+                 "tree_verify": (TREE_K + 1) * TREE_W * VERIFY_V * 4 + 2 * TREE_K * TREE_W * 4,
+                 "cats70b": cats70_bytes}
 
     def med(v):
         return float(np.median(np.asarray(v)))

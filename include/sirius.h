@@ -57,6 +57,8 @@ extern "C" {
 #define SIRIUS_OP_FFN_CONDENSED 3
 #define SIRIUS_OP_VERIFY 4
 #define SIRIUS_OP_CATS_CALIBRATE 5
+#define SIRIUS_OP_TREE_BUILD 6
+#define SIRIUS_OP_TREE_VERIFY 7
 
 /*
  * Dense SwiGLU FFN (the full model, sparsity 0):
@@ -167,11 +169,63 @@ int sirius_ffn_condensed(const float* x, int B, const uint16_t* w_gate_c, const 
  *   drafted [B, K] int32.
  *   p_draft [B, K] fp32 out (q), or NULL.
  * Errors: SIRIUS_EINVAL for null pointers (p_draft may be NULL), K < 1,
- * V < 1, R not in {K, K+1}, NaN r, temperature not > 0.
+ * V < 1, R not in {K, K+1}, B * R > 65535, NaN r, temperature not > 0.
  */
 int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
                          float r, float temperature, int32_t* accept_len, int32_t* next_token,
                          float* p_draft, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One pruned expansion step of the drafted tree (Sec. 4, hardware-friendly
+ * tree building): the sparse model drafts a tree that keeps W leaves per
+ * step, ranked by the cumulative log-likelihood of their paths, so that the
+ * tree has a fixed shape. For each of B trees, every (leaf w, token v) pair
+ * is scored
+ *   score = cum_ll[b, w] + log softmax(logits[b, w] / temperature)[v]
+ * and the W largest are kept, best first; ties go to the lower leaf slot,
+ * then the lower token id. The root step is Wc = 1 with cum_ll = NULL (0).
+ *   logits     [B, Wc, V] fp32 (sparse-model logits at the current leaves).
+ *   cum_ll     [B, Wc] fp32 cumulative log-likelihoods, or NULL (all 0).
+ *   tokens     [B, W] int32 out: the new leaves' tokens.
+ *   parents    [B, W] int32 out: their parent slots in [0, Wc).
+ *   cum_ll_out [B, W] fp32 out: their scores. May not alias cum_ll.
+ * Softmax sums accumulate in fp64, scores are formed in fp64 and stored as
+ * fp32.
+ * Errors: SIRIUS_EINVAL for null pointers (cum_ll may be NULL), B < 0,
+ * Wc or W outside [1, 16], B * Wc > 65535, V < 1 or Wc * V < W,
+ * temperature not finite and > 0.
+ */
+int sirius_tree_build_step(const float* logits, int B, int Wc, int V, const float* cum_ll, int W,
+                           float temperature, int32_t* tokens, int32_t* parents,
+                           float* cum_ll_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Verification of B drafted trees of K steps and width W in one pass of the
+ * full model (Sec. 4, hardware-friendly tree building; the acceptance test
+ * is the one of sirius_verify_accept, Algorithm 1). Node (i, w) carries the
+ * token tokens[b, i, w] and the full model's logits for that position at
+ * row i * W + w; parents[b, i, w] (i >= 1) is the slot of its parent in
+ * step i - 1 (parents[b, 0, *] is ignored). With bonus != 0, rows K * W + w
+ * hold the logits after leaf w. With q_iw = softmax(L_iw / temperature)
+ * [token] (0 for a token outside [0, V)), leaf w's advance is the first
+ * step on its root path whose node has q < r (strict), else K.
+ *   best_leaf[b]  = the leaf with the longest advance (lowest slot on ties)
+ *   accept_len[b] = its advance
+ *   next_token[b] = argmax of the raw logits at its rejected node, or of its
+ *                   bonus row when all K are accepted, else -1.
+ *   logits  [B, R, V] fp32, R = K * W (+ W with bonus), 16-byte aligned.
+ *   tokens, parents [B, K, W] int32. A parent slot outside [0, W) is read
+ *                   as slot 0.
+ *   q       [B, K, W] fp32 out, or NULL.
+ * With W = 1 this is sirius_verify_accept with R = K (+ 1).
+ * Errors: SIRIUS_EINVAL for null pointers (q may be NULL), B < 0, K < 1,
+ * W outside [1, 64], R > 1024, B * R > 65535, V < 1, NaN r, temperature not
+ * finite and > 0.
+ */
+int sirius_tree_verify(const float* logits, int B, int K, int W, int V, int bonus,
+                       const int32_t* tokens, const int32_t* parents, float r, float temperature,
+                       int32_t* best_leaf, int32_t* accept_len, int32_t* next_token, float* q,
+                       void* ws, size_t ws_bytes, void* stream);
 
 /*
  * RMSNorm with unit weight, the layer-stack glue around the FFN:
@@ -198,7 +252,8 @@ int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, 
  * unknown name). Kernel names: "cats_gate", "ffn_down", "ffn_reduce",
  * "ffn_mfma_gate_up", "verify_stats", "verify_scan", "griffin_z",
  * "griffin_rownorm", "griffin_score", "select_init", "select_hist",
- * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal".
+ * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal",
+ * "tree_topw", "tree_select", "tree_stats", "tree_scan".
  * sirius_profile_reset drops every record (it waits for pending events).
  * Errors: SIRIUS_EINVAL for NULL arguments, SIRIUS_EHIP if an event fails.
  */
@@ -211,6 +266,8 @@ int sirius_profile_query(const char* kernel, double* total_ms, int64_t* launches
  *   CATS_CALIBRATE: N, d_model, d_ff, unused, unused
  *   GRIFFIN_SELECT: unused, d_model, d_ff, T, unused
  *   VERIFY: B, unused, unused, V, R (rows per batch entry)
+ *   TREE_BUILD: B, Wc, W, V, unused
+ *   TREE_VERIFY: B, K, W, V, bonus
  * Returns 0 for an unknown op or invalid sizes. */
 size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, int K_or_R);
 

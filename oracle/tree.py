@@ -83,6 +83,8 @@ def tree_verify(logits, tokens, parents, r: float, temperature: float = 1.0, bon
     lg = np.asarray(logits)
     tk = np.asarray(tokens)
     k_n, w_n, v_n = lg.shape
+    if bonus is not None and np.shape(bonus) != (w_n, v_n):
+        raise ValueError("bonus rows must be [W, V], over the same vocabulary as the nodes")
     q = np.zeros((k_n, w_n), dtype=np.float64)
     amax = np.zeros((k_n, w_n), dtype=np.int64)
     for i in range(k_n):

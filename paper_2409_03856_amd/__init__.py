@@ -16,6 +16,8 @@ from ._lib import (  # noqa: F401
     sirius_griffin_select,
     sirius_ffn_condensed,
     sirius_verify_accept,
+    sirius_tree_build_step,
+    sirius_tree_verify,
     sirius_rmsnorm,
     sirius_fill_normal_bf16,
     sirius_workspace_size,
@@ -30,4 +32,6 @@ from ._lib import (  # noqa: F401
     OP_FFN_CONDENSED,
     OP_VERIFY,
     OP_CATS_CALIBRATE,
+    OP_TREE_BUILD,
+    OP_TREE_VERIFY,
 )

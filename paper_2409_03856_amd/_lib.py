@@ -27,6 +27,8 @@ OP_GRIFFIN_SELECT = 2
 OP_FFN_CONDENSED = 3
 OP_VERIFY = 4
 OP_CATS_CALIBRATE = 5
+OP_TREE_BUILD = 6
+OP_TREE_VERIFY = 7
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -41,6 +43,8 @@ SIGNATURES = {
     "sirius_griffin_select": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_ffn_condensed": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
     "sirius_verify_accept": (_I, [_P, _I, _I, _I, _I, _P, _F, _F, _P, _P, _P, _P, _Z, _P]),
+    "sirius_tree_build_step": (_I, [_P, _I, _I, _I, _P, _I, _F, _P, _P, _P, _P, _Z, _P]),
+    "sirius_tree_verify": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_rmsnorm": (_I, [_P, _I, _I, _F, _P, _P]),
     "sirius_fill_normal_bf16": (_I, [_P, _Z, ctypes.c_uint64, _F, _F, _P]),
     "sirius_profile_enable": (_I, [_I]),
@@ -262,6 +266,59 @@ def sirius_verify_accept(logits, drafted, r, temperature=1.0, *, accept_len=None
                                       float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(p_draft),
                                       _ptr(ws), ws.numel(), _stream(stream)))
     return accept_len, next_token, p_draft
+
+
+def sirius_tree_build_step(logits, width, cum_ll=None, temperature=1.0, *, tokens=None, parents=None,
+                           cum_ll_out=None, ws=None, stream=None):
+    """logits [B, Wc, V] fp32 at the current leaves, cum_ll [B, Wc] fp32 or None (the root).
+    Returns (tokens [B, W] int32, parents [B, W] int32, cum_ll_out [B, W] fp32), best first."""
+    torch = _torch()
+    _need(logits.dtype == torch.float32 and logits.dim() == 3, "logits must be fp32 [B, Wc, V]")
+    bsz, wc, vocab = (int(s) for s in logits.shape)
+    w = int(width)
+    if cum_ll is not None:
+        _need(cum_ll.dtype == torch.float32 and tuple(cum_ll.shape) == (bsz, wc), "cum_ll must be fp32 [B, Wc]")
+    dev = logits.device
+    if tokens is None:
+        tokens = torch.empty((bsz, w), dtype=torch.int32, device=dev)
+        parents = torch.empty((bsz, w), dtype=torch.int32, device=dev)
+        cum_ll_out = torch.empty((bsz, w), dtype=torch.float32, device=dev)
+    _dev_check(logits, cum_ll, tokens, parents, cum_ll_out)
+    if ws is None:
+        ws = workspace(OP_TREE_BUILD, max(bsz, 1), wc, w, vocab, 0, device=dev)
+    _check(lib().sirius_tree_build_step(_ptr(logits), bsz, wc, vocab, _ptr(cum_ll), w, float(temperature),
+                                        _ptr(tokens), _ptr(parents), _ptr(cum_ll_out), _ptr(ws), ws.numel(),
+                                        _stream(stream)))
+    return tokens, parents, cum_ll_out
+
+
+def sirius_tree_verify(logits, tokens, parents, r, temperature=1.0, *, bonus=False, best_leaf=None,
+                       accept_len=None, next_token=None, q=None, want_q=True, ws=None, stream=None):
+    """logits [B, K*W (+W with bonus), V] fp32, tokens / parents [B, K, W] int32.
+    Returns (best_leaf [B], accept_len [B], next_token [B] int32, q [B, K, W] fp32 or None)."""
+    torch = _torch()
+    _need(tokens.dtype == torch.int32 and tokens.dim() == 3, "tokens must be int32 [B, K, W]")
+    _need(parents.dtype == torch.int32 and tuple(parents.shape) == tuple(tokens.shape),
+          "parents must be int32 [B, K, W]")
+    bsz, k, w = (int(s) for s in tokens.shape)
+    rows = k * w + (w if bonus else 0)
+    _need(logits.dtype == torch.float32 and logits.dim() == 3 and tuple(logits.shape[:2]) == (bsz, rows),
+          "logits must be fp32 [B, K*W (+W), V]")
+    vocab = int(logits.shape[2])
+    dev = logits.device
+    if best_leaf is None:
+        best_leaf = torch.empty(bsz, dtype=torch.int32, device=dev)
+        accept_len = torch.empty(bsz, dtype=torch.int32, device=dev)
+        next_token = torch.empty(bsz, dtype=torch.int32, device=dev)
+    if want_q and q is None:
+        q = torch.empty((bsz, k, w), dtype=torch.float32, device=dev)
+    _dev_check(logits, tokens, parents, best_leaf, accept_len, next_token, q)
+    if ws is None:
+        ws = workspace(OP_TREE_VERIFY, max(bsz, 1), k, w, vocab, 1 if bonus else 0, device=dev)
+    _check(lib().sirius_tree_verify(_ptr(logits), bsz, k, w, vocab, 1 if bonus else 0, _ptr(tokens), _ptr(parents),
+                                    float(r), float(temperature), _ptr(best_leaf), _ptr(accept_len),
+                                    _ptr(next_token), _ptr(q), _ptr(ws), ws.numel(), _stream(stream)))
+    return best_leaf, accept_len, next_token, q
 
 
 def sirius_rmsnorm(h, eps=1e-5, *, out=None, stream=None):

@@ -33,6 +33,9 @@ constexpr int kMaxDModel = 8192;
 constexpr int kMaxDFF = 65536;
 constexpr int kMaxBatch = 64;
 constexpr int kMaxVerifyRows = 1024;
+constexpr int kMaxTreeBuildW = 16;   // tree width and current-leaf limit of a drafting step
+constexpr int kMaxTreeVerifyW = 64;  // tree width limit of tree verification
+constexpr long kMaxLogitRows = 65535;  // B * rows of a logit pass (second grid dimension)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -142,6 +145,17 @@ size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, i
     case SIRIUS_OP_VERIFY:
       if (B < 0 || T_or_V < 1 || K_or_R < 1 || K_or_R > kMaxVerifyRows) return 0;
       return sirius::verify_layout(std::max(B, 1), K_or_R, T_or_V).total;
+    case SIRIUS_OP_TREE_BUILD:
+      if (B < 0 || d_model < 1 || d_model > kMaxTreeBuildW || d_ff < 1 || d_ff > kMaxTreeBuildW ||
+          T_or_V < 1 || (long)d_model * T_or_V < d_ff)
+        return 0;
+      return sirius::tree_build_layout(std::max(B, 1), d_model, T_or_V).total;
+    case SIRIUS_OP_TREE_VERIFY: {
+      if (B < 0 || d_model < 1 || d_ff < 1 || d_ff > kMaxTreeVerifyW || T_or_V < 1) return 0;
+      const long R = (long)d_model * d_ff + (K_or_R ? d_ff : 0);
+      if (R > kMaxVerifyRows) return 0;
+      return sirius::verify_layout(std::max(B, 1), (int)R, T_or_V).total;
+    }
     default:
       return 0;
   }
@@ -250,6 +264,8 @@ int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const 
     return fail(SIRIUS_EINVAL, "%s: a required pointer is NULL", fn);
   if (!aligned16(logits)) return fail(SIRIUS_EINVAL, "%s: logits is not 16-byte aligned", fn);
   if (B == 0) return SIRIUS_OK;
+  if ((long)B * R > kMaxLogitRows)
+    return fail(SIRIUS_EINVAL, "%s: B*R=%ld rows above %ld", fn, (long)B * R, kMaxLogitRows);
   if ((size_t)B * R * V > ((size_t)1 << 40)) return fail(SIRIUS_EINVAL, "%s: logits too large", fn);
   const sirius::VerifyLayout L = sirius::verify_layout(B, R, V);
   if (ws_bytes < L.total)
@@ -257,6 +273,72 @@ int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const 
   return hip_status(sirius::launch_verify(logits, B, K, R, V, drafted, r, temperature, accept_len,
                                           next_token, p_draft, static_cast<char*>(ws), L,
                                           static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_tree_build_step(const float* logits, int B, int Wc, int V, const float* cum_ll, int W,
+                           float temperature, int32_t* tokens, int32_t* parents,
+                           float* cum_ll_out, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_tree_build_step";
+  if (B < 0) return fail(SIRIUS_EINVAL, "%s: B=%d < 0", fn, B);
+  if (Wc < 1 || Wc > kMaxTreeBuildW)
+    return fail(SIRIUS_EINVAL, "%s: Wc=%d outside [1, %d]", fn, Wc, kMaxTreeBuildW);
+  if (W < 1 || W > kMaxTreeBuildW)
+    return fail(SIRIUS_EINVAL, "%s: W=%d outside [1, %d]", fn, W, kMaxTreeBuildW);
+  if (V < 1 || (long)Wc * V < W)
+    return fail(SIRIUS_EINVAL, "%s: Wc*V=%ld candidates below W=%d", fn, (long)Wc * V, W);
+  if (!(temperature > 0.f) || std::isinf(temperature))
+    return fail(SIRIUS_EINVAL, "%s: temperature=%g must be finite and > 0", fn, (double)temperature);
+  if (logits == nullptr || tokens == nullptr || parents == nullptr || cum_ll_out == nullptr ||
+      ws == nullptr)
+    return fail(SIRIUS_EINVAL, "%s: a required pointer is NULL", fn);
+  if (cum_ll != nullptr && cum_ll == cum_ll_out)
+    return fail(SIRIUS_EINVAL, "%s: cum_ll_out aliases cum_ll", fn);
+  if (B == 0) return SIRIUS_OK;
+  if ((long)B * Wc > kMaxLogitRows)
+    return fail(SIRIUS_EINVAL, "%s: B*Wc=%ld rows above %ld", fn, (long)B * Wc, kMaxLogitRows);
+  if ((size_t)B * Wc * V > ((size_t)1 << 40)) return fail(SIRIUS_EINVAL, "%s: logits too large", fn);
+  const sirius::TreeBuildLayout L = sirius::tree_build_layout(B, Wc, V);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_tree_build(logits, B, Wc, V, cum_ll, W, temperature, tokens,
+                                              parents, cum_ll_out, static_cast<char*>(ws), L,
+                                              static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_tree_verify(const float* logits, int B, int K, int W, int V, int bonus,
+                       const int32_t* tokens, const int32_t* parents, float r, float temperature,
+                       int32_t* best_leaf, int32_t* accept_len, int32_t* next_token, float* q,
+                       void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_tree_verify";
+  if (B < 0) return fail(SIRIUS_EINVAL, "%s: B=%d < 0", fn, B);
+  if (K < 1) return fail(SIRIUS_EINVAL, "%s: K=%d must be >= 1", fn, K);
+  if (W < 1 || W > kMaxTreeVerifyW)
+    return fail(SIRIUS_EINVAL, "%s: W=%d outside [1, %d]", fn, W, kMaxTreeVerifyW);
+  const long R = (long)K * W + (bonus ? W : 0);
+  if (R > kMaxVerifyRows)
+    return fail(SIRIUS_EINVAL, "%s: K*W%s = %ld rows above %d", fn, bonus ? "+W" : "", R,
+                kMaxVerifyRows);
+  if (V < 1) return fail(SIRIUS_EINVAL, "%s: V=%d must be >= 1", fn, V);
+  if (std::isnan(r)) return fail(SIRIUS_EINVAL, "%s: r is NaN", fn);
+  if (!(temperature > 0.f) || std::isinf(temperature))
+    return fail(SIRIUS_EINVAL, "%s: temperature=%g must be finite and > 0", fn, (double)temperature);
+  if (logits == nullptr || tokens == nullptr || parents == nullptr || best_leaf == nullptr ||
+      accept_len == nullptr || next_token == nullptr || ws == nullptr)
+    return fail(SIRIUS_EINVAL, "%s: a required pointer is NULL", fn);
+  if (!aligned16(logits)) return fail(SIRIUS_EINVAL, "%s: logits is not 16-byte aligned", fn);
+  if (B == 0) return SIRIUS_OK;
+  if ((long)B * R > kMaxLogitRows)
+    return fail(SIRIUS_EINVAL, "%s: B*R=%ld rows above %ld", fn, (long)B * R, kMaxLogitRows);
+  if ((size_t)B * R * V > ((size_t)1 << 40)) return fail(SIRIUS_EINVAL, "%s: logits too large", fn);
+  const sirius::VerifyLayout L = sirius::verify_layout(B, (int)R, V);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_tree_verify(logits, B, K, W, V, bonus ? 1 : 0, tokens, parents,
+                                               r, temperature, best_leaf, accept_len, next_token, q,
+                                               static_cast<char*>(ws), L,
+                                               static_cast<hipStream_t>(stream)),
                     fn);
 }
 

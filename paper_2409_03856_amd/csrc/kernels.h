@@ -96,6 +96,27 @@ hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const 
                          float r, float temperature, int32_t* accept_len, int32_t* next_token,
                          float* p_draft, char* ws, const VerifyLayout& L, hipStream_t stream);
 
+// Tree verification: rows [b][i * W + w] (i < K) are the nodes of step i, then W bonus rows
+// if bonus != 0; tokens/parents [B][K][W]; q [B][K][W] or null. Needs R = K * W (+ W) <= 1024
+// and W <= 64; L = verify_layout(B, R, V).
+hipError_t launch_tree_verify(const float* logits, int B, int K, int W, int V, int bonus,
+                              const int32_t* tokens, const int32_t* parents, float r,
+                              float temperature, int32_t* best_leaf, int32_t* accept_len,
+                              int32_t* next_token, float* q, char* ws, const VerifyLayout& L,
+                              hipStream_t stream);
+
+// ---- tree drafting step: the W best (leaf, token) expansions of each of B trees
+struct TreeBuildLayout {
+  int splits;                  // segments per leaf row
+  size_t rm, rs, rv, ri, total;  // workspace byte offsets / size
+};
+TreeBuildLayout tree_build_layout(int B, int Wc, int V);
+// logits [B][Wc][V], cum_ll [B][Wc] or null (all 0); outputs [B][W]. 1 <= Wc, W <= 16.
+hipError_t launch_tree_build(const float* logits, int B, int Wc, int V, const float* cum_ll, int W,
+                             float temperature, int32_t* tokens, int32_t* parents,
+                             float* cum_out, char* ws, const TreeBuildLayout& L,
+                             hipStream_t stream);
+
 // ---- glue
 hipError_t launch_rmsnorm(const float* h, int B, int d, float eps, float* out, hipStream_t stream);
 hipError_t launch_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, float std,

@@ -30,6 +30,7 @@ constexpr int kTargetBlocks = 2048;  // enough workgroups to cover 256 CUs sever
 constexpr int kMaxRows = 1024;       // R limit of the scan kernel
 constexpr int kChunk = 8;            // float4 loads in flight per stats thread
 constexpr int kScanBatch = 16;       // split partials loaded together per scan thread
+constexpr int kMaxTreeW = 64;        // tree width limit of the tree scan
 
 struct Stat {
   float m;    // running max of the raw logits
@@ -160,51 +161,60 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
   }
 }
 
+// The row's split partials merged in split order (kScanBatch loads in flight), and the
+// drafted token's logit recorded by the split that holds it (-inf if none: an id outside
+// [0, V), which then gets q = 0).
+__device__ __forceinline__ void merge_row(size_t row, int splits, float c, const float* pm,
+                                          const double* ps, const float* pbv, const int* pbi,
+                                          const float* pd, Stat& a, float& lt) {
+  lt = -INFINITY;
+  a.m = -INFINITY;
+  a.s = 0.0;
+  a.bv = -INFINITY;
+  a.bi = 0x7fffffff;
+  for (int s0 = 0; s0 < splits; s0 += kScanBatch) {
+    Stat o[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int sp = s0 + u;
+      if (sp < splits) {
+        const size_t i = row * splits + sp;
+        o[u].m = pm[i];
+        o[u].s = ps[i];
+        o[u].bv = pbv[i];
+        o[u].bi = pbi[i];
+        lt = fmaxf(lt, pd[i]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      if (s0 + u < splits) {
+        if (s0 + u == 0) a = o[u];
+        else stat_merge(a, o[u], c);
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ float drafted_q(const Stat& a, float lt, float c) {
+  return (lt > -INFINITY) ? (float)((double)exp2f((lt - a.m) * c) / a.s) : 0.f;
+}
+
 __global__ __launch_bounds__(256) void verify_scan_kernel(
-    const float* __restrict__ logits, int K, int R, int V, const int32_t* __restrict__ drafted,
-    float r, float c, int splits, const float* __restrict__ pm, const double* __restrict__ ps,
-    const float* __restrict__ pbv, const int* __restrict__ pbi, const float* __restrict__ pd,
-    int32_t* __restrict__ accept_len,
+    int K, int R, int splits, float r, float c, const float* __restrict__ pm,
+    const double* __restrict__ ps, const float* __restrict__ pbv, const int* __restrict__ pbi,
+    const float* __restrict__ pd, int32_t* __restrict__ accept_len,
     int32_t* __restrict__ next_token, float* __restrict__ p_draft) {
   __shared__ float s_q[kMaxRows];
   __shared__ int s_amax[kMaxRows];
   const int b = blockIdx.x;
   for (int j = threadIdx.x; j < R; j += blockDim.x) {
-    const size_t row = (size_t)b * R + j;
-    // merge the row's split partials in split order, kScanBatch loads in flight; the split
-    // holding the drafted token recorded its logit (-inf elsewhere, and everywhere for an id
-    // outside [0, V), which then gets q = 0)
-    float lt = -INFINITY;
     Stat a;
-    a.m = -INFINITY;
-    a.s = 0.0;
-    a.bv = -INFINITY;
-    a.bi = 0x7fffffff;
-    for (int s0 = 0; s0 < splits; s0 += kScanBatch) {
-      Stat o[kScanBatch];
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) {
-        const int sp = s0 + u;
-        if (sp < splits) {
-          const size_t i = row * splits + sp;
-          o[u].m = pm[i];
-          o[u].s = ps[i];
-          o[u].bv = pbv[i];
-          o[u].bi = pbi[i];
-          lt = fmaxf(lt, pd[i]);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) {
-        if (s0 + u < splits) {
-          if (s0 + u == 0) a = o[u];
-          else stat_merge(a, o[u], c);
-        }
-      }
-    }
+    float lt;
+    merge_row((size_t)b * R + j, splits, c, pm, ps, pbv, pbi, pd, a, lt);
     s_amax[j] = a.bi;
     if (j < K) {
-      const float q = (lt > -INFINITY) ? (float)((double)exp2f((lt - a.m) * c) / a.s) : 0.f;
+      const float q = drafted_q(a, lt, c);
       s_q[j] = q;
       if (p_draft != nullptr) p_draft[(size_t)b * K + j] = q;
     }
@@ -223,6 +233,67 @@ __global__ __launch_bounds__(256) void verify_scan_kernel(
   }
 }
 
+// Tree verification (Sec. 4, hardware-friendly tree building): rows [i * W + w] are the
+// nodes of step i, then W bonus rows if given. Each leaf's path is walked back through the
+// parent links, its advance is the first step whose node has q < r (else K), and the leaf
+// with the longest advance (lowest slot on ties) is kept.
+__global__ __launch_bounds__(256) void tree_scan_kernel(
+    int K, int W, int bonus, const int32_t* __restrict__ parents, int splits, float r, float c,
+    const float* __restrict__ pm, const double* __restrict__ ps, const float* __restrict__ pbv,
+    const int* __restrict__ pbi, const float* __restrict__ pd, int32_t* __restrict__ best_leaf,
+    int32_t* __restrict__ accept_len, int32_t* __restrict__ next_token,
+    float* __restrict__ q_out) {
+  __shared__ float s_q[kMaxRows];
+  __shared__ int s_amax[kMaxRows];
+  __shared__ int s_par[kMaxRows];
+  __shared__ int s_path[kMaxRows];
+  __shared__ int s_adv[kMaxTreeW];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int KW = K * W, R = KW + (bonus ? W : 0);
+  for (int j = tid; j < R; j += blockDim.x) {
+    Stat a;
+    float lt;
+    merge_row((size_t)b * R + j, splits, c, pm, ps, pbv, pbi, pd, a, lt);
+    s_amax[j] = a.bi;
+    if (j < KW) {
+      const float q = drafted_q(a, lt, c);
+      s_q[j] = q;
+      if (q_out != nullptr) q_out[(size_t)b * KW + j] = q;
+      s_par[j] = parents[(size_t)b * KW + j];
+    }
+  }
+  __syncthreads();
+  if (tid < W) {
+    int w = tid;
+    for (int i = K - 1; i >= 0; --i) {
+      s_path[tid * K + i] = w;
+      if (i > 0) {
+        const int p = s_par[i * W + w];
+        w = (p >= 0 && p < W) ? p : 0;  // links outside [0, W) are a caller error; stay in bounds
+      }
+    }
+    int adv = K;
+    for (int i = 0; i < K; ++i) {
+      if (s_q[i * W + s_path[tid * K + i]] < r) {
+        adv = i;
+        break;
+      }
+    }
+    s_adv[tid] = adv;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int best = 0;
+    for (int w = 1; w < W; ++w)
+      if (s_adv[w] > s_adv[best]) best = w;
+    const int acc = s_adv[best];
+    best_leaf[b] = best;
+    accept_len[b] = acc;
+    next_token[b] = (acc < K) ? s_amax[acc * W + s_path[best * K + acc]]
+                              : (bonus ? s_amax[KW + best] : -1);
+  }
+}
+
 }  // namespace
 
 VerifyLayout verify_layout(int B, int R, int V) {
@@ -238,32 +309,70 @@ VerifyLayout verify_layout(int B, int R, int V) {
   return L;
 }
 
-hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
-                         float r, float temperature, int32_t* accept_len, int32_t* next_token,
-                         float* p_draft, char* ws, const VerifyLayout& L, hipStream_t stream) {
-  if (R > kMaxRows) return hipErrorInvalidValue;
+namespace {
+
+struct Parts {
+  float* pm;
+  double* ps;
+  float* pbv;
+  int* pbi;
+  float* pd;
+};
+
+// Per-(row, split) softmax partials of B * R rows; rows j < Kd of each batch entry have a
+// drafted token drafted[b * Kd + j] whose logit is recorded.
+hipError_t launch_stats(const float* logits, int B, int R, int V, const int32_t* drafted, int Kd,
+                        float c, char* ws, const VerifyLayout& L, hipStream_t stream, Parts* P,
+                        const char* prof_name) {
   const int splits = L.splits;
   int seg = ceil_div(V, splits);
   seg = (seg + 3) & ~3;
   const size_t n = (size_t)B * R * splits;
   char* p = ws + L.part;
-  double* ps = reinterpret_cast<double*>(p);
-  float* pm = reinterpret_cast<float*>(p + n * sizeof(double));
-  float* pbv = pm + n;
-  int* pbi = reinterpret_cast<int*>(pbv + n);
-  float* pd = reinterpret_cast<float*>(pbi + n);
-  // exp((L - m) / T) = exp2((L - m) * log2(e) / T); the factor is formed in double.
-  const float c = (float)(1.4426950408889634 / (double)temperature);
-  {
-    ProfScope prof("verify_stats", stream);
-    verify_stats_kernel<<<dim3(splits, B * R), kVerifyThreads, 0, stream>>>(
-        logits, V, seg, c, drafted, K, R, pm, ps, pbv, pbi, pd);
-  }
-  hipError_t e = hipGetLastError();
+  P->ps = reinterpret_cast<double*>(p);
+  P->pm = reinterpret_cast<float*>(p + n * sizeof(double));
+  P->pbv = P->pm + n;
+  P->pbi = reinterpret_cast<int*>(P->pbv + n);
+  P->pd = reinterpret_cast<float*>(P->pbi + n);
+  ProfScope prof(prof_name, stream);
+  verify_stats_kernel<<<dim3(splits, B * R), kVerifyThreads, 0, stream>>>(
+      logits, V, seg, c, drafted, Kd, R, P->pm, P->ps, P->pbv, P->pbi, P->pd);
+  return hipGetLastError();
+}
+
+// exp((L - m) / T) = exp2((L - m) * log2(e) / T); the factor is formed in double.
+float exp2_factor(float temperature) { return (float)(1.4426950408889634 / (double)temperature); }
+
+}  // namespace
+
+hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const int32_t* drafted,
+                         float r, float temperature, int32_t* accept_len, int32_t* next_token,
+                         float* p_draft, char* ws, const VerifyLayout& L, hipStream_t stream) {
+  if (R > kMaxRows) return hipErrorInvalidValue;
+  const float c = exp2_factor(temperature);
+  Parts P;
+  hipError_t e = launch_stats(logits, B, R, V, drafted, K, c, ws, L, stream, &P, "verify_stats");
   if (e != hipSuccess) return e;
   ProfScope prof("verify_scan", stream);
-  verify_scan_kernel<<<B, 256, 0, stream>>>(logits, K, R, V, drafted, r, c, splits, pm, ps, pbv,
-                                            pbi, pd, accept_len, next_token, p_draft);
+  verify_scan_kernel<<<B, 256, 0, stream>>>(K, R, L.splits, r, c, P.pm, P.ps, P.pbv, P.pbi, P.pd,
+                                            accept_len, next_token, p_draft);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_verify(const float* logits, int B, int K, int W, int V, int bonus,
+                              const int32_t* tokens, const int32_t* parents, float r,
+                              float temperature, int32_t* best_leaf, int32_t* accept_len,
+                              int32_t* next_token, float* q, char* ws, const VerifyLayout& L,
+                              hipStream_t stream) {
+  const int R = K * W + (bonus ? W : 0);
+  if (R > kMaxRows || W > kMaxTreeW) return hipErrorInvalidValue;
+  const float c = exp2_factor(temperature);
+  Parts P;
+  hipError_t e = launch_stats(logits, B, R, V, tokens, K * W, c, ws, L, stream, &P, "tree_stats");
+  if (e != hipSuccess) return e;
+  ProfScope prof("tree_scan", stream);
+  tree_scan_kernel<<<B, 256, 0, stream>>>(K, W, bonus, parents, L.splits, r, c, P.pm, P.ps, P.pbv,
+                                          P.pbi, P.pd, best_leaf, accept_len, next_token, q);
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@ from .inputs import (  # noqa: F401
     calibration_inputs,
     griffin_prompt,
     verify_inputs,
+    tree_build_inputs,
+    tree_verify_inputs,
     TINY,
     LLAMA3_8B,
     LLAMA3_70B,

@@ -67,6 +67,7 @@ _STREAM_DECODE = 2
 _STREAM_CALIB = 3
 _STREAM_PROMPT = 4
 _STREAM_LOGITS = 5
+_STREAM_TREE = 6
 
 
 def ffn_weights(seed: int, d_model: int, d_ff: int, std: float):
@@ -132,3 +133,47 @@ def verify_inputs(seed: int, batch: int, k: int, vocab: int, logit_var: float,
             else:
                 logits[b, j, tok] += bump[b, j]
     return logits, drafted
+
+
+def tree_build_inputs(seed: int, batch: int, wc: int, vocab: int, logit_var: float, root: bool = False):
+    """Sparse-model logits at the current leaves [batch, wc, vocab] fp32 ~ N(0, logit_var) and the
+    leaves' cumulative log-likelihoods [batch, wc] fp32 (None when root=True).
+
+    The cumulative values are -Exp(scale 3) draws put in descending order per tree (the drafting
+    step stores its leaves best first).
+    """
+    rng = _rng(seed, _STREAM_TREE)
+    logits = rng.standard_normal((batch, wc, vocab), dtype=np.float32)
+    logits *= np.float32(np.sqrt(logit_var))
+    if root:
+        return logits, None
+    cum = -np.sort(rng.exponential(3.0, size=(batch, wc)), axis=1).astype(np.float32)
+    return logits, cum
+
+
+def tree_verify_inputs(seed: int, batch: int, k: int, w: int, vocab: int, logit_var: float,
+                       bonus: bool = False, boost: float = 6.0, calibrated: bool = True):
+    """A drafted tree of k steps and width w per batch entry, with full-model logits per node.
+
+    Returns logits [batch, k*w (+ w with bonus), vocab] fp32 ~ N(0, logit_var), node tokens
+    [batch, k, w] int32 uniform over the vocabulary, and parent slots [batch, k, w] int32
+    uniform over [0, w) (step 0 holds -1: its parent is the root). The node's own token logit is
+    raised as in verify_inputs (calibrated: the row's largest logit plus U(0, boost)).
+    """
+    rows = k * w + (w if bonus else 0)
+    rng = _rng(seed, _STREAM_TREE)
+    logits = rng.standard_normal((batch, rows, vocab), dtype=np.float32)
+    logits *= np.float32(np.sqrt(logit_var))
+    tokens = rng.integers(0, vocab, size=(batch, k, w), dtype=np.int64).astype(np.int32)
+    parents = rng.integers(0, w, size=(batch, k, w), dtype=np.int64).astype(np.int32)
+    parents[:, 0, :] = -1
+    bump = rng.uniform(0.0, boost, size=(batch, k, w)).astype(np.float32)
+    for b in range(batch):
+        for i in range(k):
+            for j in range(w):
+                row, tok = i * w + j, tokens[b, i, j]
+                if calibrated:
+                    logits[b, row, tok] = logits[b, row].max() + bump[b, i, j]
+                else:
+                    logits[b, row, tok] += bump[b, i, j]
+    return logits, tokens, parents

@@ -9,7 +9,11 @@ Tolerances (see the design notes for their derivation):
     <= 1e-4 x RMS against the oracle on the rounded input (with RMSNorm plus a first-order
     allowance for inputs whose rounding is ambiguous, see check_ffn_rounded_norm), and the
     method bound against the unrounded input;
-  * acceptance lengths: bit-exact outside a guard band |q - r| <= 1e-5 r.
+  * acceptance lengths: bit-exact outside a guard band |q - r| <= 1e-5 r;
+  * tree drafting step: (parent, token) pairs bit-exact at every rank whose score is more
+    than 1e-5 from its neighbours' (and from the first excluded candidate's); near-tied ranks
+    must hold valid, distinct pairs whose scores match the oracle's rank scores within the
+    band; stored scores within 2e-5 + 2e-6 |score| (fp32 storage of an fp64 value).
 """
 
 from __future__ import annotations
@@ -28,6 +32,7 @@ MFMA_MIN_BATCH = 8
 NORM_ROUNDING_BAND = 4e-6
 CATS_BAND = 1e-3
 VERIFY_BAND = 1e-5
+TREE_SCORE_BAND = 1e-5
 
 
 def say(*a):
@@ -157,3 +162,33 @@ def verify_boundary_rows(q_oracle, acc_oracle, r, band=VERIFY_BAND):
         if np.any(np.abs(q_oracle[b, : jmax + 1] - r) <= band * abs(r)):
             rows.append(b)
     return rows
+
+
+def check_tree_build(logits, cum, width, tau, tok, par, out, band=TREE_SCORE_BAND):
+    """Check one tree's drafting step (tokens tok, parents par, scores out, best first) against
+    the oracle. Returns the number of near-tied ranks, where only validity is checked."""
+    lg = np.atleast_2d(np.asarray(logits, dtype=np.float64))
+    wc, v = lg.shape
+    n_cand = wc * v
+    tok_o, par_o, sc_o = oracle.tree_build_step(lg, cum, min(width + 1, n_cand), tau)
+    ls = oracle.log_softmax(lg, tau)
+    base = np.zeros(wc) if cum is None else np.asarray(cum, dtype=np.float64)
+    tok = np.asarray(tok, dtype=np.int64)
+    par = np.asarray(par, dtype=np.int64)
+    assert tok.shape == (width,) and par.shape == (width,)
+    assert ((tok >= 0) & (tok < v)).all(), tok
+    assert ((par >= 0) & (par < wc)).all(), par
+    assert len(set(zip(par.tolist(), tok.tolist()))) == width, "a (parent, token) pair is repeated"
+    got = base[par] + ls[par, tok]
+    tol = band * np.maximum(1.0, np.abs(sc_o[:width]))
+    assert np.all(np.abs(got - sc_o[:width]) <= tol), (got, sc_o[:width])
+    np.testing.assert_allclose(np.asarray(out, dtype=np.float64), sc_o[:width], rtol=2e-6, atol=2e-5)
+    near = 0
+    for j in range(width):
+        lo_gap = sc_o[j - 1] - sc_o[j] if j > 0 else np.inf
+        hi_gap = sc_o[j] - sc_o[j + 1] if j + 1 < len(sc_o) else np.inf
+        if min(lo_gap, hi_gap) <= tol[j]:
+            near += 1
+            continue
+        assert (par[j], tok[j]) == (par_o[j], tok_o[j]), (j, par[j], tok[j], par_o[j], tok_o[j])
+    return near

@@ -125,6 +125,64 @@ def test_verify_argument_errors(L):
     assert call(a7=float("inf")) == -1
     assert call(a5=None) == -1         # drafted NULL
     assert call(a12=16) == -2          # workspace too small
+    assert call(a1=20000) == -1 and "rows" in _err(L)  # B * R above the grid limit
+    assert call(a1=0) == 0             # empty batch
+
+
+def test_tree_build_argument_errors(L):
+    big = 1 << 30
+    # logits, B, Wc, V, cum_ll, W, temperature, tokens, parents, cum_out, ws, ws_bytes, stream
+    base = [FAKE, 2, 4, 100, FAKE, 8, 1.0, FAKE, FAKE, ctypes.c_void_p(1 << 21), FAKE, big, None]
+
+    def call(**kw):
+        a = list(base)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.sirius_tree_build_step(*a)
+
+    assert call(a1=-1) == -1           # B < 0
+    assert call(a2=0) == -1            # Wc < 1
+    assert call(a2=17) == -1           # Wc above 16
+    assert call(a5=0) == -1            # W < 1
+    assert call(a5=17) == -1           # W above 16
+    assert call(a3=1, a2=7) == -1 and "candidates" in _err(L)  # Wc * V < W
+    assert call(a3=0) == -1            # V < 1
+    assert call(a6=0.0) == -1          # temperature
+    assert call(a6=float("inf")) == -1
+    assert call(a7=None) == -1         # tokens NULL
+    assert call(a9=FAKE) == -1 and "alias" in _err(L)
+    assert call(a11=16) == -2          # workspace too small
+    assert call(a1=20000) == -1 and "rows" in _err(L)  # B * Wc above the grid limit
+    assert call(a4=None, a1=0) == 0    # cum_ll may be NULL
+    assert call(a1=0) == 0             # empty batch
+
+
+def test_tree_verify_argument_errors(L):
+    big = 1 << 30
+    nan = float("nan")
+    # logits, B, K, W, V, bonus, tokens, parents, r, T, best, acc, next, q, ws, ws_bytes, stream
+    base = [FAKE, 2, 4, 8, 100, 1, FAKE, FAKE, 0.1, 1.0, FAKE, FAKE, FAKE, None, FAKE, big, None]
+
+    def call(**kw):
+        a = list(base)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.sirius_tree_verify(*a)
+
+    assert call(a1=-1) == -1           # B < 0
+    assert call(a2=0) == -1            # K < 1
+    assert call(a3=0) == -1            # W < 1
+    assert call(a3=65) == -1           # W above 64
+    assert call(a2=16, a3=64) == -1 and "rows" in _err(L)  # K*W + W > 1024
+    assert call(a2=16, a3=64, a5=0, a1=0) == 0  # exactly 1024 rows, empty batch
+    assert call(a4=0) == -1            # V < 1
+    assert call(a8=nan) == -1          # NaN r
+    assert call(a9=0.0) == -1          # temperature
+    assert call(a7=None) == -1         # parents NULL
+    assert call(a10=None) == -1        # best_leaf NULL
+    assert call(a0=ctypes.c_void_p((1 << 20) + 4)) == -1 and "aligned" in _err(L)
+    assert call(a15=16) == -2          # workspace too small
+    assert call(a1=2000) == -1 and "rows" in _err(L)  # B * R above the grid limit
     assert call(a1=0) == 0             # empty batch
 
 
@@ -150,3 +208,14 @@ def test_workspace_sizes(L):
     assert g >= 512 * 14336 * 4
     c = f(5, 256, 4096, 14336, 0, 0)
     assert c >= 256 * 14336 * 4
+    # tree drafting step: B, Wc, W, V
+    assert f(6, 1, 8, 8, 128256, 0) > 0
+    assert f(6, 1, 17, 8, 128256, 0) == 0
+    assert f(6, 1, 8, 17, 128256, 0) == 0
+    assert f(6, 1, 8, 8, 7, 0) > 0     # 8 leaves of 7 tokens: 56 candidates
+    assert f(6, 1, 1, 8, 7, 0) == 0
+    # tree verification: B, K, W, V, bonus; the rows K*W (+W) are those of a chain check
+    assert f(7, 1, 16, 8, 128256, 1) == f(4, 1, 0, 0, 128256, 16 * 8 + 8)
+    assert f(7, 1, 16, 64, 128256, 0) > 0
+    assert f(7, 1, 16, 64, 128256, 1) == 0
+    assert f(7, 1, 4, 65, 128256, 0) == 0

@@ -1,0 +1,202 @@
+"""GPU parity: tree drafting step and tree verification (Sec. 4, hardware-friendly tree building)."""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import tree_build_inputs, tree_verify_inputs, verify_inputs
+from gpu_util import say, dev_f32, dev_i32, host, TREE_SCORE_BAND, VERIFY_BAND, check_tree_build
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "tree_hand_cases.json")
+
+
+@pytest.fixture(scope="module")
+def sr():
+    import paper_2409_03856_amd as sr
+    sr.lib()
+    return sr
+
+
+def _num(s):
+    return math.log(float(s[2:])) if s.startswith("ln") else float(s)
+
+
+def _expr(s):
+    return float(eval(s, {"__builtins__": {}}, {"log": math.log}))  # fixture expressions only
+
+
+def _golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------- drafting step
+
+def _build_and_check(sr, lg, cum, width, tau):
+    tok, par, out = sr.sirius_tree_build_step(dev_f32(lg), width, None if cum is None else dev_f32(cum), tau)
+    tok, par, out = host(tok), host(par), host(out)
+    n_amb = 0
+    for b in range(lg.shape[0]):
+        n_amb += check_tree_build(lg[b], None if cum is None else cum[b], width, tau, tok[b], par[b], out[b])
+    return tok, par, out, n_amb
+
+
+@pytest.mark.parametrize("case", _golden()["build"], ids=lambda c: c["name"])
+def test_build_hand_cases_on_gpu(sr, case):
+    say(f"tree build hand case: {case['name']}")
+    lg = np.array([[[_num(v) for v in row] for row in case["logits"]]], dtype=np.float32)
+    cum = None if case["cum"] is None else np.array([[_expr(e) for e in case["cum"]]], dtype=np.float32)
+    tok, par, out = sr.sirius_tree_build_step(dev_f32(lg), case["width"], None if cum is None else dev_f32(cum))
+    assert host(tok)[0].tolist() == case["tokens"]
+    assert host(par)[0].tolist() == case["parents"]
+    np.testing.assert_allclose(host(out)[0], [_expr(e) for e in case["cum_out"]], rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("width", [1, 4, 8, 16])
+@pytest.mark.parametrize("tau", [1.0, 0.6])
+def test_build_root_step(sr, width, tau):
+    for vocab in (1001, 128256):
+        say(f"tree build root W={width} tau={tau} V={vocab}")
+        lg, _ = tree_build_inputs(width, 3, 1, vocab, 3.0, root=True)
+        tok, par, out, n_amb = _build_and_check(sr, lg, None, width, tau)
+        assert (par == 0).all()
+        say(f"  near-tied ranks={n_amb}")
+
+
+@pytest.mark.parametrize("wc,width", [(4, 4), (8, 8), (16, 16), (16, 1), (1, 16), (3, 5)])
+def test_build_inner_step(sr, wc, width):
+    for tau in (1.0, 0.6):
+        say(f"tree build inner Wc={wc} W={width} tau={tau}")
+        lg, cum = tree_build_inputs(100 + wc * 17 + width, 2, wc, 128256, 3.0)
+        _build_and_check(sr, lg, cum, width, tau)
+
+
+def test_build_small_and_ragged_vocab(sr):
+    for vocab, width in ((16, 16), (17, 16), (5, 3), (2, 5), (2049, 8), (4097, 8), (130000, 2)):
+        say(f"tree build V={vocab} W={width}")
+        lg, cum = tree_build_inputs(vocab, 2, 3, vocab, 1.0)
+        _build_and_check(sr, lg, cum, width, 1.0)
+
+
+def test_build_tie_rules(sr):
+    # equal scores everywhere: lower parent first, then lower token, across segment boundaries
+    v = 128256
+    lg = np.zeros((1, 4, v), dtype=np.float32)
+    cum = np.zeros((1, 4), dtype=np.float32)
+    tok, par, _ = sr.sirius_tree_build_step(dev_f32(lg), 16, dev_f32(cum))
+    assert host(par)[0].tolist() == [0] * 16 and host(tok)[0].tolist() == list(range(16))
+    cum2 = np.array([[-1.0, 0.0, 0.0, -1.0]], dtype=np.float32)
+    tok, par, _ = sr.sirius_tree_build_step(dev_f32(lg), 8, dev_f32(cum2))
+    assert host(par)[0].tolist() == [1] * 8 and host(tok)[0].tolist() == list(range(8))
+    # the maximum repeated in several segments of one row: lowest ids first
+    lg3 = np.zeros((1, 1, v), dtype=np.float32)
+    for pos in (127999, 70001, 9000, 100000):
+        lg3[0, 0, pos] = 5.0
+    tok, par, _ = sr.sirius_tree_build_step(dev_f32(lg3), 5)
+    assert host(tok)[0].tolist() == [9000, 70001, 100000, 127999, 0]
+
+
+def test_build_batch_of_trees(sr):
+    lg, cum = tree_build_inputs(7, 32, 8, 32000, 3.0)
+    say("tree build 32 trees Wc=8 W=8 V=32000")
+    _build_and_check(sr, lg, cum, 8, 0.6)
+
+
+# ---------------------------------------------------------------- verification
+
+def _verify_and_check(sr, lg, tk, pa, r, tau, bonus):
+    bsz, k, w = tk.shape
+    best, acc, nxt, q = sr.sirius_tree_verify(dev_f32(lg), dev_i32(tk), dev_i32(pa), r, tau, bonus=bonus)
+    best, acc, nxt, q = host(best), host(acc), host(nxt), host(q)
+    skipped = 0
+    for b in range(bsz):
+        nodes = lg[b, : k * w].reshape(k, w, -1)
+        bon = lg[b, k * w:] if bonus else None
+        best_o, acc_o, nxt_o, q_o, _ = oracle.tree_verify(nodes, tk[b], pa[b], r, tau, bon)
+        np.testing.assert_allclose(q[b], q_o, rtol=1e-5, atol=1e-12)
+        if np.any(np.abs(q_o - r) <= VERIFY_BAND * abs(r)):
+            skipped += 1  # a node's q within the guard band of r: the decision is not determined
+            continue
+        assert (best[b], acc[b], nxt[b]) == (best_o, acc_o, nxt_o), (b, best[b], acc[b], nxt[b], best_o, acc_o, nxt_o)
+    return acc, skipped
+
+
+@pytest.mark.parametrize("case", _golden()["verify"], ids=lambda c: c["name"])
+def test_verify_hand_cases_on_gpu(sr, case):
+    say(f"tree verify hand case: {case['name']}")
+    nodes = np.array([[[_num(v) for v in row] for row in step] for step in case["logits"]], dtype=np.float32)
+    k, w, v = nodes.shape
+    rows = nodes.reshape(k * w, v)
+    bonus = "bonus" in case
+    if bonus:
+        rows = np.concatenate([rows, np.array([[_num(x) for x in row] for row in case["bonus"]], dtype=np.float32)])
+    tk = np.array([case["tokens"]], dtype=np.int32)
+    pa = np.array([case["parents"]], dtype=np.int32)
+    best, acc, nxt, q = sr.sirius_tree_verify(dev_f32(rows[None]), dev_i32(tk), dev_i32(pa), case["r"],
+                                              case["temperature"], bonus=bonus)
+    assert (int(host(best)[0]), int(host(acc)[0]), int(host(nxt)[0])) == (
+        case["best_leaf"], case["accept_len"], case["next_token"])
+    np.testing.assert_allclose(host(q)[0], [[_expr(e) for e in row] for row in case["q"]], rtol=1e-6)
+
+
+@pytest.mark.parametrize("bonus", [False, True])
+def test_width_one_is_the_chain_check(sr, bonus):
+    k, v = 16, 128256
+    lg, dr = verify_inputs(31, 4, k, v, 3.0, rows=k + (1 if bonus else 0), calibrated=True)
+    say(f"tree verify W=1 vs chain check bonus={bonus}")
+    for r in (0.05, 0.1, 0.3):
+        acc_c, nxt_c, p_c = sr.sirius_verify_accept(dev_f32(lg), dev_i32(dr), r, 0.6)
+        best, acc, nxt, q = sr.sirius_tree_verify(dev_f32(lg), dev_i32(dr[:, :, None]),
+                                                  dev_i32(np.zeros((4, k, 1), np.int32)), r, 0.6, bonus=bonus)
+        assert (host(best) == 0).all()
+        np.testing.assert_array_equal(host(acc), host(acc_c))
+        np.testing.assert_array_equal(host(nxt), host(nxt_c))
+        np.testing.assert_array_equal(host(q)[:, :, 0], host(p_c))
+
+
+@pytest.mark.parametrize("k,w,bonus", [(16, 4, True), (16, 8, True), (16, 8, False), (4, 3, True)])
+@pytest.mark.parametrize("tau", [1.0, 0.6])
+def test_random_trees_llama3_vocab(sr, k, w, bonus, tau):
+    lg, tk, pa = tree_verify_inputs(k * 100 + w, 2, k, w, 128256, 3.0, bonus=bonus)
+    for r in (0.05, 0.1, 0.3):
+        say(f"tree verify K={k} W={w} bonus={bonus} tau={tau} r={r}")
+        acc, skipped = _verify_and_check(sr, lg, tk, pa, r, tau, bonus)
+        say(f"  accept_len={acc.tolist()} skipped={skipped}")
+
+
+def test_odd_vocab_and_out_of_range_tokens(sr):
+    lg, tk, pa = tree_verify_inputs(5, 3, 5, 4, 1001, 2.0, bonus=True)
+    tk[0, 1, 2] = -7
+    tk[1, 0, 0] = 1001
+    say("tree verify V=1001 with out-of-range tokens")
+    _verify_and_check(sr, lg, tk, pa, 0.1, 1.0, True)
+
+
+def test_largest_tree(sr):
+    # K * W = 1024 rows, the scan kernel's limit
+    lg, tk, pa = tree_verify_inputs(9, 1, 16, 64, 32000, 3.0, bonus=False)
+    say("tree verify K=16 W=64 V=32000")
+    _verify_and_check(sr, lg, tk, pa, 0.1, 1.0, False)
+
+
+def test_equal_advances_keep_the_lowest_slot(sr):
+    # every node accepted: all leaves advance K; slot 0 is kept and its bonus row decides
+    k, w, v = 3, 4, 4096
+    lg = np.zeros((1, k * w + w, v), dtype=np.float32)
+    tk = np.full((1, k, w), 7, dtype=np.int32)
+    pa = np.zeros((1, k, w), dtype=np.int32)
+    lg[0, : k * w, 7] = 50.0
+    lg[0, k * w + 0, 123] = 1.0
+    lg[0, k * w + 1, 99] = 1.0
+    best, acc, nxt, _ = sr.sirius_tree_verify(dev_f32(lg), dev_i32(tk), dev_i32(pa), 0.5, 1.0, bonus=True)
+    assert (int(host(best)[0]), int(host(acc)[0]), int(host(nxt)[0])) == (0, k, 123)
+    # no bonus rows: the corrected token is -1
+    best, acc, nxt, _ = sr.sirius_tree_verify(dev_f32(np.ascontiguousarray(lg[:, : k * w])), dev_i32(tk),
+                                              dev_i32(pa), 0.5, 1.0, bonus=False)
+    assert (int(host(best)[0]), int(host(acc)[0]), int(host(nxt)[0])) == (0, k, -1)

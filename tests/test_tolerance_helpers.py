@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from synth import ffn_weights, decode_inputs, bf16_bits
-from gpu_util import check_ffn_rounded_norm
+from gpu_util import check_ffn_rounded_norm, check_tree_build
 
 
 def _widen(v):
@@ -41,3 +41,48 @@ def test_planted_error_is_rejected(case):
     y[1, 7] += 3e-4 * rms
     with pytest.raises(AssertionError):
         check_ffn_rounded_norm(y, xn, wg, wu, wd)
+
+
+def _tree_case(seed=4, wc=3, v=500, w=6):
+    rng = np.random.default_rng(seed)
+    lg = rng.normal(size=(wc, v)) * 2.0
+    cum = -np.sort(rng.exponential(3.0, size=wc))
+    tok, par, sc = oracle.tree_build_step(lg, cum, w)
+    return lg, cum, w, tok, par, sc
+
+
+def test_tree_build_check_accepts_the_oracle_and_rounded_scores():
+    lg, cum, w, tok, par, sc = _tree_case()
+    assert check_tree_build(lg, cum, w, 1.0, tok, par, sc.astype(np.float32)) == 0
+
+
+@pytest.mark.parametrize("plant", ["swap", "token", "parent", "score", "repeat"])
+def test_tree_build_check_rejects_planted_mistakes(plant):
+    lg, cum, w, tok, par, sc = _tree_case()
+    tok, par, sc = tok.copy(), par.copy(), sc.copy()
+    if plant == "swap":       # two well-separated ranks exchanged
+        tok[[1, 2]], par[[1, 2]], sc[[1, 2]] = tok[[2, 1]], par[[2, 1]], sc[[2, 1]]
+    elif plant == "token":    # a neighbouring token id
+        tok[0] = (tok[0] + 1) % lg.shape[1]
+    elif plant == "parent":   # the right token under another leaf
+        par[0] = (par[0] + 1) % lg.shape[0]
+    elif plant == "score":
+        sc[3] += 1e-3
+    else:
+        tok[4], par[4] = tok[3], par[3]
+    with pytest.raises(AssertionError):
+        check_tree_build(lg, cum, w, 1.0, tok, par, sc)
+
+
+def test_tree_build_check_allows_either_order_of_a_near_tie():
+    lg, cum, w, tok, par, sc = _tree_case()
+    # make ranks 1 and 2 tie within the band by moving one logit
+    lg = lg.copy()
+    ls = oracle.log_softmax(lg)
+    target = sc[1] - 3e-6
+    lg[par[2], tok[2]] += target - (cum[par[2]] + ls[par[2], tok[2]])
+    tok2, par2, sc2 = oracle.tree_build_step(lg, cum, w)
+    assert abs(sc2[1] - sc2[2]) < 1e-5
+    tok2, par2, sc2 = tok2.copy(), par2.copy(), sc2.copy()
+    tok2[[1, 2]], par2[[1, 2]], sc2[[1, 2]] = tok2[[2, 1]], par2[[2, 1]], sc2[[2, 1]]
+    assert check_tree_build(lg, cum, w, 1.0, tok2, par2, sc2) == 2
