@@ -184,7 +184,8 @@ int sirius_verify_accept(const float* logits, int B, int K, int R, int V, const 
  *   score = cum_ll[b, w] + log softmax(logits[b, w] / temperature)[v]
  * and the W largest are kept, best first; ties go to the lower leaf slot,
  * then the lower token id. The root step is Wc = 1 with cum_ll = NULL (0).
- *   logits     [B, Wc, V] fp32 (sparse-model logits at the current leaves).
+ *   logits     [B, Wc, V] fp32 (sparse-model logits at the current leaves),
+ *              16-byte aligned.
  *   cum_ll     [B, Wc] fp32 cumulative log-likelihoods, or NULL (all 0).
  *   tokens     [B, W] int32 out: the new leaves' tokens.
  *   parents    [B, W] int32 out: their parent slots in [0, Wc).

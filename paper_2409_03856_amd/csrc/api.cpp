@@ -149,7 +149,7 @@ size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, i
       if (B < 0 || d_model < 1 || d_model > kMaxTreeBuildW || d_ff < 1 || d_ff > kMaxTreeBuildW ||
           T_or_V < 1 || (long)d_model * T_or_V < d_ff)
         return 0;
-      return sirius::tree_build_layout(std::max(B, 1), d_model, T_or_V).total;
+      return sirius::tree_build_layout(std::max(B, 1), d_model, d_ff, T_or_V).total;
     case SIRIUS_OP_TREE_VERIFY: {
       if (B < 0 || d_model < 1 || d_ff < 1 || d_ff > kMaxTreeVerifyW || T_or_V < 1) return 0;
       const long R = (long)d_model * d_ff + (K_or_R ? d_ff : 0);
@@ -294,11 +294,12 @@ int sirius_tree_build_step(const float* logits, int B, int Wc, int V, const floa
     return fail(SIRIUS_EINVAL, "%s: a required pointer is NULL", fn);
   if (cum_ll != nullptr && cum_ll == cum_ll_out)
     return fail(SIRIUS_EINVAL, "%s: cum_ll_out aliases cum_ll", fn);
+  if (!aligned16(logits)) return fail(SIRIUS_EINVAL, "%s: logits is not 16-byte aligned", fn);
   if (B == 0) return SIRIUS_OK;
   if ((long)B * Wc > kMaxLogitRows)
     return fail(SIRIUS_EINVAL, "%s: B*Wc=%ld rows above %ld", fn, (long)B * Wc, kMaxLogitRows);
   if ((size_t)B * Wc * V > ((size_t)1 << 40)) return fail(SIRIUS_EINVAL, "%s: logits too large", fn);
-  const sirius::TreeBuildLayout L = sirius::tree_build_layout(B, Wc, V);
+  const sirius::TreeBuildLayout L = sirius::tree_build_layout(B, Wc, W, V);
   if (ws_bytes < L.total)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
   return hip_status(sirius::launch_tree_build(logits, B, Wc, V, cum_ll, W, temperature, tokens,

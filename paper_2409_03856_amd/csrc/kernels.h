@@ -107,11 +107,12 @@ hipError_t launch_tree_verify(const float* logits, int B, int K, int W, int V, i
 
 // ---- tree drafting step: the W best (leaf, token) expansions of each of B trees
 struct TreeBuildLayout {
-  int splits;                  // segments per leaf row
-  size_t rm, rs, rv, ri, total;  // workspace byte offsets / size
+  int splits;                // segments per leaf row
+  size_t rm, rs, rk, total;  // workspace byte offsets / size
 };
-TreeBuildLayout tree_build_layout(int B, int Wc, int V);
-// logits [B][Wc][V], cum_ll [B][Wc] or null (all 0); outputs [B][W]. 1 <= Wc, W <= 16.
+TreeBuildLayout tree_build_layout(int B, int Wc, int W, int V);
+// logits [B][Wc][V] (16-byte aligned), cum_ll [B][Wc] or null (all 0); outputs [B][W].
+// 1 <= Wc, W <= 16.
 hipError_t launch_tree_build(const float* logits, int B, int Wc, int V, const float* cum_ll, int W,
                              float temperature, int32_t* tokens, int32_t* parents,
                              float* cum_out, char* ws, const TreeBuildLayout& L,

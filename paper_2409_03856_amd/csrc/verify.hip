@@ -9,10 +9,10 @@
 //                      The workgroup whose segment holds the row's drafted token
 //                      also records that token's logit.
 // verify_scan_kernel   one workgroup per batch entry: merges the segments of
-//                      each row in segment order, forms q_j = softmax(L_j/T)
-//                      [drafted_j], finds the first j with q_j < r, and picks
-//                      the corrected token (argmax of row accept_len, or of the
-//                      bonus row).
+//                      each row (lanes over segments, fixed-order butterfly),
+//                      forms q_j = softmax(L_j/T)[drafted_j], finds the first
+//                      j with q_j < r, and picks the corrected token (argmax of
+//                      row accept_len, or of the bonus row).
 //
 // The pass is HBM-bound: B*R*V*4 bytes are read exactly once.
 #include <math.h>
@@ -29,8 +29,9 @@ constexpr int kMinSegment = 2048;    // logits per workgroup at least
 constexpr int kTargetBlocks = 2048;  // enough workgroups to cover 256 CUs several times
 constexpr int kMaxRows = 1024;       // R limit of the scan kernel
 constexpr int kChunk = 8;            // float4 loads in flight per stats thread
-constexpr int kScanBatch = 16;       // split partials loaded together per scan thread
-constexpr int kMaxTreeW = 64;        // tree width limit of the tree scan
+constexpr int kScanThreads = 1024;   // scan workgroup: 16 waves
+constexpr int kMaxSplits = 64;       // segments per row at most (one wave merges a row)
+constexpr int kMaxTreeW = 64;        // tree width limit of the tree scan (one wave of leaves)
 
 struct Stat {
   float m;    // running max of the raw logits
@@ -161,83 +162,98 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
   }
 }
 
-// The row's split partials merged in split order (kScanBatch loads in flight), and the
-// drafted token's logit recorded by the split that holds it (-inf if none: an id outside
-// [0, V), which then gets q = 0).
-__device__ __forceinline__ void merge_row(size_t row, int splits, float c, const float* pm,
-                                          const double* ps, const float* pbv, const int* pbi,
-                                          const float* pd, Stat& a, float& lt) {
-  lt = -INFINITY;
-  a.m = -INFINITY;
-  a.s = 0.0;
-  a.bv = -INFINITY;
-  a.bi = 0x7fffffff;
-  for (int s0 = 0; s0 < splits; s0 += kScanBatch) {
-    Stat o[kScanBatch];
+__device__ __forceinline__ float drafted_q(const Stat& a, float lt, float c) {
+  return (lt > -INFINITY) ? (float)((double)exp2f((lt - a.m) * c) / a.s) : 0.f;
+}
+
+// Merges the split partials of rows [0, R) of batch entry b. A row's splits sit on a group of
+// S2 lanes (S2 = splits rounded up to a power of two), so a wave covers 64 / S2 rows per pass;
+// the group's butterfly merge has a fixed order. The drafted token's logit comes from the
+// split that holds it (-inf if none: an id outside [0, V), which then gets q = 0). Writes the
+// row's argmax to s_amax[j] and, for rows j < Kd, q_j to s_q[j] (and q_out, if given).
+__device__ __forceinline__ void merge_rows(int b, int R, int Kd, int splits, float c,
+                                           const float* __restrict__ pm,
+                                           const double* __restrict__ ps,
+                                           const float* __restrict__ pbv,
+                                           const int* __restrict__ pbi,
+                                           const float* __restrict__ pd, float* s_q, int* s_amax,
+                                           float* __restrict__ q_out) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  int lg = 0;
+  while ((1 << lg) < splits) ++lg;
+  const int S2 = 1 << lg, rpp = kWave >> lg;
+  const int sub = lane & (S2 - 1), rsub = lane >> lg;
+  const int npass = (R + rpp - 1) / rpp;
+  for (int p0 = wave; p0 < npass; p0 += 2 * nw) {
+    // two passes per iteration, both passes' loads issued before either merge
+    Stat a[2];
+    float lt[2];
+    int j[2];
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      const int sp = s0 + u;
-      if (sp < splits) {
-        const size_t i = row * splits + sp;
-        o[u].m = pm[i];
-        o[u].s = ps[i];
-        o[u].bv = pbv[i];
-        o[u].bi = pbi[i];
-        lt = fmaxf(lt, pd[i]);
+    for (int u = 0; u < 2; ++u) {
+      j[u] = (p0 + u * nw) * rpp + rsub;
+      a[u].m = -INFINITY;
+      a[u].s = 0.0;
+      a[u].bv = -INFINITY;
+      a[u].bi = 0x7fffffff;
+      lt[u] = -INFINITY;
+      if (p0 + u * nw < npass && j[u] < R && sub < splits) {
+        const size_t i = ((size_t)b * R + j[u]) * splits + sub;
+        a[u].m = pm[i];
+        a[u].s = ps[i];
+        a[u].bv = pbv[i];
+        a[u].bi = pbi[i];
+        lt[u] = pd[i];
       }
     }
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      if (s0 + u < splits) {
-        if (s0 + u == 0) a = o[u];
-        else stat_merge(a, o[u], c);
+    for (int u = 0; u < 2; ++u) {
+      for (int msk = 1; msk < S2; msk <<= 1) {
+        const Stat o = stat_shfl_xor(a[u], msk);
+        stat_merge(a[u], o, c);
+        lt[u] = fmaxf(lt[u], __shfl_xor(lt[u], msk, kWave));
+      }
+      if (sub == 0 && p0 + u * nw < npass && j[u] < R) {
+        s_amax[j[u]] = a[u].bi;
+        if (j[u] < Kd) {
+          const float q = drafted_q(a[u], lt[u], c);
+          s_q[j[u]] = q;
+          if (q_out != nullptr) q_out[(size_t)b * Kd + j[u]] = q;
+        }
       }
     }
   }
 }
 
-__device__ __forceinline__ float drafted_q(const Stat& a, float lt, float c) {
-  return (lt > -INFINITY) ? (float)((double)exp2f((lt - a.m) * c) / a.s) : 0.f;
-}
-
-__global__ __launch_bounds__(256) void verify_scan_kernel(
+__global__ __launch_bounds__(kScanThreads) void verify_scan_kernel(
     int K, int R, int splits, float r, float c, const float* __restrict__ pm,
     const double* __restrict__ ps, const float* __restrict__ pbv, const int* __restrict__ pbi,
     const float* __restrict__ pd, int32_t* __restrict__ accept_len,
     int32_t* __restrict__ next_token, float* __restrict__ p_draft) {
   __shared__ float s_q[kMaxRows];
   __shared__ int s_amax[kMaxRows];
+  __shared__ int s_first;
   const int b = blockIdx.x;
-  for (int j = threadIdx.x; j < R; j += blockDim.x) {
-    Stat a;
-    float lt;
-    merge_row((size_t)b * R + j, splits, c, pm, ps, pbv, pbi, pd, a, lt);
-    s_amax[j] = a.bi;
-    if (j < K) {
-      const float q = drafted_q(a, lt, c);
-      s_q[j] = q;
-      if (p_draft != nullptr) p_draft[(size_t)b * K + j] = q;
-    }
-  }
+  if (threadIdx.x == 0) s_first = K;
+  merge_rows(b, R, K, splits, c, pm, ps, pbv, pbi, pd, s_q, s_amax, p_draft);
+  __syncthreads();
+  // first rejection: the lowest j < K with q_j < r
+  for (int j = threadIdx.x; j < K; j += blockDim.x)
+    if (s_q[j] < r) atomicMin(&s_first, j);
   __syncthreads();
   if (threadIdx.x == 0) {
-    int acc = K;
-    for (int j = 0; j < K; ++j) {
-      if (s_q[j] < r) {
-        acc = j;
-        break;
-      }
-    }
+    const int acc = s_first;
     accept_len[b] = acc;
     next_token[b] = (acc < K) ? s_amax[acc] : ((R == K + 1) ? s_amax[K] : -1);
   }
 }
 
 // Tree verification (Sec. 4, hardware-friendly tree building): rows [i * W + w] are the
-// nodes of step i, then W bonus rows if given. Each leaf's path is walked back through the
-// parent links, its advance is the first step whose node has q < r (else K), and the leaf
+// nodes of step i, then W bonus rows if given. Each leaf's root path is walked back through
+// the parent links; its advance is the first step whose node has q < r (else K), and the leaf
 // with the longest advance (lowest slot on ties) is kept.
-__global__ __launch_bounds__(256) void tree_scan_kernel(
+__global__ __launch_bounds__(kScanThreads) void tree_scan_kernel(
     int K, int W, int bonus, const int32_t* __restrict__ parents, int splits, float r, float c,
     const float* __restrict__ pm, const double* __restrict__ ps, const float* __restrict__ pbv,
     const int* __restrict__ pbi, const float* __restrict__ pd, int32_t* __restrict__ best_leaf,
@@ -247,50 +263,34 @@ __global__ __launch_bounds__(256) void tree_scan_kernel(
   __shared__ int s_amax[kMaxRows];
   __shared__ int s_par[kMaxRows];
   __shared__ int s_path[kMaxRows];
-  __shared__ int s_adv[kMaxTreeW];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int KW = K * W, R = KW + (bonus ? W : 0);
-  for (int j = tid; j < R; j += blockDim.x) {
-    Stat a;
-    float lt;
-    merge_row((size_t)b * R + j, splits, c, pm, ps, pbv, pbi, pd, a, lt);
-    s_amax[j] = a.bi;
-    if (j < KW) {
-      const float q = drafted_q(a, lt, c);
-      s_q[j] = q;
-      if (q_out != nullptr) q_out[(size_t)b * KW + j] = q;
-      s_par[j] = parents[(size_t)b * KW + j];
-    }
-  }
+  for (int j = tid; j < KW; j += blockDim.x) s_par[j] = parents[(size_t)b * KW + j];
+  merge_rows(b, R, KW, splits, c, pm, ps, pbv, pbi, pd, s_q, s_amax, q_out);
   __syncthreads();
-  if (tid < W) {
-    int w = tid;
-    for (int i = K - 1; i >= 0; --i) {
-      s_path[tid * K + i] = w;
-      if (i > 0) {
-        const int p = s_par[i * W + w];
-        w = (p >= 0 && p < W) ? p : 0;  // links outside [0, W) are a caller error; stay in bounds
+  if (tid < kWave) {  // wave 0: lane w walks leaf w's path (W <= 64)
+    int adv = K, w = tid;
+    if (tid < W) {
+      for (int i = K - 1; i >= 0; --i) {
+        s_path[tid * K + i] = w;
+        if (s_q[i * W + w] < r) adv = i;  // the last one set is the first on the path
+        if (i > 0) {
+          const int p = s_par[i * W + w];
+          w = (p >= 0 && p < W) ? p : 0;  // links outside [0, W) are a caller error; stay in bounds
+        }
       }
     }
-    int adv = K;
-    for (int i = 0; i < K; ++i) {
-      if (s_q[i * W + s_path[tid * K + i]] < r) {
-        adv = i;
-        break;
-      }
+    // longest advance, lowest slot on ties: the largest of adv * 128 + (127 - slot)
+    int key = (tid < W) ? adv * 128 + (127 - tid) : -1;
+#pragma unroll
+    for (int k = 1; k < kWave; k <<= 1) key = max(key, __shfl_xor(key, k, kWave));
+    if (tid == 0) {
+      const int best = 127 - (key & 127), acc = key >> 7;
+      best_leaf[b] = best;
+      accept_len[b] = acc;
+      next_token[b] = (acc < K) ? s_amax[acc * W + s_path[best * K + acc]]
+                                : (bonus ? s_amax[KW + best] : -1);
     }
-    s_adv[tid] = adv;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int best = 0;
-    for (int w = 1; w < W; ++w)
-      if (s_adv[w] > s_adv[best]) best = w;
-    const int acc = s_adv[best];
-    best_leaf[b] = best;
-    accept_len[b] = acc;
-    next_token[b] = (acc < K) ? s_amax[acc * W + s_path[best * K + acc]]
-                              : (bonus ? s_amax[KW + best] : -1);
   }
 }
 
@@ -300,7 +300,7 @@ VerifyLayout verify_layout(int B, int R, int V) {
   VerifyLayout L{};
   const int rows = std::max(1, B * R);
   int splits = ceil_div(kTargetBlocks, rows);
-  splits = std::max(1, std::min(splits, ceil_div(V, kMinSegment)));
+  splits = std::max(1, std::min(std::min(splits, ceil_div(V, kMinSegment)), kMaxSplits));
   L.splits = splits;
   const size_t n = (size_t)rows * splits;
   Carve c;
@@ -354,7 +354,7 @@ hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const 
   hipError_t e = launch_stats(logits, B, R, V, drafted, K, c, ws, L, stream, &P, "verify_stats");
   if (e != hipSuccess) return e;
   ProfScope prof("verify_scan", stream);
-  verify_scan_kernel<<<B, 256, 0, stream>>>(K, R, L.splits, r, c, P.pm, P.ps, P.pbv, P.pbi, P.pd,
+  verify_scan_kernel<<<B, kScanThreads, 0, stream>>>(K, R, L.splits, r, c, P.pm, P.ps, P.pbv, P.pbi, P.pd,
                                             accept_len, next_token, p_draft);
   return hipGetLastError();
 }
@@ -371,7 +371,7 @@ hipError_t launch_tree_verify(const float* logits, int B, int K, int W, int V, i
   hipError_t e = launch_stats(logits, B, R, V, tokens, K * W, c, ws, L, stream, &P, "tree_stats");
   if (e != hipSuccess) return e;
   ProfScope prof("tree_scan", stream);
-  tree_scan_kernel<<<B, 256, 0, stream>>>(K, W, bonus, parents, L.splits, r, c, P.pm, P.ps, P.pbv,
+  tree_scan_kernel<<<B, kScanThreads, 0, stream>>>(K, W, bonus, parents, L.splits, r, c, P.pm, P.ps, P.pbv,
                                           P.pbi, P.pd, best_leaf, accept_len, next_token, q);
   return hipGetLastError();
 }

@@ -152,6 +152,7 @@ def test_tree_build_argument_errors(L):
     assert call(a7=None) == -1         # tokens NULL
     assert call(a9=FAKE) == -1 and "alias" in _err(L)
     assert call(a11=16) == -2          # workspace too small
+    assert call(a0=ctypes.c_void_p((1 << 20) + 4)) == -1 and "aligned" in _err(L)
     assert call(a1=20000) == -1 and "rows" in _err(L)  # B * Wc above the grid limit
     assert call(a4=None, a1=0) == 0    # cum_ll may be NULL
     assert call(a1=0) == 0             # empty batch

@@ -78,7 +78,8 @@ def test_build_inner_step(sr, wc, width):
 
 
 def test_build_small_and_ragged_vocab(sr):
-    for vocab, width in ((16, 16), (17, 16), (5, 3), (2, 5), (2049, 8), (4097, 8), (130000, 2)):
+    for vocab, width in ((16, 16), (17, 16), (5, 3), (2, 5), (2049, 8), (4097, 8), (130000, 2), (300000, 4),
+                         (262147, 3)):
         say(f"tree build V={vocab} W={width}")
         lg, cum = tree_build_inputs(vocab, 2, 3, vocab, 1.0)
         _build_and_check(sr, lg, cum, width, 1.0)

@@ -91,3 +91,11 @@ def test_ties_in_argmax_across_segments(sr):
     dr = np.array([[3]], dtype=np.int32)
     acc, nxt, _ = sr.sirius_verify_accept(dev_f32(lg), dev_i32(dr), 0.5, 1.0)
     assert int(host(acc)[0]) == 0 and int(host(nxt)[0]) == 9000
+
+
+def test_long_rows_cap_the_segment_count(sr):
+    # a single long row: more than 64 segments of 2048 would be wanted; the count is capped
+    for v, rows in ((300000, 2), (262147, 2)):
+        say(f"verify V={v}")
+        lg, dr = verify_inputs(40, 2, 1, v, 3.0, rows=rows, calibrated=True)
+        _run_and_check(sr, lg, dr, 0.1, 1.0)
