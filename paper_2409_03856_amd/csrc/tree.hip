@@ -27,12 +27,13 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "softmax.h"
 
 namespace sirius {
 namespace {
 
 constexpr int kTopThreads = 256;
-constexpr int kElems = 16;                         // contiguous logits per thread per pass
+constexpr int kElems = 16;  // contiguous logits per thread per pass (the stats sum assumes 16)
 constexpr int kPassElems = kTopThreads * kElems;   // 4096 logits per workgroup pass
 constexpr int kKW = 16;          // tree width and current-leaf limit (list length in registers)
 constexpr int kMaxSplits = 64;   // segments per leaf row at most (one lane each in the select)
@@ -139,10 +140,13 @@ __global__ __launch_bounds__(kTopThreads) void tree_topw_kernel(
     float cm = m;
 #pragma unroll
     for (int j = 0; j < kElems; ++j) cm = fmaxf(cm, v[j]);
-    double cs = (s > 0.0) ? s * (double)exp2f((m - cm) * c) : 0.0;
+    float t[kElems / 4];  // the pass's exps, summed pairwise in fp32 (16 terms, each <= 1)
 #pragma unroll
-    for (int j = 0; j < kElems; ++j)
-      if (v[j] > -INFINITY) cs += (double)exp2f((v[j] - cm) * c);
+    for (int g = 0; g < kElems / 4; ++g)
+      t[g] = (exp2_nonpos((v[4 * g] - cm) * c) + exp2_nonpos((v[4 * g + 1] - cm) * c)) +
+             (exp2_nonpos((v[4 * g + 2] - cm) * c) + exp2_nonpos((v[4 * g + 3] - cm) * c));
+    double cs = (s > 0.0) ? s * (double)exp2_nonpos((m - cm) * c) : 0.0;
+    if (cm > -INFINITY) cs += (double)((t[0] + t[1]) + (t[2] + t[3]));  // -inf logits add nothing
     m = cm;
     s = cs;
     // keys; the largest key of each of G thread groups (group = thread index mod G, G the

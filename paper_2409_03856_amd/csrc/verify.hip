@@ -20,6 +20,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "softmax.h"
 
 namespace sirius {
 namespace {
@@ -63,34 +64,50 @@ __device__ __forceinline__ Stat stat_shfl_xor(const Stat& v, int mask) {
   return o;
 }
 
-// Fold G groups of 4 logits (group g starts at index i0[g]) into the running stat:
-// one max over all of them, one rescale of the running sum, then the exps.
+// Fold G groups of 4 logits (group g starts at index i0[g], groups in increasing index order)
+// into the running stat: one max over all of them and one rescale of the running sum; the
+// chunk's exps are summed pairwise in fp32 (at most 4 G terms, each at most 1) and added to the
+// fp64 sum. The argmax is looked up only when the chunk raises the maximum: the first index
+// holding the new maximum (ties with earlier chunks keep the earlier, lower index).
 template <int G>
 __device__ __forceinline__ void stat_fold(Stat& st, const float4* v, const int* i0, float c) {
   float m = st.m;
 #pragma unroll
   for (int g = 0; g < G; ++g) m = fmaxf(fmaxf(m, fmaxf(v[g].x, v[g].y)), fmaxf(v[g].z, v[g].w));
-  double s = (st.s > 0.0) ? st.s * (double)exp2f((st.m - m) * c) : 0.0;
+  if (m > st.m) {
+    int bi = st.bi;
+#pragma unroll
+    for (int g = G - 1; g >= 0; --g) {
+      bi = (v[g].w == m) ? i0[g] + 3 : bi;
+      bi = (v[g].z == m) ? i0[g] + 2 : bi;
+      bi = (v[g].y == m) ? i0[g] + 1 : bi;
+      bi = (v[g].x == m) ? i0[g] : bi;
+    }
+    st.bv = m;
+    st.bi = bi;
+  }
+  float t[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const float e[4] = {v[g].x, v[g].y, v[g].z, v[g].w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      s += (double)exp2f((e[q] - m) * c);
-      if (e[q] > st.bv) {
-        st.bv = e[q];
-        st.bi = i0[g] + q;
-      }
-    }
+    const float a = exp2_nonpos((v[g].x - m) * c) + exp2_nonpos((v[g].y - m) * c);
+    const float b = exp2_nonpos((v[g].z - m) * c) + exp2_nonpos((v[g].w - m) * c);
+    t[g] = a + b;
   }
+#pragma unroll
+  for (int w = 1; w < G; w <<= 1) {
+#pragma unroll
+    for (int g = 0; g + w < G; g += 2 * w) t[g] += t[g + w];
+  }
+  double s = (st.s > 0.0) ? st.s * (double)exp2_nonpos((st.m - m) * c) : 0.0;
+  if (m > -INFINITY) s += (double)t[0];  // a chunk of -inf logits adds nothing
   st.m = m;
   st.s = s;
 }
 
 __device__ __forceinline__ void stat_fold1(Stat& st, float v, int i, float c) {
   const float m = fmaxf(st.m, v);
-  double s = (st.s > 0.0) ? st.s * (double)exp2f((st.m - m) * c) : 0.0;
-  s += (double)exp2f((v - m) * c);
+  double s = (st.s > 0.0) ? st.s * (double)exp2_nonpos((st.m - m) * c) : 0.0;
+  if (v > -INFINITY) s += (double)exp2_nonpos((v - m) * c);
   if (v > st.bv) {
     st.bv = v;
     st.bi = i;
