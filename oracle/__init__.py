@@ -2,7 +2,8 @@
 
 A plain, slow, float64 NumPy statement of what the GPU library computes:
 
-  * ffn      -- dense SwiGLU FFN, CATS-style threshold sparsity (FSparse),
+  * ffn      -- dense SwiGLU FFN, CATS-style threshold sparsity and the
+                paper's per-token top-k variant (FSparse),
                 Griffin-style prompt-chosen top-k neurons (CSparse) with
                 condensed weights, threshold calibration, RMSNorm layer stack;
   * verify   -- the full model's likelihood check of drafted tokens:
@@ -32,6 +33,8 @@ from .ffn import (  # noqa: F401
     ffn_dense,
     gate_activations,
     cats_active_sets,
+    topk_active_sets,
+    ffn_topk,
     ffn_masked,
     ffn_cats,
     calibrate_threshold,

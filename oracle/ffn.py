@@ -109,6 +109,35 @@ def ffn_cats(x, w_gate, w_up, w_down, t: float):
     return ffn_masked(x, w_gate, w_up, w_down, sets), sets
 
 
+def topk_active_sets(x, w_gate, k: int):
+    """Per-token top-k neuron sets: the paper's own fine-grained implementation.
+
+    The paper replaces CATS's threshold by a top-k over the gate layer's
+    activations, so that every token keeps exactly the target density, and
+    implements the rest as CATS does (Sec. 3, footnote on the fine-grained
+    implementation). Reading adopted: for each token, the k neurons with the
+    largest |SiLU(g_bi)| (the magnitude CATS thresholds), ties to the lower
+    neuron index. Returns ascending int64 index arrays (one per row of x) and
+    the gate activations a [B, d_ff].
+    """
+    a = gate_activations(x, w_gate)
+    f = a.shape[1]
+    if not 1 <= k <= f:
+        raise ValueError("k must lie in [1, d_ff]")
+    idx = np.arange(f)
+    sets = []
+    for b in range(a.shape[0]):
+        order = np.lexsort((idx, -np.abs(a[b])))  # primary key: larger |a|; then lower index
+        sets.append(np.sort(order[:k]))
+    return sets, a
+
+
+def ffn_topk(x, w_gate, w_up, w_down, k: int):
+    """Per-token top-k sparse FFN: returns (y [B, d_model], active sets)."""
+    sets, _ = topk_active_sets(x, w_gate, k)
+    return ffn_masked(x, w_gate, w_up, w_down, sets), sets
+
+
 def calibrate_threshold(x_cal, w_gate, q: float) -> float:
     """Threshold t for target sparsity q from calibration inputs.
 
