@@ -59,6 +59,7 @@ extern "C" {
 #define SIRIUS_OP_CATS_CALIBRATE 5
 #define SIRIUS_OP_TREE_BUILD 6
 #define SIRIUS_OP_TREE_VERIFY 7
+#define SIRIUS_OP_FFN_TOPK 8
 
 /*
  * Dense SwiGLU FFN (the full model, sparsity 0):
@@ -101,6 +102,26 @@ int sirius_ffn_dense(const float* x, int B, const uint16_t* w_gate, const uint16
  */
 int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
                     const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                    const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Per-token top-k sparse FFN, the paper's own fine-grained (FSparse)
+ * implementation (Sec. 3, footnote on the fine-grained implementation): in
+ * place of CATS's threshold, every token keeps exactly the k neurons of
+ * largest |SiLU(W_gate[i].xn)| (ties to the lower neuron index); the gate is
+ * read whole, W_up and W_down only for the kept neurons:
+ *   y[b] = resid[b] + sum_{i in A_b} SiLU(W_gate[i].xn[b]) (W_up[i].xn[b]) W_down[i]
+ * with xn as for sirius_ffn_dense. The gate activations are computed in
+ * fp32 (bf16 weights x fp32 inputs), the selection is taken on those values.
+ *   x, resid, y   as for sirius_ffn_cats.
+ *   active_idx    [B, d_ff] int32 out: row b starts with the ascending A_b
+ *                 (k entries), or NULL (then active_cnt must be NULL too).
+ *   active_cnt    [B] int32 out: k, or NULL.
+ * Errors: as for sirius_ffn_cats, and SIRIUS_EINVAL for k outside [1, d_ff].
+ */
+int sirius_ffn_topk(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                    const uint16_t* w_down, int d_model, int d_ff, int k, float norm_eps,
                     const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
                     void* ws, size_t ws_bytes, void* stream);
 
@@ -254,7 +275,8 @@ int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, 
  * "ffn_mfma_gate_up", "verify_stats", "verify_scan", "griffin_z",
  * "griffin_rownorm", "griffin_score", "select_init", "select_hist",
  * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal",
- * "tree_topw", "tree_select", "tree_stats", "tree_scan".
+ * "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate",
+ * "topk_cut", "topk_decode", "topk_up", "topk_down", "topk_reduce".
  * sirius_profile_reset drops every record (it waits for pending events).
  * Errors: SIRIUS_EINVAL for NULL arguments, SIRIUS_EHIP if an event fails.
  */
@@ -263,7 +285,8 @@ int sirius_profile_reset(void);
 int sirius_profile_query(const char* kernel, double* total_ms, int64_t* launches);
 
 /* Workspace bytes needed by an operation (SIRIUS_OP_*). Arguments:
- *   FFN_DENSE / FFN_CATS / FFN_CONDENSED: B, d_model, d_ff (= k), unused, unused
+ *   FFN_DENSE / FFN_CATS / FFN_CONDENSED / FFN_TOPK: B, d_model, d_ff (= k for
+ *     the condensed layer), unused, unused
  *   CATS_CALIBRATE: N, d_model, d_ff, unused, unused
  *   GRIFFIN_SELECT: unused, d_model, d_ff, T, unused
  *   VERIFY: B, unused, unused, V, R (rows per batch entry)

@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     workspace,
     sirius_ffn_dense,
     sirius_ffn_cats,
+    sirius_ffn_topk,
     sirius_cats_calibrate,
     sirius_griffin_select,
     sirius_ffn_condensed,
@@ -34,4 +35,5 @@ from ._lib import (  # noqa: F401
     OP_CATS_CALIBRATE,
     OP_TREE_BUILD,
     OP_TREE_VERIFY,
+    OP_FFN_TOPK,
 )

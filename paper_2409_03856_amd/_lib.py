@@ -29,6 +29,7 @@ OP_VERIFY = 4
 OP_CATS_CALIBRATE = 5
 OP_TREE_BUILD = 6
 OP_TREE_VERIFY = 7
+OP_FFN_TOPK = 8
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -39,6 +40,7 @@ _Z = ctypes.c_size_t
 SIGNATURES = {
     "sirius_ffn_dense": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
     "sirius_ffn_cats": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "sirius_ffn_topk": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_cats_calibrate": (_I, [_P, _I, _P, _I, _I, ctypes.c_double, _P, _P, _Z, _P]),
     "sirius_griffin_select": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_ffn_condensed": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
@@ -194,6 +196,30 @@ def sirius_ffn_cats(x, w_gate, w_up, w_down, t, *, norm_eps=-1.0, resid=None, y=
     if ws is None:
         ws = workspace(OP_FFN_CATS, max(bsz, 1), d, f, device=x.device)
     _check(lib().sirius_ffn_cats(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, float(t),
+                                 float(norm_eps), _ptr(resid), _ptr(y), _ptr(active_idx), _ptr(active_cnt),
+                                 _ptr(ws), ws.numel(), _stream(stream)))
+    return y, active_idx, active_cnt
+
+
+def sirius_ffn_topk(x, w_gate, w_up, w_down, k, *, norm_eps=-1.0, resid=None, y=None, active_idx=None,
+                    active_cnt=None, want_active=True, ws=None, stream=None):
+    """Per-token top-k sparse FFN. x [B, d_model] fp32; weights bf16 [d_ff, d_model].
+    Returns (y, active_idx [B, d_ff] or None, active_cnt [B] or None)."""
+    torch = _torch()
+    _need(x.dtype == torch.float32 and x.dim() == 2, "x must be fp32 [B, d_model]")
+    d, f = _w_dims(w_gate, w_up, w_down)
+    bsz = int(x.shape[0])
+    _need(int(x.shape[1]) == d, "x and the weights disagree on d_model")
+    dev = x.device
+    if y is None:
+        y = torch.empty((bsz, d), dtype=torch.float32, device=dev)
+    if want_active and active_idx is None:
+        active_idx = torch.empty((bsz, f), dtype=torch.int32, device=dev)
+        active_cnt = torch.empty(bsz, dtype=torch.int32, device=dev)
+    _dev_check(x, w_gate, w_up, w_down, resid, y, active_idx, active_cnt)
+    if ws is None:
+        ws = workspace(OP_FFN_TOPK, max(bsz, 1), d, f, device=dev)
+    _check(lib().sirius_ffn_topk(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, int(k),
                                  float(norm_eps), _ptr(resid), _ptr(y), _ptr(active_idx), _ptr(active_cnt),
                                  _ptr(ws), ws.numel(), _stream(stream)))
     return y, active_idx, active_cnt

@@ -145,6 +145,9 @@ size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, i
     case SIRIUS_OP_VERIFY:
       if (B < 0 || T_or_V < 1 || K_or_R < 1 || K_or_R > kMaxVerifyRows) return 0;
       return sirius::verify_layout(std::max(B, 1), K_or_R, T_or_V).total;
+    case SIRIUS_OP_FFN_TOPK:
+      if (B < 0 || B > kMaxBatch || !dims_ok(d_model, d_ff)) return 0;
+      return sirius::topk_layout(std::max(B, 1), d_model, d_ff).total;
     case SIRIUS_OP_TREE_BUILD:
       if (B < 0 || d_model < 1 || d_model > kMaxTreeBuildW || d_ff < 1 || d_ff > kMaxTreeBuildW ||
           T_or_V < 1 || (long)d_model * T_or_V < d_ff)
@@ -193,8 +196,33 @@ int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_
   const size_t need = gemv_ws(B, d_model, d_ff);
   if (ws_bytes < need)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
-  return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, /*mode=*/1, t, norm_eps, resid,
+  return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, sirius::kFfnModeThreshold, t, norm_eps, resid,
                       y, active_idx, active_cnt, ws, static_cast<hipStream_t>(stream));
+}
+
+int sirius_ffn_topk(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                    const uint16_t* w_down, int d_model, int d_ff, int k, float norm_eps,
+                    const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                    void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_ffn_topk";
+  int rc = check_ffn_dims(fn, B, d_model, d_ff);
+  if (rc) return rc;
+  if ((rc = check_ptrs(fn, {{x, "x"}, {w_gate, "w_gate"}, {w_up, "w_up"}, {w_down, "w_down"}, {y, "y"}, {ws, "ws"}})))
+    return rc;
+  if (resid != nullptr && !aligned16(resid)) return fail(SIRIUS_EINVAL, "%s: resid is not 16-byte aligned", fn);
+  if ((active_idx == nullptr) != (active_cnt == nullptr))
+    return fail(SIRIUS_EINVAL, "%s: active_idx and active_cnt must both be given or both be NULL", fn);
+  if (k < 1 || k > d_ff) return fail(SIRIUS_EINVAL, "%s: k=%d outside [1, d_ff=%d]", fn, k, d_ff);
+  if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
+  if (B == 0) return SIRIUS_OK;
+  const sirius::TopkLayout L = sirius::topk_layout(B, d_model, d_ff);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_ffn_topk(x, B, w_gate, w_up, w_down, d_model, d_ff, k, norm_eps,
+                                            resid, y, active_idx, active_cnt,
+                                            static_cast<char*>(ws), L,
+                                            static_cast<hipStream_t>(stream)),
+                    fn);
 }
 
 int sirius_cats_calibrate(const float* x_cal, int N, const uint16_t* w_gate, int d_model, int d_ff,

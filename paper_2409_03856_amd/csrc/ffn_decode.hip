@@ -1,6 +1,6 @@
-// Batch-1 SwiGLU FFN decode on gfx950 in one pass per row segment: dense, condensed and
+// Batch-1 SwiGLU FFN decode on gfx950 in one pass per row segment: dense, condensed,
 // per-token threshold sparsity (FSparse after CATS: the gate is read whole, W_up and W_down
-// only for the kept neurons).
+// only for the kept neurons) and the second pass of per-token top-k sparsity.
 //
 //  decode1_kernel  one 1024-thread workgroup (16 waves) per segment of contiguous neuron
 //                  rows, one workgroup per CU. In order:
@@ -24,6 +24,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "topk.h"
 
 namespace sirius {
 namespace {
@@ -36,7 +37,9 @@ constexpr int kMaxRows = 256;             // rows per segment at most: d_ff <= 6
 constexpr int kMaxD = 8192;               // x staged in LDS: 32 KiB
 constexpr int kDownUnroll = 8;            // W_down row chunks in flight per thread
 
-constexpr int kModeDense = 0, kModeSparse = 1;
+// kModeKeyed: per-token top-k; the gate activations come from a separate gate pass, and a
+// neuron is kept iff its top-k key reaches the token's cut (no W_gate read here).
+constexpr int kModeDense = 0, kModeSparse = 1, kModeKeyed = 2;
 
 template <int CPL>
 __device__ __forceinline__ void load_row(uint4 (&w)[CPL], const uint4* row, int lane, int nch,
@@ -65,7 +68,8 @@ template <int CPL, int MODE>
 __global__ __launch_bounds__(kThreads) void decode1_kernel(
     const float* __restrict__ x, const uint4* __restrict__ wg, const uint4* __restrict__ wu,
     const uint4* __restrict__ wd, int d, int F, float t, float norm_eps, int rmax,
-    int32_t* __restrict__ uidx, int32_t* __restrict__ ucnt, float* __restrict__ part) {
+    int32_t* __restrict__ uidx, int32_t* __restrict__ ucnt, float* __restrict__ part,
+    const float* __restrict__ act, const unsigned long long* __restrict__ cut) {
   // x (normalised) during gate and up; the down phase's row-group partials afterwards
   __shared__ float4 s_x4[kMaxD / 4];
   __shared__ float s_a[kMaxRows];
@@ -84,7 +88,7 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
   const int nr = (int)(((long long)F * (seg + 1)) / G) - r0;  // 1 <= nr <= rmax <= kMaxRows
 
   uint4 wa[CPL], wb[CPL];
-  load_row(wa, wg + (size_t)(r0 + wave) * nch, lane, nch, wave < nr);
+  load_row(wa, wg + (size_t)(r0 + wave) * nch, lane, nch, MODE != kModeKeyed && wave < nr);
 
   // ---- x into LDS, RMS-normalised when norm_eps >= 0
   float ss = 0.f;
@@ -124,7 +128,15 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
       s_keep[j] = (MODE == kModeDense || fabsf(a) > t) ? 1 : 0;
     }
   };
-  for (int j = wave; j < nr; j += NB * kWaves) {
+  if (MODE == kModeKeyed) {
+    const unsigned long long c0 = cut[0];
+    for (int j = tid; j < nr; j += kThreads) {
+      const float a = act[r0 + j];
+      s_a[j] = a;
+      s_keep[j] = topk_key(a, r0 + j) >= c0 ? 1 : 0;
+    }
+  }
+  for (int j = wave; MODE != kModeKeyed && j < nr; j += NB * kWaves) {
     if (NB == 2) {
       const int j1 = j + kWaves, j2 = j + 2 * kWaves;
       load_row(wb, wg + (size_t)(r0 + j1) * nch, lane, nch, j1 < nr);
@@ -221,11 +233,12 @@ int pow2_cpl(int nch) {
 template <int MODE>
 hipError_t launch_mode(int cpl, int G, hipStream_t s, const float* x, const uint4* wg,
                        const uint4* wu, const uint4* wd, int d, int F, float t, float norm_eps,
-                       int rmax, int32_t* uidx, int32_t* ucnt, float* part) {
+                       int rmax, int32_t* uidx, int32_t* ucnt, float* part, const float* act,
+                       const unsigned long long* cut) {
 #define SIRIUS_DECODE1(CPLV)                                                                    \
   case CPLV:                                                                                    \
     decode1_kernel<CPLV, MODE><<<G, kThreads, 0, s>>>(x, wg, wu, wd, d, F, t, norm_eps, rmax,    \
-                                                      uidx, ucnt, part);                        \
+                                                      uidx, ucnt, part, act, cut);              \
     break;
   switch (cpl) {
     SIRIUS_DECODE1(1)
@@ -258,8 +271,10 @@ hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t
                               const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                               const float* resid, float* y, int32_t* active_idx,
                               int32_t* active_cnt, char* ws, const Decode1Layout& L,
-                              hipStream_t stream) {
+                              hipStream_t stream, const float* act,
+                              const unsigned long long* cut) {
   if (d > kMaxD || (d & 7) != 0 || L.rmax > kMaxRows || L.nseg > kSegs) return hipErrorInvalidValue;
+  if (mode == kFfnModeTopK && (act == nullptr || cut == nullptr)) return hipErrorInvalidValue;
   int32_t* uidx = reinterpret_cast<int32_t*>(ws + L.uidx);
   int32_t* ucnt = reinterpret_cast<int32_t*>(ws + L.ucnt);
   float* part = reinterpret_cast<float*>(ws + L.part);
@@ -267,18 +282,23 @@ hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t
   const uint4* wu4 = reinterpret_cast<const uint4*>(wu);
   const uint4* wd4 = reinterpret_cast<const uint4*>(wd);
   const int cpl = pow2_cpl(d / 8);
-  const bool sparse = mode == kModeSparse;
+  const bool thr = mode == kFfnModeThreshold, topk = mode == kFfnModeTopK;
   hipError_t e;
   {
-    ProfScope prof(sparse ? "cats_decode" : "dense_decode", stream);
-    e = sparse ? launch_mode<kModeSparse>(cpl, L.nseg, stream, x, wg4, wu4, wd4, d, F, t,
-                                          norm_eps, L.rmax, uidx, ucnt, part)
-               : launch_mode<kModeDense>(cpl, L.nseg, stream, x, wg4, wu4, wd4, d, F, t,
-                                         norm_eps, L.rmax, uidx, ucnt, part);
+    ProfScope prof(topk ? "topk_decode" : (thr ? "cats_decode" : "dense_decode"), stream);
+    if (topk)
+      e = launch_mode<kModeKeyed>(cpl, L.nseg, stream, x, wg4, wu4, wd4, d, F, t, norm_eps, L.rmax,
+                                  uidx, ucnt, part, act, cut);
+    else if (thr)
+      e = launch_mode<kModeSparse>(cpl, L.nseg, stream, x, wg4, wu4, wd4, d, F, t, norm_eps,
+                                   L.rmax, uidx, ucnt, part, nullptr, nullptr);
+    else
+      e = launch_mode<kModeDense>(cpl, L.nseg, stream, x, wg4, wu4, wd4, d, F, t, norm_eps, L.rmax,
+                                  uidx, ucnt, part, nullptr, nullptr);
     if (e != hipSuccess) return e;
   }
-  ProfScope prof(sparse ? "cats_reduce" : "dense_reduce", stream);
-  if (sparse && active_idx != nullptr)
+  ProfScope prof(topk ? "topk_reduce" : (thr ? "cats_reduce" : "dense_reduce"), stream);
+  if (mode != kFfnModeDense && active_idx != nullptr)
     return launch_reduce(part, L.nseg, 1, d, resid, y, stream, F, L.nseg, L.rmax, uidx, ucnt,
                          active_idx, active_cnt);
   return launch_reduce(part, L.nseg, 1, d, resid, y, stream);

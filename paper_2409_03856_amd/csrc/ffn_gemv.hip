@@ -33,6 +33,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "topk.h"
 
 namespace sirius {
 namespace {
@@ -54,14 +55,18 @@ constexpr int kRedGroups = 256 / kRedOut4;  // partial-row groups per reduce wor
 constexpr int kRedUnroll = 8;               // partial rows in flight per reduce thread
 constexpr int kXLdsFloats = 32768;          // fp32 x staged in LDS: 128 KiB (LDS is 160 KiB)
 
-constexpr int kModeDense = 0, kModeSparse = 1, kModeAbsAct = 2;
+// kModeAct writes the signed gate activations and stops; kModeKeyed takes them (and a per-token
+// top-k key cut) from that pass instead of reading W_gate again.
+constexpr int kModeDense = 0, kModeSparse = 1, kModeAbsAct = 2, kModeAct = 3, kModeKeyed = 4;
+constexpr bool writes_act(int mode) { return mode == kModeAbsAct || mode == kModeAct; }
 
 template <int BM, int CPL, int MODE>
 __global__ __launch_bounds__(256) void gate_kernel(
     const float* __restrict__ x, int B, const uint4* __restrict__ wg, const uint4* __restrict__ wu,
     int d, int F, float t, float norm_eps, int rmax, int32_t* __restrict__ uidx,
     float* __restrict__ hbuf, int32_t* __restrict__ ucnt, int32_t* __restrict__ bidx,
-    int32_t* __restrict__ bcnt, float* __restrict__ absact) {
+    int32_t* __restrict__ bcnt, float* __restrict__ absact,
+    const unsigned long long* __restrict__ cut) {
   extern __shared__ float xs[];  // [B][d] fp32
   __shared__ float s_a[kMaxSeg * BM];
   __shared__ uint32_t s_flag[kMaxSeg];
@@ -121,8 +126,21 @@ __global__ __launch_bounds__(256) void gate_kernel(
   __syncthreads();
 
   uint4 w[kRPW][CPL];
+  if (MODE == kModeKeyed) {
+    // ---- phase a from the stored activations: kept iff the top-k key reaches the cut
+    for (int j = tid; j < nr; j += 256) {
+      uint32_t fl = 0u;
+#pragma unroll
+      for (int b = 0; b < BM; ++b) {
+        const float a = (b < B) ? absact[(size_t)b * F + r0 + j] : 0.f;
+        if (b < B && topk_key(a, r0 + j) >= cut[b]) fl |= 1u << b;
+        s_a[j * BM + b] = a;
+      }
+      s_flag[j] = fl;
+    }
+  }
   // ---- phase a: gate rows j = wave, wave + 4, ... of the segment, kRPW rows in flight
-  for (int j0 = wave; j0 < nr; j0 += kRPW * kGateWaves) {
+  for (int j0 = wave; MODE != kModeKeyed && j0 < nr; j0 += kRPW * kGateWaves) {
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
       const int j = j0 + r * kGateWaves;
@@ -156,10 +174,10 @@ __global__ __launch_bounds__(256) void gate_kernel(
         if (b < B && (MODE == kModeDense || fabsf(a[b]) > t)) fl |= 1u << b;
       }
       if (lane == 0 && j < nr) {
-        if (MODE == kModeAbsAct) {
+        if (writes_act(MODE)) {
 #pragma unroll
           for (int b = 0; b < BM; ++b)
-            if (b < B) absact[(size_t)b * F + r0 + j] = fabsf(a[b]);
+            if (b < B) absact[(size_t)b * F + r0 + j] = (MODE == kModeAbsAct) ? fabsf(a[b]) : a[b];
         } else {
           s_flag[j] = fl;
 #pragma unroll
@@ -168,7 +186,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
       }
     }
   }
-  if (MODE == kModeAbsAct) return;  // uniform over the block
+  if (writes_act(MODE)) return;  // uniform over the block
   __syncthreads();
 
   // ---- compact the segment's kept rows (some token keeps them), ascending
@@ -176,7 +194,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
   int nkept;
   const int pos = block_exclusive_scan_256(myfl != 0u ? 1 : 0, s_tmp, &nkept);
   if (myfl != 0u) s_list[pos] = tid;
-  if (MODE == kModeSparse && bidx != nullptr) {
+  if ((MODE == kModeSparse || MODE == kModeKeyed) && bidx != nullptr) {
 #pragma unroll
     for (int b = 0; b < BM; ++b) {
       if (b < B) {
@@ -478,11 +496,12 @@ template <int BM, int MODE>
 hipError_t launch_gate_bm(int cpl, dim3 grid, size_t lds, hipStream_t s, const float* x, int B,
                           const uint4* wg, const uint4* wu, int d, int F, float t, float norm_eps,
                           int rmax, int32_t* uidx, float* hbuf, int32_t* ucnt, int32_t* bidx,
-                          int32_t* bcnt, float* absact) {
+                          int32_t* bcnt, float* absact, const unsigned long long* cut) {
 #define SIRIUS_GATE(CPLV)                                                                        \
   case CPLV:                                                                                     \
     gate_kernel<BM, CPLV, MODE><<<grid, 256, lds, s>>>(x, B, wg, wu, d, F, t, norm_eps, rmax,    \
-                                                       uidx, hbuf, ucnt, bidx, bcnt, absact);    \
+                                                       uidx, hbuf, ucnt, bidx, bcnt, absact,     \
+                                                       cut);                                     \
     break;
   switch (cpl) {
     SIRIUS_GATE(1)
@@ -501,12 +520,13 @@ template <int MODE>
 hipError_t launch_gate_mode(int bm, int cpl, dim3 grid, size_t lds, hipStream_t s, const float* x,
                             int B, const uint4* wg, const uint4* wu, int d, int F, float t,
                             float norm_eps, int rmax, int32_t* uidx, float* hbuf, int32_t* ucnt,
-                            int32_t* bidx, int32_t* bcnt, float* absact) {
+                            int32_t* bidx, int32_t* bcnt, float* absact,
+                            const unsigned long long* cut = nullptr) {
   switch (bm) {
-    case 1: return launch_gate_bm<1, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
-    case 2: return launch_gate_bm<2, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
-    case 4: return launch_gate_bm<4, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
-    case 8: return launch_gate_bm<8, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact);
+    case 1: return launch_gate_bm<1, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact, cut);
+    case 2: return launch_gate_bm<2, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact, cut);
+    case 4: return launch_gate_bm<4, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact, cut);
+    case 8: return launch_gate_bm<8, MODE>(cpl, grid, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax, uidx, hbuf, ucnt, bidx, bcnt, absact, cut);
     default: return hipErrorInvalidValue;
   }
 }
@@ -538,43 +558,50 @@ GemvLayout gemv_layout(int B, int d, int F) {
 hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                            const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
-                           char* ws, const GemvLayout& L, hipStream_t stream) {
+                           char* ws, const GemvLayout& L, hipStream_t stream, const float* act,
+                           const unsigned long long* cut) {
   if (B < 1 || B > L.bc || L.rmax > kMaxSeg || L.ntiles > kGateSegs) return hipErrorInvalidValue;
+  if (mode == kFfnModeTopK && (act == nullptr || cut == nullptr)) return hipErrorInvalidValue;
+  const bool topk = mode == kFfnModeTopK;
   const int bm = pow2_at_least(B, 8);
   const int cpl = pow2_at_least(ceil_div(d / 8, kWave), 16);
   int32_t* uidx = reinterpret_cast<int32_t*>(ws + L.uidx);
   float* hbuf = reinterpret_cast<float*>(ws + L.h);
   int32_t* ucnt = reinterpret_cast<int32_t*>(ws + L.ucnt);
-  const bool lists = (mode == kModeSparse) && active_idx != nullptr;
+  const bool lists = (mode != kFfnModeDense) && active_idx != nullptr;
   int32_t* bidx = lists ? reinterpret_cast<int32_t*>(ws + L.bidx) : nullptr;
   int32_t* bcnt = lists ? reinterpret_cast<int32_t*>(ws + L.bcnt) : nullptr;
   const size_t lds = (size_t)B * d * sizeof(float);
   const uint4* wg4 = reinterpret_cast<const uint4*>(wg);
   const uint4* wu4 = reinterpret_cast<const uint4*>(wu);
 
+  const bool thr = mode == kFfnModeThreshold;
   hipError_t e;
   {
-    ProfScope prof(mode == kModeSparse ? "cats_gate" : "dense_gate", stream);
-    e = (mode == kModeSparse)
-            ? launch_gate_mode<kModeSparse>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d,
-                                            F, t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt,
-                                            nullptr)
-            : launch_gate_mode<kModeDense>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d,
-                                           F, t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt,
-                                           nullptr);
+    ProfScope prof(topk ? "topk_up" : (thr ? "cats_gate" : "dense_gate"), stream);
+    if (topk)
+      e = launch_gate_mode<kModeKeyed>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d, F,
+                                       t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt,
+                                       const_cast<float*>(act), cut);
+    else if (thr)
+      e = launch_gate_mode<kModeSparse>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d, F,
+                                        t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt, nullptr);
+    else
+      e = launch_gate_mode<kModeDense>(bm, cpl, dim3(L.ntiles), lds, stream, x, B, wg4, wu4, d, F,
+                                       t, norm_eps, L.rmax, uidx, hbuf, ucnt, bidx, bcnt, nullptr);
   }
   if (e != hipSuccess) return e;
 
   float* part = reinterpret_cast<float*>(ws + L.part);
   {
-    ProfScope prof(mode == kModeSparse ? "cats_down" : "dense_down", stream);
+    ProfScope prof(topk ? "topk_down" : (thr ? "cats_down" : "dense_down"), stream);
     if ((e = launch_down(B, d, L.ntiles, L.rmax, L.gr, wd, uidx, hbuf, B, ucnt, part, stream)) !=
         hipSuccess)
       return e;
   }
   const int n = B * d;
   const int nred = ceil_div(n, 4 * kRedOut4);
-  ProfScope prof(mode == kModeSparse ? "cats_reduce" : "dense_reduce", stream);
+  ProfScope prof(topk ? "topk_reduce" : (thr ? "cats_reduce" : "dense_reduce"), stream);
   reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
       part, L.gr, n, resid, y, nred, B, F, L.ntiles, L.rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();
@@ -614,6 +641,26 @@ hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* r
   reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
       part, gr, n, resid, y, nred, B, F, nseg, rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();
+}
+
+hipError_t launch_gate_act(const float* x, int N, const uint16_t* wg, int d, int F,
+                           float norm_eps, float* act, hipStream_t stream) {
+  const int bc = std::max(1, std::min(8, kXLdsFloats / d));
+  const int cpl = pow2_at_least(ceil_div(d / 8, kWave), 16);
+  const int nseg = gate_segments(F);
+  const int rmax = ceil_div(F, nseg);
+  if (rmax > kMaxSeg) return hipErrorInvalidValue;
+  for (int b0 = 0; b0 < N; b0 += bc) {
+    const int nb = std::min(bc, N - b0);
+    const int bm = pow2_at_least(nb, 8);
+    ProfScope prof("topk_gate", stream);
+    hipError_t e = launch_gate_mode<kModeAct>(
+        bm, cpl, dim3(nseg), (size_t)nb * d * sizeof(float), stream, x + (size_t)b0 * d, nb,
+        reinterpret_cast<const uint4*>(wg), nullptr, d, F, 0.f, norm_eps, rmax, nullptr, nullptr,
+        nullptr, nullptr, nullptr, act + (size_t)b0 * F);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, int F,

@@ -9,6 +9,11 @@
 
 namespace sirius {
 
+// FFN selection modes of the small-batch and batch-1 launchers
+constexpr int kFfnModeDense = 0;      // every neuron (dense and condensed)
+constexpr int kFfnModeThreshold = 1;  // |SiLU(gate)| > t per token
+constexpr int kFfnModeTopK = 2;       // the top-k key cut per token (stored activations)
+
 // ---- small-batch FFN (gate GEMV + SiLU + threshold + compaction, sparse down, reduce)
 struct GemvLayout {
   int bc;       // batch rows handled per pass (x staged in LDS needs bc*d*4 <= 64 KiB)
@@ -19,12 +24,18 @@ struct GemvLayout {
 };
 GemvLayout gemv_layout(int B, int d, int F);
 
-// mode 0: dense (every neuron), 1: threshold sparsity. x/y/resid/active_* already offset
+// mode: kFfnMode*. x/y/resid/active_* (and act [B][F], cut [B] for top-k) already offset
 // to the chunk; B <= layout.bc.
 hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                            const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
-                           char* ws, const GemvLayout& L, hipStream_t stream);
+                           char* ws, const GemvLayout& L, hipStream_t stream,
+                           const float* act = nullptr, const unsigned long long* cut = nullptr);
+
+// Signed gate activations SiLU(W_gate xn) for N inputs into act [N, F] (top-k first pass);
+// xn = RMSNorm(x) when norm_eps >= 0.
+hipError_t launch_gate_act(const float* x, int N, const uint16_t* wg, int d, int F,
+                           float norm_eps, float* act, hipStream_t stream);
 
 // Gate activations |SiLU(W_gate x)| for N inputs into absact [N, F] (calibration).
 hipError_t launch_gate_absact(const float* x, int N, const uint16_t* wg, int d, int F,
@@ -55,7 +66,18 @@ hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t
                               const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                               const float* resid, float* y, int32_t* active_idx,
                               int32_t* active_cnt, char* ws, const Decode1Layout& L,
-                              hipStream_t stream);
+                              hipStream_t stream, const float* act = nullptr,
+                              const unsigned long long* cut = nullptr);
+
+// ---- per-token top-k FSparse: gate pass, key cut per token, then the keyed FFN pass
+struct TopkLayout {
+  size_t act, cut, ffn, total;  // act [B][F] fp32, cut [B] u64, then the FFN workspace
+};
+TopkLayout topk_layout(int B, int d, int F);
+hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, int d, int F, int k, float norm_eps,
+                           const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                           char* ws, const TopkLayout& L, hipStream_t stream);
 
 // ---- multi-token FFN on MFMA (B >= kMfmaMinBatch)
 constexpr int kMfmaMinBatch = 8;

@@ -1,0 +1,179 @@
+// Per-token top-k FSparse on gfx950 (Sec. 3, footnote on the fine-grained implementation: the
+// paper keeps the top-k gate activations per token instead of thresholding them, so every
+// token has exactly the target density; up and down stay sparse as in CATS).
+//
+// The k kept neurons depend on all d_ff gate activations of the token, so the pass splits in
+// three:
+//  1. gate_kernel (ffn_gemv.hip, activation mode): a = SiLU(W_gate xn) for every neuron into a
+//     [B, d_ff] buffer; the whole gate is read once, as in the threshold path.
+//  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
+//     (|a| descending, then the lower index): a most-significant-digit radix select over the
+//     bits of |a| (four 8-bit digits, per-wave LDS histograms, a block scan over the 256 bins)
+//     gives the k-th largest magnitude T and how many of the neurons equal to T are kept; a
+//     block scan over the threads' contiguous index ranges then finds the last kept one.
+//  3. the keyed FFN pass: decode1_kernel (batch 1) or gate_kernel + down_kernel (small
+//     batches) read the stored activations, keep a neuron iff its key reaches the token's cut,
+//     and stream W_up and W_down for the kept neurons only; reduce_kernel sums the partials
+//     and writes the ascending active lists.
+#include "common.h"
+#include "kernels.h"
+#include "profile.h"
+#include "topk.h"
+
+namespace sirius {
+namespace {
+
+constexpr int kCutThreads = 1024;
+constexpr int kCutWaves = kCutThreads / kWave;  // 16
+constexpr int kBins = 256;                      // 8-bit digits
+
+// Inclusive scan of one int per thread over the 1024-thread workgroup; *total is the sum.
+__device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += t;
+  }
+  if (lane == kWave - 1) s_w[wave] = incl;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kCutWaves; ++w) {
+    const int c = s_w[w];
+    off += (w < wave) ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + incl;
+}
+
+// Thread t owns neurons [t * PER, t * PER + PER) of the token (contiguous, for the tie scan).
+template <int PER>
+__global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __restrict__ act,
+                                                               int F, int k,
+                                                               unsigned long long* __restrict__ cut) {
+  __shared__ uint32_t s_hist[kCutWaves * kBins];
+  __shared__ int s_w[kCutWaves];
+  __shared__ uint32_t s_digit;
+  __shared__ int s_kr;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const int b = blockIdx.x;
+  const float* a = act + (size_t)b * F;
+  const int i0 = tid * PER;
+
+  uint32_t v[PER];  // bits of |a|: for non-negative floats the bit order is the value order
+#pragma unroll
+  for (int j = 0; j < PER; ++j) v[j] = (i0 + j < F) ? __float_as_uint(fabsf(a[i0 + j])) : 0u;
+
+  uint32_t prefix = 0u, pmask = 0u;
+  int kr = k;  // rank (1-based, descending) of the wanted key among those matching the prefix
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < kCutWaves * kBins; i += kCutThreads) s_hist[i] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (i0 + j < F && (v[j] & pmask) == prefix)
+        atomicAdd(&s_hist[wave * kBins + ((v[j] >> shift) & 255u)], 1u);
+    __syncthreads();
+    // thread t < 256 holds digit 255 - t, so the inclusive scan counts the digits >= it
+    int c = 0;
+    if (tid < kBins) {
+#pragma unroll
+      for (int w = 0; w < kCutWaves; ++w) c += (int)s_hist[w * kBins + (kBins - 1 - tid)];
+    }
+    int tot;
+    const int incl = block_inclusive_scan_1024(c, s_w, &tot);
+    if (tid < kBins && incl >= kr && incl - c < kr) {
+      s_digit = (uint32_t)(kBins - 1 - tid);
+      s_kr = kr - (incl - c);
+    }
+    __syncthreads();
+    prefix |= s_digit << shift;
+    pmask |= 255u << shift;
+    kr = s_kr;
+  }
+  // prefix is the k-th largest |a|; the first kr neurons (by index) equal to it are kept
+  int eq = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) eq += (i0 + j < F && v[j] == prefix) ? 1 : 0;
+  int tot;
+  const int incl = block_inclusive_scan_1024(eq, s_w, &tot);
+  const int before = incl - eq;
+  if (before < kr && kr <= incl) {
+    int m = kr - before, idx = i0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (i0 + j < F && v[j] == prefix) {
+        if (m == 1) idx = i0 + j;
+        --m;
+      }
+    }
+    cut[b] = ((unsigned long long)prefix << 32) | (unsigned)(~(unsigned)idx);
+  }
+}
+
+hipError_t launch_cut(const float* act, int B, int F, int k, unsigned long long* cut,
+                      hipStream_t s) {
+  const int per = ceil_div(F, kCutThreads);
+#define SIRIUS_CUT(P)                                                        \
+  if (per <= P) {                                                            \
+    topk_cut_kernel<P><<<B, kCutThreads, 0, s>>>(act, F, k, cut);            \
+    return hipGetLastError();                                                \
+  }
+  SIRIUS_CUT(1)
+  SIRIUS_CUT(2)
+  SIRIUS_CUT(4)
+  SIRIUS_CUT(8)
+  SIRIUS_CUT(16)
+  SIRIUS_CUT(32)
+  SIRIUS_CUT(64)
+#undef SIRIUS_CUT
+  return hipErrorInvalidValue;  // d_ff above 65536
+}
+
+}  // namespace
+
+TopkLayout topk_layout(int B, int d, int F) {
+  TopkLayout L{};
+  Carve c;
+  L.act = c.take((size_t)B * F * sizeof(float));
+  L.cut = c.take((size_t)B * sizeof(unsigned long long));
+  L.ffn = c.take(B <= 1 ? decode1_layout(d, F).total : gemv_layout(B, d, F).total);
+  L.total = c.off;
+  return L;
+}
+
+hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                           const uint16_t* wd, int d, int F, int k, float norm_eps,
+                           const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                           char* ws, const TopkLayout& L, hipStream_t stream) {
+  if (B < 1 || k < 1 || k > F) return hipErrorInvalidValue;
+  float* act = reinterpret_cast<float*>(ws + L.act);
+  unsigned long long* cut = reinterpret_cast<unsigned long long*>(ws + L.cut);
+  char* fws = ws + L.ffn;
+  hipError_t e = launch_gate_act(x, B, wg, d, F, norm_eps, act, stream);
+  if (e != hipSuccess) return e;
+  {
+    ProfScope prof("topk_cut", stream);
+    if ((e = launch_cut(act, B, F, k, cut, stream)) != hipSuccess) return e;
+  }
+  if (B == 1)
+    return launch_ffn_decode1(x, wg, wu, wd, d, F, kFfnModeTopK, 0.f, norm_eps, resid, y,
+                              active_idx, active_cnt, fws, decode1_layout(d, F), stream, act, cut);
+  const GemvLayout G = gemv_layout(B, d, F);
+  for (int b0 = 0; b0 < B; b0 += G.bc) {
+    const int nb = std::min(G.bc, B - b0);
+    e = launch_ffn_gemv(x + (size_t)b0 * d, nb, wg, wu, wd, d, F, kFfnModeTopK, 0.f, norm_eps,
+                        resid ? resid + (size_t)b0 * d : nullptr, y + (size_t)b0 * d,
+                        active_idx ? active_idx + (size_t)b0 * F : nullptr,
+                        active_cnt ? active_cnt + b0 : nullptr, fws, G, stream,
+                        act + (size_t)b0 * F, cut + b0);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace sirius

@@ -9,6 +9,9 @@ Tolerances (see the design notes for their derivation):
     <= 1e-4 x RMS against the oracle on the rounded input (with RMSNorm plus a first-order
     allowance for inputs whose rounding is ambiguous, see check_ffn_rounded_norm), and the
     method bound against the unrounded input;
+  * per-token top-k sets: exactly k neurons, bit-exact outside |(|a| - a_(k))| <= 1e-3
+    (a_(k) the token's k-th largest |a|), then the output against the oracle's FFN on the
+    GPU's own set;
   * acceptance lengths: bit-exact outside a guard band |q - r| <= 1e-5 r;
   * tree drafting step: (parent, token) pairs bit-exact at every rank whose score is more
     than 1e-5 from its neighbours' (and from the first excluded candidate's); near-tied ranks
@@ -85,6 +88,27 @@ def check_cats_sets(x_in, wg, t, idx, cnt, band=CATS_BAND):
         g = idx[b, : int(cnt[b])].astype(np.int64)
         assert np.all(np.diff(g) > 0), "active list must be strictly ascending"
         near = np.abs(np.abs(a[b]) - t) <= band
+        n_boundary += int(near.sum())
+        sym = np.setxor1d(g, sets_o[b])
+        assert np.all(near[sym]), f"token {b}: {int((~near[sym]).sum())} set mismatches outside the band"
+        gpu_sets.append(g)
+    return gpu_sets, n_boundary
+
+
+def check_topk_sets(x_in, wg, k, idx, cnt, band=CATS_BAND):
+    """Per-token top-k sets: exactly k ascending neurons per token, equal to the oracle's outside
+    the guard band around the token's k-th largest |a| (the GPU decides on fp32 activations).
+    Returns (gpu_sets, boundary_count)."""
+    sets_o, a = oracle.topk_active_sets(x_in, wg, k)
+    gpu_sets = []
+    n_boundary = 0
+    for b in range(len(sets_o)):
+        assert int(cnt[b]) == k, f"token {b}: {int(cnt[b])} neurons kept, expected {k}"
+        g = idx[b, :k].astype(np.int64)
+        assert np.all(np.diff(g) > 0), "active list must be strictly ascending"
+        assert g[0] >= 0 and g[-1] < a.shape[1]
+        tk = np.sort(np.abs(a[b]))[::-1][k - 1]
+        near = np.abs(np.abs(a[b]) - tk) <= band
         n_boundary += int(near.sum())
         sym = np.setxor1d(g, sets_o[b])
         assert np.all(near[sym]), f"token {b}: {int((~near[sym]).sum())} set mismatches outside the band"

@@ -89,6 +89,25 @@ def test_cats_argument_errors(L):
     assert rc == -1
 
 
+def test_topk_argument_errors(L):
+    big = 1 << 30
+    base = [FAKE, 1, FAKE, FAKE, FAKE, 64, 100, 50, -1.0, None, FAKE, FAKE, FAKE, FAKE, big, None]
+
+    def call(**kw):
+        a = list(base)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.sirius_ffn_topk(*a)
+
+    assert call(a7=0) == -1 and "k=" in _err(L)
+    assert call(a7=101) == -1
+    assert call(a5=100) == -1            # d_model not a multiple of 8
+    assert call(a12=None) == -1          # exactly one list pointer
+    assert call(a8=float("nan")) == -1   # NaN norm_eps
+    assert call(a14=16) == -2            # workspace too small
+    assert call(a1=0) == 0               # empty batch
+
+
 def test_griffin_argument_errors(L):
     big = 1 << 30
     args = [FAKE, 8, FAKE, FAKE, FAKE, 64, 100, 50, 0, FAKE, None, FAKE, FAKE, FAKE, FAKE, big, None]
@@ -209,6 +228,9 @@ def test_workspace_sizes(L):
     assert g >= 512 * 14336 * 4
     c = f(5, 256, 4096, 14336, 0, 0)
     assert c >= 256 * 14336 * 4
+    # per-token top-k: the activation buffer and cuts come before the FFN workspace
+    assert f(8, 1, 4096, 14336, 0, 0) >= 14336 * 4 + f(1, 1, 4096, 14336, 0, 0)
+    assert f(8, 3, 4096, 14336, 0, 0) >= 3 * 14336 * 4 + f(1, 3, 4096, 14336, 0, 0)
     # tree drafting step: B, Wc, W, V
     assert f(6, 1, 8, 8, 128256, 0) > 0
     assert f(6, 1, 17, 8, 128256, 0) == 0
