@@ -20,6 +20,7 @@ batch, all inputs resident in HBM:
   verify    correction check over logits [8, 16, 128256]
   tree_build one drafting step of a width-4 tree: logits [4, 128256] at the current leaves
   tree_verify verification of a 16-step, width-4 tree with bonus rows: logits [68, 128256]
+  topk      per-token top-k sparse FFN decode, one token, k = d_ff / 2 (the paper's FSparse)
   cats70b   sparse FFN decode, one token, one Llama-3-70B FFN layer (d_model 8192,
             d_ff 28672, 50% calibrated), four rotated copies (5.6 GB)
 The printed value is the sparse FFN decode time per token (rows.cats, from
@@ -195,9 +196,12 @@ def main():
     nxt = torch.empty(VERIFY_B, dtype=torch.int32, device=dev)
     tb_out = [torch.empty((1, TREE_W), dtype=dt, device=dev) for dt in (torch.int32, torch.int32, torch.float32)]
     tv_out = [torch.empty(1, dtype=torch.int32, device=dev) for _ in range(3)]
+    yt = torch.empty_like(y)
+    act_t = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
+    cnt_t = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
 
     rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "tree_build", "tree_verify",
-            "cats70b"]
+            "topk", "cats70b"]
     stream = torch.cuda.current_stream()
 
     def step(s, ev=None, with70=True):
@@ -233,12 +237,15 @@ def main():
         sr.sirius_tree_verify(tv_logits[b], tv_tok[b], tv_par[b], 0.1, 1.0, bonus=True, best_leaf=tv_out[0],
                               accept_len=tv_out[1], next_token=tv_out[2], want_q=False)
         mark(9)
+        sr.sirius_ffn_topk(xs[(s + 3) % N_DECODE:(s + 3) % N_DECODE + 1], *layers[(c + 5) % NCOPY], k_keep, y=yt,
+                           active_idx=act_t, active_cnt=cnt_t[s:s + 1])
+        mark(10)
         if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
             return
         c70 = s % NCOPY70
         sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
                            active_idx=act70, active_cnt=cnt70[s:s + 1])
-        mark(10)
+        mark(11)
 
     log("warmup")
     for s in range(args.warmup):
@@ -272,7 +279,8 @@ def main():
     kern = {}
     for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
                  "ffn_mfma_reduce",
-                 "verify_stats", "verify_scan", "tree_topw", "tree_select", "tree_stats", "tree_scan", "griffin_z", "griffin_topk", "griffin_score", "condense",
+                 "verify_stats", "verify_scan", "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate", "topk_cut", "topk_decode",
+                 "topk_reduce", "griffin_z", "griffin_topk", "griffin_score", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:
         tot, n = sr.sirius_profile_query(name)
         if n:
@@ -293,6 +301,7 @@ def main():
                  "condensed": cond_bytes, "dense": dense_bytes, "dense16": dense_bytes + 2 * VERIFY_K * D_MODEL * 4,
                  "verify": verify_bytes, "tree_build": TREE_W * VERIFY_V * 4 + 2 * TREE_W * 4,
                  "tree_verify": (TREE_K + 1) * TREE_W * VERIFY_V * 4 + 2 * TREE_K * TREE_W * 4,
+                 "topk": D_FF * D_MODEL * 2 + 2 * k_keep * D_MODEL * 2 + 2 * D_MODEL * 4,
                  "cats70b": cats70_bytes}
 
     def med(v):

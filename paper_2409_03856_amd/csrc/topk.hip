@@ -8,9 +8,10 @@
 //     [B, d_ff] buffer; the whole gate is read once, as in the threshold path.
 //  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
 //     (|a| descending, then the lower index): a most-significant-digit radix select over the
-//     bits of |a| (four 8-bit digits, per-wave LDS histograms, a block scan over the 256 bins)
-//     gives the k-th largest magnitude T and how many of the neurons equal to T are kept; a
-//     block scan over the threads' contiguous index ranges then finds the last kept one.
+//     bits of |a| (the exponent byte, then mantissa bytes; LDS histograms, four copies per
+//     wave; a block scan over the 256 bins) until the digit holding it has few members, which
+//     are then gathered and ranked by counting on the full key; when every value bit is
+//     decided first, a block scan over the threads' contiguous index ranges settles the ties.
 //  3. the keyed FFN pass: decode1_kernel (batch 1) or gate_kernel + down_kernel (small
 //     batches) read the stored activations, keep a neuron iff its key reaches the token's cut,
 //     and stream W_up and W_down for the kept neurons only; reduce_kernel sums the partials
@@ -26,6 +27,8 @@ namespace {
 constexpr int kCutThreads = 1024;
 constexpr int kCutWaves = kCutThreads / kWave;  // 16
 constexpr int kBins = 256;                      // 8-bit digits
+constexpr int kCopies = 4 * kCutWaves;          // histogram copies: four per wave
+constexpr int kGather = 512;                    // digit members ranked directly at most
 
 // Inclusive scan of one int per thread over the 1024-thread workgroup; *total is the sum.
 __device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* total) {
@@ -51,51 +54,101 @@ __device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* t
 }
 
 // Thread t owns neurons [t * PER, t * PER + PER) of the token (contiguous, for the tie scan).
+// Digits of the bits of |a|, most significant first: the 8 exponent bits, then the mantissa in
+// 8, 8 and 7 bits (activations crowd into a few exponents, so the exponent digit comes
+// alone). Each wave keeps four histogram copies (one per 16 lanes) so that equal digits
+// collide less in the LDS atomics. As soon as the digit holding the k-th largest has at most
+// kGather members (usually after the second digit), they are gathered and ranked by counting
+// on the full key; only when every value bit is decided does an index scan settle the ties.
 template <int PER>
 __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __restrict__ act,
                                                                int F, int k,
                                                                unsigned long long* __restrict__ cut) {
-  __shared__ uint32_t s_hist[kCutWaves * kBins];
+  __shared__ uint32_t s_hist[kCopies * kBins];
+  __shared__ unsigned long long s_cand[kGather];
   __shared__ int s_w[kCutWaves];
-  __shared__ uint32_t s_digit;
-  __shared__ int s_kr;
-  const int tid = threadIdx.x, wave = tid >> 6;
+  __shared__ int s_sel[3];
+  __shared__ int s_n;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int copy = wave * (kCopies / kCutWaves) + (lane >> 4);
   const int b = blockIdx.x;
   const float* a = act + (size_t)b * F;
   const int i0 = tid * PER;
 
   uint32_t v[PER];  // bits of |a|: for non-negative floats the bit order is the value order
+  if ((PER & 3) == 0 && (F & 3) == 0) {  // rows start 16-byte aligned: whole float4s
+    const float4* a4 = reinterpret_cast<const float4*>(a + i0);
 #pragma unroll
-  for (int j = 0; j < PER; ++j) v[j] = (i0 + j < F) ? __float_as_uint(fabsf(a[i0 + j])) : 0u;
+    for (int g = 0; g < PER / 4; ++g) {
+      const float4 x = (i0 + 4 * g < F) ? a4[g] : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[4 * g] = __float_as_uint(fabsf(x.x));
+      v[4 * g + 1] = __float_as_uint(fabsf(x.y));
+      v[4 * g + 2] = __float_as_uint(fabsf(x.z));
+      v[4 * g + 3] = __float_as_uint(fabsf(x.w));
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) v[j] = (i0 + j < F) ? __float_as_uint(fabsf(a[i0 + j])) : 0u;
+  }
+  if (tid == 0) s_n = 0;
 
   uint32_t prefix = 0u, pmask = 0u;
   int kr = k;  // rank (1-based, descending) of the wanted key among those matching the prefix
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = tid; i < kCutWaves * kBins; i += kCutThreads) s_hist[i] = 0u;
+#pragma unroll 1
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = pass == 0 ? 23 : (pass == 1 ? 15 : (pass == 2 ? 7 : 0));
+    const uint32_t dmask = pass == 3 ? 127u : 255u;
+    for (int i = tid; i < kCopies * kBins; i += kCutThreads) s_hist[i] = 0u;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < PER; ++j)
       if (i0 + j < F && (v[j] & pmask) == prefix)
-        atomicAdd(&s_hist[wave * kBins + ((v[j] >> shift) & 255u)], 1u);
+        atomicAdd(&s_hist[copy * kBins + ((v[j] >> shift) & dmask)], 1u);
     __syncthreads();
     // thread t < 256 holds digit 255 - t, so the inclusive scan counts the digits >= it
     int c = 0;
     if (tid < kBins) {
-#pragma unroll
-      for (int w = 0; w < kCutWaves; ++w) c += (int)s_hist[w * kBins + (kBins - 1 - tid)];
+#pragma unroll 16
+      for (int q = 0; q < kCopies; ++q) c += (int)s_hist[q * kBins + (kBins - 1 - tid)];
     }
     int tot;
     const int incl = block_inclusive_scan_1024(c, s_w, &tot);
     if (tid < kBins && incl >= kr && incl - c < kr) {
-      s_digit = (uint32_t)(kBins - 1 - tid);
-      s_kr = kr - (incl - c);
+      s_sel[0] = kBins - 1 - tid;
+      s_sel[1] = kr - (incl - c);
+      s_sel[2] = c;
     }
     __syncthreads();
-    prefix |= s_digit << shift;
-    pmask |= 255u << shift;
-    kr = s_kr;
+    prefix |= (uint32_t)s_sel[0] << shift;
+    pmask |= dmask << shift;
+    kr = s_sel[1];
+    if (pass < 3 && s_sel[2] <= kGather) {  // uniform: gather the digit's members, rank them
+      const int cnt = s_sel[2];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        if (i0 + j < F && (v[j] & pmask) == prefix) {
+          const int pos = atomicAdd(&s_n, 1);
+          s_cand[pos] = ((unsigned long long)v[j] << 32) | (unsigned)(~(unsigned)(i0 + j));
+        }
+      }
+      __syncthreads();
+      if (tid < cnt) {  // cnt <= kGather <= kCutThreads
+        const unsigned long long mine = s_cand[tid];
+        int r = 0;
+        for (int j0 = 0; j0 < cnt; j0 += 16) {
+          unsigned long long o[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) o[q] = s_cand[min(j0 + q, cnt - 1)];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) r += (int)((j0 + q < cnt) & (o[q] > mine));
+        }
+        if (r == kr - 1) cut[b] = mine;  // keys are distinct: one member has this rank
+      }
+      return;
+    }
   }
-  // prefix is the k-th largest |a|; the first kr neurons (by index) equal to it are kept
+  // every value bit decided: prefix is the k-th largest |a|; the first kr neurons (by index)
+  // equal to it are kept
   int eq = 0;
 #pragma unroll
   for (int j = 0; j < PER; ++j) eq += (i0 + j < F && v[j] == prefix) ? 1 : 0;

@@ -90,6 +90,32 @@ def test_ties_keep_the_lower_index(sr):
         check_ffn(host(y), oracle.ffn_masked(x, wg, wu, wd, [sorted(g)]))
 
 
+def test_all_equal_activations_keep_the_first_k(sr):
+    # every gate row equal: one value everywhere, so the cut falls back to the index order
+    d, f = 64, 4000
+    wg, wu, wd = ffn_weights(950, d, f, 1.0 / 8.0)
+    wg = np.tile(wg[:1], (f, 1))
+    W = tuple(dev_bf16(w) for w in (wg, wu, wd))
+    x = decode_inputs(950, 1, d)
+    for k in (1, 999, 3999):
+        say(f"topk all-equal k={k}")
+        y, idx, cnt = sr.sirius_ffn_topk(dev_f32(x), *W, k)
+        assert host(idx)[0, :k].tolist() == list(range(k)) and int(host(cnt)[0]) == k
+        check_ffn(host(y), oracle.ffn_masked(x, wg, wu, wd, [np.arange(k)]))
+
+
+def test_largest_layer_width(sr):
+    # d_ff = 65536: the widest bin of the first digit pass holds more than can be ranked
+    # directly, so a second digit pass runs
+    (wg, wu, wd), W = _layer(960, 256, 65536, 1.0 / 16.0)
+    x = decode_inputs(960, 2, 256)
+    for bsz in (1, 2):
+        say(f"topk d_ff=65536 B={bsz}")
+        y, idx, cnt = sr.sirius_ffn_topk(dev_f32(x[:bsz]), *W, 32768)
+        sets, _ = check_topk_sets(x[:bsz], wg, 32768, host(idx), host(cnt))
+        check_ffn(host(y), oracle.ffn_masked(x[:bsz], wg, wu, wd, sets))
+
+
 def test_llama3_8b_layer_half_density(sr):
     s = LLAMA3_8B
     (wg, wu, wd), W = _layer(1000, s.d_model, s.d_ff, s.weight_std)
