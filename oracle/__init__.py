@@ -12,6 +12,9 @@ A plain, slow, float64 NumPy statement of what the GPU library computes:
   * tree     -- the pruned tree drafting step (fixed treewidth, cumulative
                 log-likelihood ranking) and the verification of a drafted tree
                 (longest advance over its complete paths), Sec. 4;
+  * kv       -- attention over the KV cache shared by the sparse and the full
+                model, with the full model's direct rewrite of the drafted chunk's
+                rows and the rollback after the check (Algorithm 1);
   * apu      -- the efficiency bookkeeping of Sec. 2.2 and Sec. 2.3
                 (APU, effective density, speculative-decoding AAL).
 
@@ -48,3 +51,4 @@ from .ffn import (  # noqa: F401
 from .verify import softmax_row_stats, verify_accept  # noqa: F401
 from .tree import log_softmax, tree_build_step, tree_paths, tree_verify  # noqa: F401
 from .apu import sd_aal, apu, effective_density  # noqa: F401
+from .kv import attn_kv, kv_rollback  # noqa: F401
