@@ -60,6 +60,7 @@ extern "C" {
 #define SIRIUS_OP_TREE_BUILD 6
 #define SIRIUS_OP_TREE_VERIFY 7
 #define SIRIUS_OP_FFN_TOPK 8
+#define SIRIUS_OP_ATTN_KV 9
 
 /*
  * Dense SwiGLU FFN (the full model, sparsity 0):
@@ -250,6 +251,44 @@ int sirius_tree_verify(const float* logits, int B, int K, int W, int V, int bonu
                        void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * One attention layer over the KV cache shared by the sparse and the full
+ * model, with the full model's direct rewrite (Algorithm 1; Sec. 4, how to
+ * correct): the n tokens of batch entry b sit at positions p .. p + n - 1,
+ * p = cache_pos[b]; their keys and values k_new, v_new are written into the
+ * cache rows there (replacing what the sparse model wrote while drafting),
+ * and token i attends causally to cache rows 0 .. p + i:
+ *   out[b,i,h] = sum_j softmax_j(q[b,i,h] . K[b,j,h/G] / sqrt(head_dim)) V[b,j,h/G]
+ * over j <= p + i, G = H / Hkv (grouped-query attention). n = 1 is the
+ * sparse model's decode step; n = the kernel size is the full model's
+ * verification pass over the drafted chunk. Scores, softmax and the weighted
+ * sum run in fp32 on the stored bf16 keys and values.
+ *   q          [B, n, H, head_dim] fp32 (any positional rotation applied).
+ *   k_new, v_new [B, n, Hkv, head_dim] bf16.
+ *   k_cache, v_cache [B, Lmax, Hkv, head_dim] bf16, updated in place.
+ *   cache_pos  [B] int32 on the device, read only. An entry with p < 0 or
+ *              p + n > Lmax leaves the cache untouched and gets NaN outputs.
+ *   out        [B, n, H, head_dim] fp32.
+ * All arrays 16-byte aligned. Errors: SIRIUS_EINVAL for null pointers, B
+ * outside [0, 65535], n outside [1, 1024], H not a positive multiple of Hkv,
+ * head_dim not a multiple of 8 in [8, 128], Lmax outside [n, 2^20].
+ */
+int sirius_attn_kv(const float* q, const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                   uint16_t* v_cache, const int32_t* cache_pos, int B, int n, int H, int Hkv,
+                   int head_dim, int Lmax, float* out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Rollback after the check (Algorithm 1): with the first rejected position
+ * accept_len[b] of a chunk of n (n when all are accepted), the cache
+ * position moves past the inputs that stay valid:
+ *   cache_pos[b] += min(accept_len[b] + 1, n)
+ * (cache_pos holding the chunk's start p, as passed to the verification
+ * pass). Rows past the new position are simply overwritten later. Runs on
+ * the device: no synchronisation with the host.
+ * Errors: SIRIUS_EINVAL for null pointers, B < 0, n < 1.
+ */
+int sirius_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n, void* stream);
+
+/*
  * RMSNorm with unit weight, the layer-stack glue around the FFN:
  *   out[b] = h[b] / sqrt(mean(h[b]^2) + eps). out may alias h.
  * Errors: SIRIUS_EINVAL for null pointers, d_model < 1, eps < 0.
@@ -276,7 +315,8 @@ int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, 
  * "griffin_rownorm", "griffin_score", "select_init", "select_hist",
  * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal",
  * "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate",
- * "topk_cut", "topk_decode", "topk_up", "topk_down", "topk_reduce".
+ * "topk_cut", "topk_decode", "topk_up", "topk_down", "topk_reduce",
+ * "attn_partial", "attn_combine", "kv_rollback".
  * sirius_profile_reset drops every record (it waits for pending events).
  * Errors: SIRIUS_EINVAL for NULL arguments, SIRIUS_EHIP if an event fails.
  */
@@ -292,6 +332,7 @@ int sirius_profile_query(const char* kernel, double* total_ms, int64_t* launches
  *   VERIFY: B, unused, unused, V, R (rows per batch entry)
  *   TREE_BUILD: B, Wc, W, V, unused
  *   TREE_VERIFY: B, K, W, V, bonus
+ *   ATTN_KV: B, n, H * 65536 + Hkv, head_dim, Lmax
  * Returns 0 for an unknown op or invalid sizes. */
 size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, int K_or_R);
 

@@ -19,6 +19,8 @@ from ._lib import (  # noqa: F401
     sirius_verify_accept,
     sirius_tree_build_step,
     sirius_tree_verify,
+    sirius_attn_kv,
+    sirius_kv_rollback,
     sirius_rmsnorm,
     sirius_fill_normal_bf16,
     sirius_workspace_size,
@@ -36,4 +38,5 @@ from ._lib import (  # noqa: F401
     OP_TREE_BUILD,
     OP_TREE_VERIFY,
     OP_FFN_TOPK,
+    OP_ATTN_KV,
 )

@@ -30,6 +30,7 @@ OP_CATS_CALIBRATE = 5
 OP_TREE_BUILD = 6
 OP_TREE_VERIFY = 7
 OP_FFN_TOPK = 8
+OP_ATTN_KV = 9
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -47,6 +48,8 @@ SIGNATURES = {
     "sirius_verify_accept": (_I, [_P, _I, _I, _I, _I, _P, _F, _F, _P, _P, _P, _P, _Z, _P]),
     "sirius_tree_build_step": (_I, [_P, _I, _I, _I, _P, _I, _F, _P, _P, _P, _P, _Z, _P]),
     "sirius_tree_verify": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "sirius_attn_kv": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _Z, _P]),
+    "sirius_kv_rollback": (_I, [_P, _P, _I, _I, _P]),
     "sirius_rmsnorm": (_I, [_P, _I, _I, _F, _P, _P]),
     "sirius_fill_normal_bf16": (_I, [_P, _Z, ctypes.c_uint64, _F, _F, _P]),
     "sirius_profile_enable": (_I, [_I]),
@@ -345,6 +348,49 @@ def sirius_tree_verify(logits, tokens, parents, r, temperature=1.0, *, bonus=Fal
                                     float(r), float(temperature), _ptr(best_leaf), _ptr(accept_len),
                                     _ptr(next_token), _ptr(q), _ptr(ws), ws.numel(), _stream(stream)))
     return best_leaf, accept_len, next_token, q
+
+
+def _bits16(t):
+    torch = _torch()
+    _need(t.dtype in (torch.bfloat16, torch.int16, torch.uint16), "keys and values must be bf16 (or 16-bit bits)")
+
+
+def sirius_attn_kv(q, k_new, v_new, k_cache, v_cache, cache_pos, *, out=None, ws=None, stream=None):
+    """q [B, n, H, hd] fp32; k_new, v_new [B, n, Hkv, hd] bf16; caches [B, Lmax, Hkv, hd] bf16
+    (updated in place: rows cache_pos[b] .. + n - 1 take the new keys and values);
+    cache_pos [B] int32 on the GPU. Returns out [B, n, H, hd] fp32."""
+    torch = _torch()
+    _need(q.dtype == torch.float32 and q.dim() == 4, "q must be fp32 [B, n, H, hd]")
+    bsz, n, h, hd = (int(s) for s in q.shape)
+    for t in (k_new, v_new, k_cache, v_cache):
+        _bits16(t)
+        _need(t.dim() == 4 and int(t.shape[0]) == bsz and int(t.shape[3]) == hd, "bad key/value shape")
+    hkv = int(k_new.shape[2])
+    _need(tuple(k_new.shape) == (bsz, n, hkv, hd) and tuple(v_new.shape) == tuple(k_new.shape),
+          "k_new, v_new must be [B, n, Hkv, hd]")
+    lmax = int(k_cache.shape[1])
+    _need(tuple(k_cache.shape) == (bsz, lmax, hkv, hd) and tuple(v_cache.shape) == tuple(k_cache.shape),
+          "caches must be [B, Lmax, Hkv, hd]")
+    _need(cache_pos.dtype == torch.int32 and tuple(cache_pos.shape) == (bsz,), "cache_pos must be int32 [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev_check(q, k_new, v_new, k_cache, v_cache, cache_pos, out)
+    if ws is None:
+        ws = workspace(OP_ATTN_KV, max(bsz, 1), n, h * 65536 + hkv, hd, lmax, device=q.device)
+    _check(lib().sirius_attn_kv(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(cache_pos),
+                                bsz, n, h, hkv, hd, lmax, _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def sirius_kv_rollback(cache_pos, accept_len, n, *, stream=None):
+    """cache_pos[b] += min(accept_len[b] + 1, n), on the GPU."""
+    torch = _torch()
+    _need(cache_pos.dtype == torch.int32 and accept_len.dtype == torch.int32, "int32 tensors expected")
+    _need(cache_pos.shape == accept_len.shape and cache_pos.dim() == 1, "cache_pos and accept_len must be [B]")
+    _dev_check(cache_pos, accept_len)
+    _check(lib().sirius_kv_rollback(_ptr(cache_pos), _ptr(accept_len), int(cache_pos.shape[0]), int(n),
+                                    _stream(stream)))
+    return cache_pos
 
 
 def sirius_rmsnorm(h, eps=1e-5, *, out=None, stream=None):

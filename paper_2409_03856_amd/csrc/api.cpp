@@ -36,6 +36,8 @@ constexpr int kMaxVerifyRows = 1024;
 constexpr int kMaxTreeBuildW = 16;   // tree width and current-leaf limit of a drafting step
 constexpr int kMaxTreeVerifyW = 64;  // tree width limit of tree verification
 constexpr long kMaxLogitRows = 65535;  // B * rows of a logit pass (second grid dimension)
+constexpr int kMaxAttnTokens = 1024;   // tokens per attention call
+constexpr int kMaxCacheLen = 1 << 20;  // cache rows per batch entry
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -148,6 +150,15 @@ size_t sirius_workspace_size(int op, int B, int d_model, int d_ff, int T_or_V, i
     case SIRIUS_OP_FFN_TOPK:
       if (B < 0 || B > kMaxBatch || !dims_ok(d_model, d_ff)) return 0;
       return sirius::topk_layout(std::max(B, 1), d_model, d_ff).total;
+    case SIRIUS_OP_ATTN_KV: {
+      // B, n, H, Hkv, head_dim (d_model) ... packed: B, d_model = n, d_ff = H * 65536 + Hkv,
+      // T_or_V = head_dim, K_or_R = Lmax
+      const int H = d_ff >> 16, Hkv = d_ff & 0xffff;
+      if (B < 0 || d_model < 1 || H < 1 || Hkv < 1 || H % Hkv != 0 || T_or_V < 8 ||
+          T_or_V > 128 || T_or_V % 8 != 0 || K_or_R < d_model)
+        return 0;
+      return sirius::attn_layout(std::max(B, 1), d_model, H, Hkv, T_or_V, K_or_R).total;
+    }
     case SIRIUS_OP_TREE_BUILD:
       if (B < 0 || d_model < 1 || d_model > kMaxTreeBuildW || d_ff < 1 || d_ff > kMaxTreeBuildW ||
           T_or_V < 1 || (long)d_model * T_or_V < d_ff)
@@ -367,6 +378,46 @@ int sirius_tree_verify(const float* logits, int B, int K, int W, int V, int bonu
   return hip_status(sirius::launch_tree_verify(logits, B, K, W, V, bonus ? 1 : 0, tokens, parents,
                                                r, temperature, best_leaf, accept_len, next_token, q,
                                                static_cast<char*>(ws), L,
+                                               static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_attn_kv(const float* q, const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                   uint16_t* v_cache, const int32_t* cache_pos, int B, int n, int H, int Hkv,
+                   int head_dim, int Lmax, float* out, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sirius_attn_kv";
+  if (B < 0 || B > kMaxLogitRows) return fail(SIRIUS_EINVAL, "%s: B=%d outside [0, %ld]", fn, B, kMaxLogitRows);
+  if (n < 1 || n > kMaxAttnTokens) return fail(SIRIUS_EINVAL, "%s: n=%d outside [1, %d]", fn, n, kMaxAttnTokens);
+  if (H < 1 || Hkv < 1 || H % Hkv != 0)
+    return fail(SIRIUS_EINVAL, "%s: H=%d must be a positive multiple of Hkv=%d", fn, H, Hkv);
+  if (head_dim < 8 || head_dim > 128 || head_dim % 8 != 0)
+    return fail(SIRIUS_EINVAL, "%s: head_dim=%d must be a multiple of 8 in [8, 128]", fn, head_dim);
+  if (Lmax < n || Lmax > kMaxCacheLen)
+    return fail(SIRIUS_EINVAL, "%s: Lmax=%d outside [n, %d]", fn, Lmax, kMaxCacheLen);
+  const long rows = (long)(H / Hkv) * n;
+  if ((long)Hkv * ((rows + 63) / 64) > kMaxLogitRows)
+    return fail(SIRIUS_EINVAL, "%s: too many query rows per call", fn);
+  int rc;
+  if ((rc = check_ptrs(fn, {{q, "q"}, {k_new, "k_new"}, {v_new, "v_new"}, {k_cache, "k_cache"},
+                            {v_cache, "v_cache"}, {out, "out"}, {ws, "ws"}})))
+    return rc;
+  if (cache_pos == nullptr) return fail(SIRIUS_EINVAL, "%s: cache_pos is NULL", fn);
+  if (B == 0) return SIRIUS_OK;
+  const sirius::AttnLayout L = sirius::attn_layout(B, n, H, Hkv, head_dim, Lmax);
+  if (ws_bytes < L.total)
+    return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, L.total);
+  return hip_status(sirius::launch_attn_kv(q, k_new, v_new, k_cache, v_cache, cache_pos, B, n, H,
+                                           Hkv, head_dim, Lmax, out, static_cast<char*>(ws), L,
+                                           static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int sirius_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n, void* stream) {
+  const char* fn = "sirius_kv_rollback";
+  if (cache_pos == nullptr || accept_len == nullptr) return fail(SIRIUS_EINVAL, "%s: NULL pointer", fn);
+  if (B < 0 || n < 1) return fail(SIRIUS_EINVAL, "%s: bad sizes B=%d n=%d", fn, B, n);
+  if (B == 0) return SIRIUS_OK;
+  return hip_status(sirius::launch_kv_rollback(cache_pos, accept_len, B, n,
                                                static_cast<hipStream_t>(stream)),
                     fn);
 }

@@ -140,6 +140,21 @@ hipError_t launch_tree_build(const float* logits, int B, int Wc, int V, const fl
                              float* cum_out, char* ws, const TreeBuildLayout& L,
                              hipStream_t stream);
 
+// ---- attention over the shared KV cache with the direct rewrite, and the rollback
+struct AttnLayout {
+  int rgroups, chunk, nsplit;    // query-row groups per kv head, positions per chunk, chunks
+  size_t pm, pl, po, total;      // per-chunk partials: max, sum, output
+};
+AttnLayout attn_layout(int B, int n, int H, int Hkv, int hd, int Lmax);
+// q [B][n][H][hd] fp32; k_new, v_new [B][n][Hkv][hd] bf16; caches [B][Lmax][Hkv][hd] bf16;
+// cache_pos [B] on the device; out [B][n][H][hd]. hd % 8 == 0, hd <= 128, H % Hkv == 0.
+hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t* v_new,
+                          uint16_t* k_cache, uint16_t* v_cache, const int32_t* cache_pos, int B,
+                          int n, int H, int Hkv, int hd, int Lmax, float* out, char* ws,
+                          const AttnLayout& L, hipStream_t stream);
+hipError_t launch_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n,
+                              hipStream_t stream);
+
 // ---- glue
 hipError_t launch_rmsnorm(const float* h, int B, int d, float eps, float* out, hipStream_t stream);
 hipError_t launch_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, float std,

@@ -15,6 +15,7 @@ from .inputs import (  # noqa: F401
     verify_inputs,
     tree_build_inputs,
     tree_verify_inputs,
+    attn_inputs,
     TINY,
     LLAMA3_8B,
     LLAMA3_70B,

@@ -68,6 +68,7 @@ _STREAM_CALIB = 3
 _STREAM_PROMPT = 4
 _STREAM_LOGITS = 5
 _STREAM_TREE = 6
+_STREAM_ATTN = 7
 
 
 def ffn_weights(seed: int, d_model: int, d_ff: int, std: float):
@@ -177,3 +178,16 @@ def tree_verify_inputs(seed: int, batch: int, k: int, w: int, vocab: int, logit_
                 else:
                     logits[b, row, tok] += bump[b, i, j]
     return logits, tokens, parents
+
+
+def attn_inputs(seed: int, batch: int, n: int, heads: int, kv_heads: int, head_dim: int, lmax: int):
+    """One attention call's inputs: q [batch, n, heads, head_dim] fp32 ~ N(0, 1); new keys and
+    values [batch, n, kv_heads, head_dim] and the caches [batch, lmax, kv_heads, head_dim] ~ N(0, 1)
+    stored as bf16 bits."""
+    rng = _rng(seed, _STREAM_ATTN)
+    q = rng.standard_normal((batch, n, heads, head_dim), dtype=np.float32)
+    kn = bf16_bits(rng.standard_normal((batch, n, kv_heads, head_dim), dtype=np.float32))
+    vn = bf16_bits(rng.standard_normal((batch, n, kv_heads, head_dim), dtype=np.float32))
+    kc = bf16_bits(rng.standard_normal((batch, lmax, kv_heads, head_dim), dtype=np.float32))
+    vc = bf16_bits(rng.standard_normal((batch, lmax, kv_heads, head_dim), dtype=np.float32))
+    return q, kn, vn, kc, vc

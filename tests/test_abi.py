@@ -206,6 +206,32 @@ def test_tree_verify_argument_errors(L):
     assert call(a1=0) == 0             # empty batch
 
 
+def test_attn_argument_errors(L):
+    big = 1 << 30
+    # q, k_new, v_new, k_cache, v_cache, cache_pos, B, n, H, Hkv, hd, Lmax, out, ws, ws_bytes, stream
+    base = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 16, 32, 8, 128, 4096, FAKE, FAKE, big, None]
+
+    def call(**kw):
+        a = list(base)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.sirius_attn_kv(*a)
+
+    assert call(a7=0) == -1            # n < 1
+    assert call(a7=2000) == -1         # n above 1024
+    assert call(a8=30) == -1 and "Hkv" in _err(L)   # H not a multiple of Hkv
+    assert call(a10=100) == -1         # head_dim not a multiple of 8
+    assert call(a10=256) == -1         # head_dim above 128
+    assert call(a11=8) == -1           # Lmax < n
+    assert call(a5=None) == -1         # cache_pos NULL
+    assert call(a3=ctypes.c_void_p((1 << 20) + 8)) == -1 and "aligned" in _err(L)
+    assert call(a14=16) == -2          # workspace too small
+    assert call(a6=0) == 0             # empty batch
+    assert L.sirius_kv_rollback(None, FAKE, 1, 16, None) == -1
+    assert L.sirius_kv_rollback(FAKE, FAKE, 1, 0, None) == -1
+    assert L.sirius_kv_rollback(FAKE, FAKE, 0, 16, None) == 0
+
+
 def test_glue_argument_errors(L):
     assert L.sirius_rmsnorm(None, 1, 64, 1e-5, FAKE, None) == -1
     assert L.sirius_rmsnorm(FAKE, 1, 64, -1.0, FAKE, None) == -1
@@ -231,6 +257,10 @@ def test_workspace_sizes(L):
     # per-token top-k: the activation buffer and cuts come before the FFN workspace
     assert f(8, 1, 4096, 14336, 0, 0) >= 14336 * 4 + f(1, 1, 4096, 14336, 0, 0)
     assert f(8, 3, 4096, 14336, 0, 0) >= 3 * 14336 * 4 + f(1, 3, 4096, 14336, 0, 0)
+    # attention: B, n, H * 65536 + Hkv, head_dim, Lmax
+    assert f(9, 1, 16, 32 * 65536 + 8, 128, 4096) > 0
+    assert f(9, 1, 16, 30 * 65536 + 8, 128, 4096) == 0
+    assert f(9, 1, 16, 32 * 65536 + 8, 128, 8) == 0
     # tree drafting step: B, Wc, W, V
     assert f(6, 1, 8, 8, 128256, 0) > 0
     assert f(6, 1, 17, 8, 128256, 0) == 0

@@ -38,3 +38,13 @@ def test_verify_generator_shapes_and_boost():
     for b in range(2):
         for j in range(4):
             assert lg2[b, j, dr2[b, j]] == lg2[b, j].max()
+
+
+def test_attention_generator_shapes_and_types():
+    from synth import attn_inputs
+    q, kn, vn, kc, vc = attn_inputs(3, 2, 4, 8, 2, 16, 50)
+    assert q.shape == (2, 4, 8, 16) and q.dtype == np.float32
+    assert kn.shape == vn.shape == (2, 4, 2, 16) and kn.dtype == np.uint16
+    assert kc.shape == vc.shape == (2, 50, 2, 16) and kc.dtype == np.uint16
+    q2, *_ = attn_inputs(3, 2, 4, 8, 2, 16, 50)
+    assert np.array_equal(q, q2)
