@@ -21,6 +21,10 @@ batch, all inputs resident in HBM:
   tree_build one drafting step of a width-4 tree: logits [4, 128256] at the current leaves
   tree_verify verification of a 16-step, width-4 tree with bonus rows: logits [68, 128256]
   topk      per-token top-k sparse FFN decode, one token, k = d_ff / 2 (the paper's FSparse)
+  attn1     attention decode step over the shared KV cache (Llama-3-8B heads: 32 query, 8
+            key/value, head size 128; 2048 cached rows), writing its own row
+  attn16    the full model's verification pass over a 16-token chunk at the same position:
+            rewrite of the 16 rows + causal attention; then the device-side rollback
   cats70b   sparse FFN decode, one token, one Llama-3-70B FFN layer (d_model 8192,
             d_ff 28672, 50% calibrated), four rotated copies (5.6 GB)
 The printed value is the sparse FFN decode time per token (rows.cats, from
@@ -55,6 +59,7 @@ N_DECODE = 64
 PROMPT_T = 512
 VERIFY_B, VERIFY_K, VERIFY_V = 8, 16, 128256
 TREE_K, TREE_W = 16, 4
+ATT_H, ATT_HKV, ATT_HD, ATT_L, ATT_P = 32, 8, 128, 4096, 2048
 N_LOGIT_BUFS = 4
 
 
@@ -117,7 +122,7 @@ def main():
     import torch
     import paper_2409_03856_amd as sr
     from synth import (decode_inputs, calibration_inputs, griffin_prompt, verify_inputs, tree_build_inputs,
-                       tree_verify_inputs)
+                       tree_verify_inputs, attn_inputs)
 
     assert torch.cuda.is_available()
     dev = torch.device("cuda", 0)
@@ -197,11 +202,20 @@ def main():
     tb_out = [torch.empty((1, TREE_W), dtype=dt, device=dev) for dt in (torch.int32, torch.int32, torch.float32)]
     tv_out = [torch.empty(1, dtype=torch.int32, device=dev) for _ in range(3)]
     yt = torch.empty_like(y)
+    log("setup: attention caches")
+    att = []
+    for i in range(2):
+        q1, kn1, vn1, kc, vc = attn_inputs(40 + i, 1, 16, ATT_H, ATT_HKV, ATT_HD, ATT_L)
+        bits = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        att.append((torch.from_numpy(q1).to(dev), bits(kn1), bits(vn1), bits(kc), bits(vc)))
+    att_pos = torch.full((1,), ATT_P, dtype=torch.int32, device=dev)
+    att_acc = torch.zeros((1,), dtype=torch.int32, device=dev)
+    att_out = torch.empty((1, 16, ATT_H, ATT_HD), dtype=torch.float32, device=dev)
     act_t = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
     cnt_t = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
 
     rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "tree_build", "tree_verify",
-            "topk", "cats70b"]
+            "topk", "attn1", "attn16", "cats70b"]
     stream = torch.cuda.current_stream()
 
     def step(s, ev=None, with70=True):
@@ -211,6 +225,7 @@ def main():
             if ev is not None:
                 ev[i].record(stream)
 
+        att_pos.fill_(ATT_P)  # every step's attention starts from the same cached prefix
         mark(0)
         sr.sirius_ffn_cats(xs[s % N_DECODE: s % N_DECODE + 1], *layers[c], thresholds[c], y=y,
                            active_idx=act_idx, active_cnt=cnt_log[s:s + 1])
@@ -240,12 +255,18 @@ def main():
         sr.sirius_ffn_topk(xs[(s + 3) % N_DECODE:(s + 3) % N_DECODE + 1], *layers[(c + 5) % NCOPY], k_keep, y=yt,
                            active_idx=act_t, active_cnt=cnt_t[s:s + 1])
         mark(10)
+        a = att[s % 2]
+        sr.sirius_attn_kv(a[0][:, :1], a[1][:, :1], a[2][:, :1], a[3], a[4], att_pos, out=att_out[:, :1])
+        mark(11)
+        sr.sirius_attn_kv(a[0], a[1], a[2], a[3], a[4], att_pos, out=att_out)
+        sr.sirius_kv_rollback(att_pos, att_acc, 16)
+        mark(12)
         if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
             return
         c70 = s % NCOPY70
         sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
                            active_idx=act70, active_cnt=cnt70[s:s + 1])
-        mark(11)
+        mark(13)
 
     log("warmup")
     for s in range(args.warmup):
@@ -280,7 +301,7 @@ def main():
     for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
                  "ffn_mfma_reduce",
                  "verify_stats", "verify_scan", "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate", "topk_cut", "topk_decode",
-                 "topk_reduce", "griffin_z", "griffin_topk", "griffin_score", "condense",
+                 "topk_reduce", "attn_partial", "attn_combine", "kv_rollback", "griffin_z", "griffin_topk", "griffin_score", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:
         tot, n = sr.sirius_profile_query(name)
         if n:
@@ -302,6 +323,9 @@ def main():
                  "verify": verify_bytes, "tree_build": TREE_W * VERIFY_V * 4 + 2 * TREE_W * 4,
                  "tree_verify": (TREE_K + 1) * TREE_W * VERIFY_V * 4 + 2 * TREE_K * TREE_W * 4,
                  "topk": D_FF * D_MODEL * 2 + 2 * k_keep * D_MODEL * 2 + 2 * D_MODEL * 4,
+                 "attn1": (ATT_P + 1) * ATT_HKV * ATT_HD * 2 * 2 + 2 * ATT_H * ATT_HD * 4,
+                 "attn16": (ATT_P + 16) * ATT_HKV * ATT_HD * 2 * 2 + 16 * ATT_HKV * ATT_HD * 2 * 2
+                 + 2 * 16 * ATT_H * ATT_HD * 4,
                  "cats70b": cats70_bytes}
 
     def med(v):

@@ -34,31 +34,27 @@ constexpr int kMaxHd = 128;
 constexpr int kMaxRowsWg = 64;            // query rows per workgroup
 constexpr int kPitch = kMaxHd + 4;        // LDS row pitch (floats): 16-byte rows off the banks
 constexpr int kPPitch = kMaxRowsWg + 4;   // score tile pitch: a position's rows off the banks
+constexpr int kKVPitch8 = kMaxHd / 8 + 1; // bf16 key/value rows in 16-byte units (+1 off the banks)
 constexpr int kMaxOB = 2;                 // 4 x 4 output blocks per thread: 64 rows x 128 / 256 / 16
+constexpr int kStagePer = kTile * kMaxHd / 8 / kAttnThreads;  // 16-byte loads per thread and tile
+constexpr int kMaxSplits = 256;           // position chunks per call at most
 
-__device__ __forceinline__ void widen8(uint4 w, float* dst) {
-  dst[0] = bf16_lo(w.x);
-  dst[1] = bf16_hi(w.x);
-  dst[2] = bf16_lo(w.y);
-  dst[3] = bf16_hi(w.y);
-  dst[4] = bf16_lo(w.z);
-  dst[5] = bf16_hi(w.z);
-  dst[6] = bf16_lo(w.w);
-  dst[7] = bf16_hi(w.w);
-}
-
-// BIG: up to 64 rows, scores in 4 x 4 blocks; else up to 16 rows, 4 x 1 blocks.
+// BIG: up to 64 rows, scores in 4 x 4 register blocks; else up to 16 rows, each score's dot
+// product split over four lanes. Keys and values are staged as bf16; the score tile reuses
+// the key buffer once the scores are formed (69 KB of LDS: two workgroups per CU).
 template <bool BIG>
 __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float* __restrict__ q, const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
     uint4* __restrict__ k_cache, uint4* __restrict__ v_cache, const int32_t* __restrict__ cache_pos,
     int n, int H, int Hkv, int hd, int Lmax, int chunk, int rgroups, int R, float scale,
     float* __restrict__ pm, float* __restrict__ pl, float* __restrict__ po) {
-  __shared__ float s_q[kMaxRowsWg * kPitch];
-  __shared__ float s_k[kTile * kPitch];
-  __shared__ float s_v[kTile * kPitch];
-  __shared__ float s_p[kTile * kPPitch];  // scores, then probabilities, [position][row]
-  __shared__ float s_m[kMaxRowsWg], s_l[kMaxRowsWg], s_alpha[kMaxRowsWg];
+  constexpr int kRows = BIG ? kMaxRowsWg : 16;
+  __shared__ float s_q[kRows * kPitch];
+  __shared__ uint4 s_kp[kTile * kKVPitch8];  // keys (bf16), then the score tile [position][row]
+  __shared__ uint4 s_v[kTile * kKVPitch8];   // values (bf16)
+  __shared__ float s_m[kRows], s_l[kRows], s_alpha[kRows];
+  float* s_p = reinterpret_cast<float*>(s_kp);
+  const uint16_t* s_v16 = reinterpret_cast<const uint16_t*>(s_v);
   const int tid = threadIdx.x;
   const int split = blockIdx.x, nsplit = gridDim.x;
   const int kvh = blockIdx.y / rgroups, rg = blockIdx.y % rgroups, b = blockIdx.z;
@@ -67,7 +63,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   const bool valid = p >= 0 && p + n <= Lmax;
   const int L = p + n;
   const int c0 = split * chunk, c1 = min(c0 + chunk, L);
-  const int r0 = rg * kMaxRowsWg, nr = min(kMaxRowsWg, R - r0);
+  const int r0 = rg * kMaxRowsWg, nr = min(kRows, R - r0);
   const int nr4 = (nr + 3) & ~3;
   const int hd4 = hd >> 2, hd8 = hd >> 3;
   const size_t rowbase = ((size_t)b * Hkv + kvh) * R + r0;  // partial row index of row r0
@@ -108,8 +104,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     s_m[tid] = -INFINITY;
     s_l[tid] = 0.f;
   }
-  // output blocks: block ob = rows 4 (ob / hd4) .. + 4, columns 4 (ob % hd4) .. + 4
+  // output blocks of 4 rows x 4 columns; with few blocks the positions of a tile are split
+  // over jg groups of threads, each accumulating its own share (summed once at the end)
   const int nob = (nr4 >> 2) * hd4;
+  const int jg = BIG ? 1 : max(1, min(8, kAttnThreads / nob));
+  const int jgrp = tid / nob, job = tid - jgrp * nob;  // group, block (non-BIG)
   float4 acc[kMaxOB][4];
 #pragma unroll
   for (int u = 0; u < kMaxOB; ++u)
@@ -118,64 +117,133 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 
   for (int t0 = c0; t0 < c1; t0 += kTile) {
     const int tn = min(kTile, c1 - t0);
-    __syncthreads();  // the previous step's readers are done with s_k, s_v, s_p
-    // ---- stage keys and values (fp32): cache rows below p, new rows from p on; zero past tn
-    for (int e = tid; e < kTile * hd8; e += kAttnThreads) {
-      const int j = e / hd8, c = e - j * hd8, pos = t0 + j;
-      uint4 kw = make_uint4(0u, 0u, 0u, 0u), vw = make_uint4(0u, 0u, 0u, 0u);
-      if (j < tn) {
-        if (pos < p) {
-          const size_t i = (((size_t)b * Lmax + pos) * Hkv + kvh) * hd8 + c;
-          kw = k_cache[i];
-          vw = v_cache[i];
-        } else {
-          const size_t i = (((size_t)b * n + (pos - p)) * Hkv + kvh) * hd8 + c;
-          kw = k_new[i];
-          vw = v_new[i];
+    __syncthreads();  // the previous step's readers are done with s_kp, s_v
+    // ---- stage keys and values (bf16): cache rows below p, new rows from p on; zero past tn.
+    // Every load of the tile is issued before the first is stored.
+    {
+      uint4 kw[kStagePer], vw[kStagePer];
+#pragma unroll
+      for (int u = 0; u < kStagePer; ++u) {
+        const int e = tid + u * kAttnThreads;
+        const int j = e / hd8, c = e - j * hd8, pos = t0 + j;
+        kw[u] = make_uint4(0u, 0u, 0u, 0u);
+        vw[u] = make_uint4(0u, 0u, 0u, 0u);
+        if (j < tn) {
+          const size_t i = (pos < p) ? (((size_t)b * Lmax + pos) * Hkv + kvh) * hd8 + c
+                                     : (((size_t)b * n + (pos - p)) * Hkv + kvh) * hd8 + c;
+          kw[u] = ((pos < p) ? k_cache : k_new)[i];
+          vw[u] = ((pos < p) ? v_cache : v_new)[i];
         }
       }
-      widen8(kw, &s_k[j * kPitch + 8 * c]);
-      widen8(vw, &s_v[j * kPitch + 8 * c]);
+#pragma unroll
+      for (int u = 0; u < kStagePer; ++u) {
+        const int e = tid + u * kAttnThreads;
+        const int j = e / hd8, c = e - j * hd8;
+        if (j < kTile) {
+          s_kp[j * kKVPitch8 + c] = kw[u];
+          s_v[j * kKVPitch8 + c] = vw[u];
+        }
+      }
     }
     __syncthreads();
-    // ---- scores with the causal mask, into s_p[position][row]
-    {
-      constexpr int CB = BIG ? 4 : 1;
-      const int ncb = kTile / CB;  // positions cb, cb + ncb, ... (neighbouring lanes, rows)
-      const int rb = tid / ncb, cb = tid - rb * ncb;
+    // ---- scores with the causal mask (held in registers until the keys are no longer read)
+    constexpr int CB = BIG ? 4 : 1;
+    float sc[4][CB];   // BIG: rows 4 rb.., positions cb + 16 cc; else rows of row block rbs
+    float scs[4][4];   // non-BIG: four row blocks x four rows, one position
+    if (BIG) {
+      const int rb = tid >> 4, cb = tid & 15;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+        for (int cc = 0; cc < CB; ++cc) sc[rr][cc] = 0.f;
       if (4 * rb < nr4) {
-        float s[4][CB];
+        for (int d8 = 0; d8 < hd8; ++d8) {
+          float kf[CB][8];
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
+          for (int cc = 0; cc < CB; ++cc) {
+            const uint4 w = s_kp[(cb + 16 * cc) * kKVPitch8 + d8];
+            kf[cc][0] = bf16_lo(w.x); kf[cc][1] = bf16_hi(w.x); kf[cc][2] = bf16_lo(w.y);
+            kf[cc][3] = bf16_hi(w.y); kf[cc][4] = bf16_lo(w.z); kf[cc][5] = bf16_hi(w.z);
+            kf[cc][6] = bf16_lo(w.w); kf[cc][7] = bf16_hi(w.w);
+          }
 #pragma unroll
-          for (int cc = 0; cc < CB; ++cc) s[rr][cc] = 0.f;
-        for (int d4 = 0; d4 < hd4; ++d4) {
-          float4 qv[4], kv[CB];
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            qv[rr] = *reinterpret_cast<const float4*>(&s_q[(4 * rb + rr) * kPitch + 4 * d4]);
-#pragma unroll
-          for (int cc = 0; cc < CB; ++cc)
-            kv[cc] = *reinterpret_cast<const float4*>(&s_k[(cb + ncb * cc) * kPitch + 4 * d4]);
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
+          for (int rr = 0; rr < 4; ++rr) {
+            const float4 qa = *reinterpret_cast<const float4*>(&s_q[(4 * rb + rr) * kPitch + 8 * d8]);
+            const float4 qb = *reinterpret_cast<const float4*>(&s_q[(4 * rb + rr) * kPitch + 8 * d8 + 4]);
 #pragma unroll
             for (int cc = 0; cc < CB; ++cc) {
-              s[rr][cc] = fmaf(qv[rr].x, kv[cc].x, s[rr][cc]);
-              s[rr][cc] = fmaf(qv[rr].y, kv[cc].y, s[rr][cc]);
-              s[rr][cc] = fmaf(qv[rr].z, kv[cc].z, s[rr][cc]);
-              s[rr][cc] = fmaf(qv[rr].w, kv[cc].w, s[rr][cc]);
+              float a = sc[rr][cc];
+              a = fmaf(qa.x, kf[cc][0], a); a = fmaf(qa.y, kf[cc][1], a);
+              a = fmaf(qa.z, kf[cc][2], a); a = fmaf(qa.w, kf[cc][3], a);
+              a = fmaf(qb.x, kf[cc][4], a); a = fmaf(qb.y, kf[cc][5], a);
+              a = fmaf(qb.z, kf[cc][6], a); a = fmaf(qb.w, kf[cc][7], a);
+              sc[rr][cc] = a;
             }
+          }
         }
+      }
+    } else {
+      // position j = tid / 4; lane quarter dq takes head-dim chunks dq, dq + 4, ...
+      const int j = tid >> 2, dq = tid & 3;
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) scs[rb][rr] = 0.f;
+      for (int d8 = dq; d8 < hd8; d8 += 4) {
+        const uint4 w = s_kp[j * kKVPitch8 + d8];
+        const float kf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                             bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+          if (4 * rb < nr4) {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+              const float4 qa = *reinterpret_cast<const float4*>(&s_q[(4 * rb + rr) * kPitch + 8 * d8]);
+              const float4 qb = *reinterpret_cast<const float4*>(&s_q[(4 * rb + rr) * kPitch + 8 * d8 + 4]);
+              float a = scs[rb][rr];
+              a = fmaf(qa.x, kf[0], a); a = fmaf(qa.y, kf[1], a);
+              a = fmaf(qa.z, kf[2], a); a = fmaf(qa.w, kf[3], a);
+              a = fmaf(qb.x, kf[4], a); a = fmaf(qb.y, kf[5], a);
+              a = fmaf(qb.z, kf[6], a); a = fmaf(qb.w, kf[7], a);
+              scs[rb][rr] = a;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          scs[rb][rr] += __shfl_xor(scs[rb][rr], 1, kWave);
+          scs[rb][rr] += __shfl_xor(scs[rb][rr], 2, kWave);
+        }
+    }
+    __syncthreads();  // keys read: the score tile takes their place
+    if (BIG) {
+      const int rb = tid >> 4, cb = tid & 15;
+      if (4 * rb < nr4) {
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
           const int r = 4 * rb + rr;
           const int lim = p + (r0 + r) / G;  // last visible position of row r
 #pragma unroll
           for (int cc = 0; cc < CB; ++cc) {
-            const int j = cb + ncb * cc;
+            const int j = cb + 16 * cc;
             // padding rows get 0 (they never enter the softmax); hidden positions -inf
-            s_p[j * kPPitch + r] = (r >= nr) ? 0.f : ((j < tn && t0 + j <= lim) ? s[rr][cc] : -INFINITY);
+            s_p[j * kPPitch + r] = (r >= nr) ? 0.f : ((j < tn && t0 + j <= lim) ? sc[rr][cc] : -INFINITY);
+          }
+        }
+      }
+    } else if ((tid & 3) == 0) {
+      const int j = tid >> 2;
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        if (4 * rb < nr4) {
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int r = 4 * rb + rr;
+            const int lim = p + (r0 + r) / G;
+            s_p[j * kPPitch + r] = (r >= nr) ? 0.f : ((j < tn && t0 + j <= lim) ? scs[rb][rr] : -INFINITY);
           }
         }
       }
@@ -216,11 +284,12 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       }
     }
     __syncthreads();
-    // ---- O = alpha O + P V over 4 x 4 output blocks
+    // ---- O = alpha O + P V over 4 x 4 output blocks (a thread group's share of positions)
 #pragma unroll
     for (int u = 0; u < kMaxOB; ++u) {
-      const int ob = tid + u * kAttnThreads;
-      if (ob < nob) {
+      const int ob = BIG ? tid + u * kAttnThreads : job;
+      const bool mine = BIG ? (ob < nob) : (u == 0 && jgrp < jg);
+      if (mine) {
         const int rb = ob / hd4, d4 = ob - rb * hd4;
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
@@ -231,62 +300,120 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
           acc[u][rr].z *= al;
           acc[u][rr].w *= al;
         }
-        for (int j = 0; j < tn; ++j) {
+        const int span = kTile / jg, j0 = (BIG ? 0 : jgrp) * span, j1 = min(j0 + span, tn);
+        for (int j = j0; j < j1; ++j) {
           const float4 pv = *reinterpret_cast<const float4*>(&s_p[j * kPPitch + 4 * rb]);
-          const float4 vv = *reinterpret_cast<const float4*>(&s_v[j * kPitch + 4 * d4]);
+          const uint2 vw = *reinterpret_cast<const uint2*>(&s_v16[j * kKVPitch8 * 8 + 4 * d4]);
+          const float vv[4] = {bf16_lo(vw.x), bf16_hi(vw.x), bf16_lo(vw.y), bf16_hi(vw.y)};
           const float pr[4] = {pv.x, pv.y, pv.z, pv.w};
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            acc[u][rr].x = fmaf(pr[rr], vv.x, acc[u][rr].x);
-            acc[u][rr].y = fmaf(pr[rr], vv.y, acc[u][rr].y);
-            acc[u][rr].z = fmaf(pr[rr], vv.z, acc[u][rr].z);
-            acc[u][rr].w = fmaf(pr[rr], vv.w, acc[u][rr].w);
+            acc[u][rr].x = fmaf(pr[rr], vv[0], acc[u][rr].x);
+            acc[u][rr].y = fmaf(pr[rr], vv[1], acc[u][rr].y);
+            acc[u][rr].z = fmaf(pr[rr], vv[2], acc[u][rr].z);
+            acc[u][rr].w = fmaf(pr[rr], vv[3], acc[u][rr].w);
           }
         }
       }
     }
   }
   // ---- this chunk's partial: max, sum and the unnormalised output per row
+  __syncthreads();
   if (tid < nr) {
     pm[(rowbase + tid) * nsplit + split] = s_m[tid];
     pl[(rowbase + tid) * nsplit + split] = s_l[tid];
   }
+  if (BIG) {
 #pragma unroll
-  for (int u = 0; u < kMaxOB; ++u) {
-    const int ob = tid + u * kAttnThreads;
-    if (ob < nob) {
-      const int rb = ob / hd4, d4 = ob - rb * hd4;
+    for (int u = 0; u < kMaxOB; ++u) {
+      const int ob = tid + u * kAttnThreads;
+      if (ob < nob) {
+        const int rb = ob / hd4, d4 = ob - rb * hd4;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int r = 4 * rb + rr;
+          if (r < nr)
+            reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = acc[u][rr];
+        }
+      }
+    }
+  } else {
+    // sum the position groups' shares in order through LDS (the value buffer is free)
+    float4* s_red = reinterpret_cast<float4*>(s_v);  // [group][block][4 rows]: <= 8 x 64 x 4
+    if (jgrp < jg) {
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) s_red[(jgrp * nob + job) * 4 + rr] = acc[0][rr];
+    }
+    __syncthreads();
+    if (tid < nob) {
+      const int rb = tid / hd4, d4 = tid - rb * hd4;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
+        float4 t = s_red[tid * 4 + rr];
+        for (int g2 = 1; g2 < jg; ++g2) {
+          const float4 o = s_red[(g2 * nob + tid) * 4 + rr];
+          t.x += o.x;
+          t.y += o.y;
+          t.z += o.z;
+          t.w += o.w;
+        }
         const int r = 4 * rb + rr;
-        if (r < nr)
-          reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = acc[u][rr];
+        if (r < nr) reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = t;
       }
     }
   }
 }
 
-// One workgroup (hd threads) per query row: the chunks merged in order.
+// One workgroup (hd threads) per query row: the chunks' maxima and weights first (one chunk
+// per thread, LDS), then each thread sums its output column over the chunks in order with the
+// loads issued ahead.
 __global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
     int n, int H, int Hkv, int hd, int R, int nsplit, const float* __restrict__ pm,
     const float* __restrict__ pl, const float* __restrict__ po, float* __restrict__ out) {
+  __shared__ float s_m[kMaxSplits], s_w[kMaxSplits], s_red[kMaxHd / kWave];
   const int row = blockIdx.x;  // (b, kvh, r)
   const int r = row % R, bk = row / R, kvh = bk % Hkv, b = bk / Hkv;
   const int G = H / Hkv, i = r / G, h = kvh * G + (r - i * G);
-  const int d = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const float* m = pm + (size_t)row * nsplit;
   const float* l = pl + (size_t)row * nsplit;
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, m[s]);
-  float den = 0.f, num = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    if (m[s] > -INFINITY) {
-      const float w = expf(m[s] - M);
-      den = fmaf(l[s], w, den);
-      if (d < hd) num = fmaf(po[((size_t)row * nsplit + s) * hd + d], w, num);
-    }
+  float mx = -INFINITY;
+  for (int sp = tid; sp < nsplit; sp += kMaxHd) {
+    const float v = m[sp];
+    s_m[sp] = v;
+    mx = fmaxf(mx, v);
   }
-  if (d < hd) out[(((size_t)b * n + i) * H + h) * hd + d] = num / den;
+  mx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
+  for (int k = 2; k < kWave; k <<= 1) mx = fmaxf(mx, __shfl_xor(mx, k, kWave));
+  if (lane == 0) s_red[wave] = mx;
+  __syncthreads();
+  float M = s_red[0];
+  for (int w = 1; w < kMaxHd / kWave; ++w) M = fmaxf(M, s_red[w]);
+  __syncthreads();
+  float den = 0.f;
+  for (int sp = tid; sp < nsplit; sp += kMaxHd) {
+    const float w = (s_m[sp] > -INFINITY) ? expf(s_m[sp] - M) : 0.f;
+    s_w[sp] = w;
+    den = fmaf(l[sp], w, den);
+  }
+  for (int k = 1; k < kWave; k <<= 1) den += __shfl_xor(den, k, kWave);
+  if (lane == 0) s_red[wave] = den;
+  __syncthreads();
+  den = 0.f;
+  for (int w = 0; w < kMaxHd / kWave; ++w) den += s_red[w];
+  if (tid < hd) {
+    const float* o = po + (size_t)row * nsplit * hd + tid;
+    float num = 0.f;
+    for (int s0 = 0; s0 < nsplit; s0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = (s0 + u < nsplit && s_w[s0 + u] > 0.f) ? o[(size_t)(s0 + u) * hd] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < nsplit) num = fmaf(v[u], s_w[s0 + u], num);
+    }
+    out[(((size_t)b * n + i) * H + h) * hd + tid] = num / den;
+  }
 }
 
 __global__ void kv_rollback_kernel(int32_t* __restrict__ cache_pos,
@@ -304,7 +431,7 @@ AttnLayout attn_layout(int B, int n, int H, int Hkv, int hd, int Lmax) {
   AttnLayout L{};
   const int R = (H / Hkv) * n;
   L.rgroups = ceil_div(R, kMaxRowsWg);
-  L.chunk = kTile * std::max(1, ceil_div(ceil_div(Lmax, kTile), 256));  // 256 chunks at most
+  L.chunk = kTile * std::max(1, ceil_div(ceil_div(Lmax, kTile), kMaxSplits));
   L.nsplit = ceil_div(Lmax, L.chunk);
   const size_t rows = (size_t)B * Hkv * R;
   Carve c;
@@ -328,7 +455,7 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
   const dim3 grid(L.nsplit, Hkv * L.rgroups, B);
   {
     ProfScope prof("attn_partial", stream);
-    if (std::min(R, kMaxRowsWg) > 16)
+    if (R > 16)
       attn_partial_kernel<true><<<grid, kAttnThreads, 0, stream>>>(
           q, reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new),
           reinterpret_cast<uint4*>(k_cache), reinterpret_cast<uint4*>(v_cache), cache_pos, n, H,
