@@ -32,7 +32,9 @@ row-boundary HIP events in the timed region). The roofline object is for the
 sparse path's dominant kernel (cats_decode: gate GEMV, threshold, compaction,
 kept up rows and kept down rows in one pass; the other launch is the small
 fixed-order reduce), timed by the library's per-kernel HIP events in a second
-pass of the same K steps right after the timed region. Its `traffic` is the
+pass of the same K steps right after the timed region. Those events ride on the
+kernel's own dispatch packet (hipExtLaunchKernel), so they time the kernel from
+its start to its end, as a kernel trace does. Its `traffic` is the
 HBM byte count per launch from the committed rocprofv3 counter summary under
 profiles/, reported only while that summary's kernel-source digest matches the
 current sources (`--copy-mib` adds the plain copy whose counters scale
@@ -377,7 +379,7 @@ def main():
             "traffic": counted_traffic(),
             "alg_bytes_per_launch": int(dom_bytes),
             "avg_launch_us": dom_us,
-            "timing": "library per-kernel HIP events on the launch stream, separate K-step pass",
+            "timing": "library per-kernel HIP events carried by the kernel dispatch itself (hipExtLaunchKernel) on the launch stream, separate K-step pass",
         },
         "rows": rows_out,
         "kernels": kern,

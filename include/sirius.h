@@ -305,18 +305,22 @@ int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, 
                             void* stream);
 
 /*
- * Per-kernel timing, for measurement. While enabled, every kernel the library
- * launches is bracketed by a pair of HIP events recorded on the stream the
- * kernel runs on (a small launch overhead per kernel). sirius_profile_query
- * waits for the recorded events of one kernel name and returns the summed
- * duration in milliseconds and the number of launches (0 and 0 for an
- * unknown name). Kernel names: "cats_gate", "ffn_down", "ffn_reduce",
- * "ffn_mfma_gate_up", "verify_stats", "verify_scan", "griffin_z",
- * "griffin_rownorm", "griffin_score", "select_init", "select_hist",
- * "select_pick", "griffin_pick", "condense", "rmsnorm", "fill_normal",
- * "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate",
- * "topk_cut", "topk_decode", "topk_up", "topk_down", "topk_reduce",
- * "attn_partial", "attn_combine", "kv_rollback".
+ * Per-kernel timing, for measurement. While enabled, each kernel the library
+ * launches carries a pair of HIP events on its own dispatch (hipExtLaunchKernel):
+ * the elapsed time between them is the kernel's execution time, as a kernel
+ * trace reports it (where one name covers several launches of one call, from
+ * the first one's start to the last one's end). sirius_profile_query waits for
+ * the events of one kernel name and returns the summed duration in
+ * milliseconds and the number of launches (0 and 0 for an unknown name).
+ * Kernel names: "cats_decode", "cats_reduce", "dense_decode", "dense_reduce",
+ * "topk_decode", "topk_reduce" (batch 1); "cats_gate", "cats_down",
+ * "dense_gate", "dense_down", "topk_up", "topk_down" (batches 2..8);
+ * "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down", "ffn_mfma_reduce";
+ * "calib_gate", "select_init", "select_hist", "select_pick"; "topk_gate",
+ * "topk_cut"; "verify_stats", "verify_scan", "tree_stats", "tree_scan",
+ * "tree_topw", "tree_select"; "griffin_z", "griffin_rownorm", "griffin_score",
+ * "griffin_topk", "condense"; "rmsnorm", "fill_normal"; "attn_partial",
+ * "attn_combine", "kv_rollback".
  * sirius_profile_reset drops every record (it waits for pending events).
  * Errors: SIRIUS_EINVAL for NULL arguments, SIRIUS_EHIP if an event fails.
  */

@@ -456,12 +456,12 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
   {
     ProfScope prof("attn_partial", stream);
     if (R > 16)
-      attn_partial_kernel<true><<<grid, kAttnThreads, 0, stream>>>(
+      klaunch(attn_partial_kernel<true>, grid, kAttnThreads, 0, stream, 
           q, reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new),
           reinterpret_cast<uint4*>(k_cache), reinterpret_cast<uint4*>(v_cache), cache_pos, n, H,
           Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po);
     else
-      attn_partial_kernel<false><<<grid, kAttnThreads, 0, stream>>>(
+      klaunch(attn_partial_kernel<false>, grid, kAttnThreads, 0, stream, 
           q, reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new),
           reinterpret_cast<uint4*>(k_cache), reinterpret_cast<uint4*>(v_cache), cache_pos, n, H,
           Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po);
@@ -469,7 +469,7 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
     if (e != hipSuccess) return e;
   }
   ProfScope prof("attn_combine", stream);
-  attn_combine_kernel<<<B * Hkv * R, kMaxHd, 0, stream>>>(n, H, Hkv, hd, R, L.nsplit, pm, pl, po,
+  klaunch(attn_combine_kernel, B * Hkv * R, kMaxHd, 0, stream, n, H, Hkv, hd, R, L.nsplit, pm, pl, po,
                                                           out);
   return hipGetLastError();
 }
@@ -477,7 +477,7 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
 hipError_t launch_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n,
                               hipStream_t stream) {
   ProfScope prof("kv_rollback", stream);
-  kv_rollback_kernel<<<ceil_div(B, 256), 256, 0, stream>>>(cache_pos, accept_len, B, n);
+  klaunch(kv_rollback_kernel, ceil_div(B, 256), 256, 0, stream, cache_pos, accept_len, B, n);
   return hipGetLastError();
 }
 

@@ -237,7 +237,7 @@ hipError_t launch_mode(int cpl, int G, hipStream_t s, const float* x, const uint
                        const unsigned long long* cut) {
 #define SIRIUS_DECODE1(CPLV)                                                                    \
   case CPLV:                                                                                    \
-    decode1_kernel<CPLV, MODE><<<G, kThreads, 0, s>>>(x, wg, wu, wd, d, F, t, norm_eps, rmax,    \
+    klaunch(decode1_kernel<CPLV, MODE>, G, kThreads, 0, s, x, wg, wu, wd, d, F, t, norm_eps, rmax,    \
                                                       uidx, ucnt, part, act, cut);              \
     break;
   switch (cpl) {

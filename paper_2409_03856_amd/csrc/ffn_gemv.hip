@@ -499,7 +499,7 @@ hipError_t launch_gate_bm(int cpl, dim3 grid, size_t lds, hipStream_t s, const f
                           int32_t* bcnt, float* absact, const unsigned long long* cut) {
 #define SIRIUS_GATE(CPLV)                                                                        \
   case CPLV:                                                                                     \
-    gate_kernel<BM, CPLV, MODE><<<grid, 256, lds, s>>>(x, B, wg, wu, d, F, t, norm_eps, rmax,    \
+    klaunch(gate_kernel<BM, CPLV, MODE>, grid, 256, lds, s, x, B, wg, wu, d, F, t, norm_eps, rmax,    \
                                                        uidx, hbuf, ucnt, bidx, bcnt, absact,     \
                                                        cut);                                     \
     break;
@@ -602,7 +602,7 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
   const int n = B * d;
   const int nred = ceil_div(n, 4 * kRedOut4);
   ProfScope prof(topk ? "topk_reduce" : (thr ? "cats_reduce" : "dense_reduce"), stream);
-  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
+  klaunch(reduce_kernel, nred + (lists ? B * kListBlocks : 0), 256, 0, stream, 
       part, L.gr, n, resid, y, nred, B, F, L.ntiles, L.rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();
 }
@@ -615,7 +615,7 @@ hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t*
   const uint4* wd4 = reinterpret_cast<const uint4*>(wd);
 #define SIRIUS_DOWN(BMV)                                                                     \
   case BMV:                                                                                  \
-    down_kernel<BMV><<<dgrid, 256, 0, stream>>>(wd4, d, B, uidx, hbuf, hstride, ucnt, nseg, \
+    klaunch(down_kernel<BMV>, dgrid, 256, 0, stream, wd4, d, B, uidx, hbuf, hstride, ucnt, nseg, \
                                                 rmax, gr, part);                             \
     break;
   switch (pow2_at_least(B, 16)) {
@@ -638,7 +638,7 @@ hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* r
   const int nred = ceil_div(n, 4 * kRedOut4);
   const bool lists = active_idx != nullptr;
   if (lists && nseg > kGateSegs) return hipErrorInvalidValue;
-  reduce_kernel<<<nred + (lists ? B * kListBlocks : 0), 256, 0, stream>>>(
+  klaunch(reduce_kernel, nred + (lists ? B * kListBlocks : 0), 256, 0, stream, 
       part, gr, n, resid, y, nred, B, F, nseg, rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();
 }

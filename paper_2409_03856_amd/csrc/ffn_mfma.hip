@@ -364,7 +364,7 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
   const int mt = L.mpad / kMTile;
   {
     ProfScope prof("ffn_mfma_prep", stream);
-    prep_x_kernel<<<L.mpad, 256, 0, stream>>>(x, B, d, norm_eps, xb);
+    klaunch(prep_x_kernel, L.mpad, 256, 0, stream, x, B, d, norm_eps, xb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   {
@@ -372,7 +372,7 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
     const dim3 grid(L.f16 / kGuRows);  // every row below F16 is written (0 past d_ff)
 #define SIRIUS_GU(MTV)                                                                       \
   case MTV:                                                                                  \
-    gate_up_kernel<MTV><<<grid, 128, 0, stream>>>(xb, wg, wu, d, F, L.f16, hhi, hlo);        \
+    klaunch(gate_up_kernel<MTV>, grid, 128, 0, stream, xb, wg, wu, d, F, L.f16, hhi, hlo);        \
     break;
     switch (mt) {
       SIRIUS_GU(1)
@@ -390,7 +390,7 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
     const dim3 grid(L.cs, L.gr);
 #define SIRIUS_DN(MTV)                                                                        \
   case MTV:                                                                                   \
-    down_kernel<MTV><<<grid, 256, 0, stream>>>(hhi, hlo, L.f16, wd, d, F, B, L.nchunk, part); \
+    klaunch(down_kernel<MTV>, grid, 256, 0, stream, hhi, hlo, L.f16, wd, d, F, B, L.nchunk, part); \
     break;
     switch (mt) {
       SIRIUS_DN(1)

@@ -135,8 +135,8 @@ hipError_t launch_rmsnorm(const float* h, int B, int d, float eps, float* out, h
   ProfScope prof("rmsnorm", stream);
   const bool vec = (d & 3) == 0 && d <= 8192 && (reinterpret_cast<uintptr_t>(h) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(out) & 15) == 0;
-  if (vec) rmsnorm_vec_kernel<<<B, 256, 0, stream>>>(h, d, eps, out);
-  else rmsnorm_kernel<<<B, 256, 0, stream>>>(h, d, eps, out);
+  if (vec) klaunch(rmsnorm_vec_kernel, B, 256, 0, stream, h, d, eps, out);
+  else klaunch(rmsnorm_kernel, B, 256, 0, stream, h, d, eps, out);
   return hipGetLastError();
 }
 
@@ -146,7 +146,7 @@ hipError_t launch_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float
   const size_t want = (nblk + 255) / 256;
   const int grid = (int)std::min<size_t>(want, 65536);
   ProfScope prof("fill_normal", stream);
-  fill_normal_bf16_kernel<<<grid, 256, 0, stream>>>(out, n, (uint32_t)seed, (uint32_t)(seed >> 32),
+  klaunch(fill_normal_bf16_kernel, grid, 256, 0, stream, out, n, (uint32_t)seed, (uint32_t)(seed >> 32),
                                                     mean, std);
   return hipGetLastError();
 }

@@ -395,36 +395,36 @@ hipError_t launch_griffin(const uint16_t* xp, int T, const uint16_t* wg, const u
   hipError_t e;
   {
     ProfScope prof("griffin_z", stream);
-    griffin_z_kernel<<<ntn * ntm, 256, 0, stream>>>(xp, T, wg, wu, d, F, Z, part);
+    klaunch(griffin_z_kernel, ntn * ntm, 256, 0, stream, xp, T, wg, wu, d, F, Z, part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   float* sc = scores_out != nullptr ? scores_out : scores;
   if (normalize) {  // the normalised variant needs every z of a token first
     {
       ProfScope prof("griffin_rownorm", stream);
-      griffin_rownorm_kernel<<<T, 256, 0, stream>>>(Z, F, rn2);
+      klaunch(griffin_rownorm_kernel, T, 256, 0, stream, Z, F, rn2);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     ProfScope prof("griffin_score", stream);
-    griffin_score_kernel<<<ceil_div(F, 256), 256, 0, stream>>>(Z, T, F, rn2, sc);
+    klaunch(griffin_score_kernel, ceil_div(F, 256), 256, 0, stream, Z, T, F, rn2, sc);
   } else {
     ProfScope prof("griffin_score", stream);
-    griffin_tile_score_kernel<<<ceil_div(F, 256), 256, 0, stream>>>(part, ntm, F, sc);
+    klaunch(griffin_tile_score_kernel, ceil_div(F, 256), 256, 0, stream, part, ntm, F, sc);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   {
     ProfScope prof("griffin_topk", stream);
     const int per = ceil_div(ceil_div(F, 16), kWave);  // slots per lane
     if (per <= 16)
-      griffin_topk_kernel<16><<<1, kTopkThreads, 0, stream>>>(sc, F, k, sel);
+      klaunch(griffin_topk_kernel<16>, 1, kTopkThreads, 0, stream, sc, F, k, sel);
     else if (per <= 32)
-      griffin_topk_kernel<32><<<1, kTopkThreads, 0, stream>>>(sc, F, k, sel);
+      klaunch(griffin_topk_kernel<32>, 1, kTopkThreads, 0, stream, sc, F, k, sel);
     else
-      griffin_topk_kernel<64><<<1, kTopkThreads, 0, stream>>>(sc, F, k, sel);
+      klaunch(griffin_topk_kernel<64>, 1, kTopkThreads, 0, stream, sc, F, k, sel);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   ProfScope prof("condense", stream);
-  condense_kernel<<<dim3(k, 3), 256, 0, stream>>>(
+  klaunch(condense_kernel, dim3(k, 3), 256, 0, stream, 
       reinterpret_cast<const uint4*>(wg), reinterpret_cast<const uint4*>(wu),
       reinterpret_cast<const uint4*>(wd), d / 8, F, sel, reinterpret_cast<uint4*>(wgc),
       reinterpret_cast<uint4*>(wuc), reinterpret_cast<uint4*>(wdc));

@@ -1,5 +1,5 @@
-// Per-kernel timing: when enabled, every library kernel launch is bracketed by a pair of
-// HIP events recorded on the stream the kernel is launched on.
+// Per-kernel timing: when enabled, the kernels of every ProfScope carry a pair of HIP events
+// on their own dispatches (see profile.h).
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -12,11 +12,15 @@
 #include "profile.h"
 
 namespace sirius {
+
+thread_local ProfScope* t_prof = nullptr;
+
 namespace {
 
 struct Rec {
   const char* name;
   hipEvent_t a, b;
+  bool used;  // false until a kernel carried the events
 };
 
 std::atomic<bool> g_on{false};
@@ -37,20 +41,31 @@ hipEvent_t take_event() {
 
 }  // namespace
 
-int prof_begin(const char* name, hipStream_t s) {
+int prof_open(const char* name) {
   if (!g_on.load(std::memory_order_relaxed)) return -1;
   std::lock_guard<std::mutex> lk(g_mu);
-  Rec r{name, take_event(), take_event()};
-  if (r.a == nullptr || r.b == nullptr) return -1;
-  if (hipEventRecord(r.a, s) != hipSuccess) return -1;
+  Rec r{name, take_event(), take_event(), false};
+  if (r.a == nullptr || r.b == nullptr) {
+    if (r.a != nullptr) g_free.push_back(r.a);
+    if (r.b != nullptr) g_free.push_back(r.b);
+    return -1;
+  }
   g_recs.push_back(r);
   return (int)g_recs.size() - 1;
 }
 
-void prof_end(int id, hipStream_t s) {
+bool prof_events(int id, hipEvent_t* start, hipEvent_t* stop) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (id < 0 || id >= (int)g_recs.size()) return false;
+  *start = g_recs[id].a;
+  *stop = g_recs[id].b;
+  return true;
+}
+
+void prof_close(int id, bool launched) {
   if (id < 0) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  if (id < (int)g_recs.size()) (void)hipEventRecord(g_recs[id].b, s);
+  if (id < (int)g_recs.size()) g_recs[id].used = launched;
 }
 
 }  // namespace sirius
@@ -65,7 +80,7 @@ int sirius_profile_enable(int on) {
 int sirius_profile_reset(void) {
   std::lock_guard<std::mutex> lk(sirius::g_mu);
   for (auto& r : sirius::g_recs) {
-    (void)hipEventSynchronize(r.b);
+    if (r.used) (void)hipEventSynchronize(r.b);
     sirius::g_free.push_back(r.a);
     sirius::g_free.push_back(r.b);
   }
@@ -79,7 +94,7 @@ int sirius_profile_query(const char* kernel, double* total_ms, int64_t* launches
   double tot = 0.0;
   int64_t n = 0;
   for (auto& r : sirius::g_recs) {
-    if (std::strcmp(r.name, kernel) != 0) continue;
+    if (!r.used || std::strcmp(r.name, kernel) != 0) continue;
     if (hipEventSynchronize(r.b) != hipSuccess) return SIRIUS_EHIP;
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return SIRIUS_EHIP;

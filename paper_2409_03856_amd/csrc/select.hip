@@ -81,16 +81,16 @@ hipError_t launch_select_kth_largest(const float* v, int n, int k, float* out_va
   int* ghist = reinterpret_cast<int*>(ws + 256);
   {
     ProfScope prof("select_init", stream);
-    select_init_kernel<<<1, 256, 0, stream>>>(st, k, ghist);
+    klaunch(select_init_kernel, 1, 256, 0, stream, st, k, ghist);
   }
   const int blocks = std::max(1, std::min(kHistBlocks, ceil_div(n, 256 * 8)));
   for (int shift = 24; shift >= 0; shift -= 8) {
     {
       ProfScope prof("select_hist", stream);
-      select_hist_kernel<<<blocks, 256, 0, stream>>>(v, n, shift, st, ghist);
+      klaunch(select_hist_kernel, blocks, 256, 0, stream, v, n, shift, st, ghist);
     }
     ProfScope prof("select_pick", stream);
-    select_pick_kernel<<<1, 256, 0, stream>>>(shift, st, ghist, out_value);
+    klaunch(select_pick_kernel, 1, 256, 0, stream, shift, st, ghist, out_value);
   }
   return hipGetLastError();
 }

@@ -173,7 +173,7 @@ hipError_t launch_cut(const float* act, int B, int F, int k, unsigned long long*
   const int per = ceil_div(F, kCutThreads);
 #define SIRIUS_CUT(P)                                                        \
   if (per <= P) {                                                            \
-    topk_cut_kernel<P><<<B, kCutThreads, 0, s>>>(act, F, k, cut);            \
+    klaunch(topk_cut_kernel<P>, B, kCutThreads, 0, s, act, F, k, cut);            \
     return hipGetLastError();                                                \
   }
   SIRIUS_CUT(1)

@@ -350,13 +350,13 @@ hipError_t launch_tree_build(const float* logits, int B, int Wc, int V, const fl
   const float c = (float)(1.4426950408889634 / (double)temperature);
   {
     ProfScope prof("tree_topw", stream);
-    tree_topw_kernel<<<dim3(splits, B * Wc), kTopThreads, 0, stream>>>(logits, V, seg, W, c, rm, rs,
+    klaunch(tree_topw_kernel, dim3(splits, B * Wc), kTopThreads, 0, stream, logits, V, seg, W, c, rm, rs,
                                                                      rk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   ProfScope prof("tree_select", stream);
-  tree_select_kernel<<<B, kSelThreads, 0, stream>>>(Wc, W, splits, c, (float)(1.0 / temperature),
+  klaunch(tree_select_kernel, B, kSelThreads, 0, stream, Wc, W, splits, c, (float)(1.0 / temperature),
                                                     rm, rs, rk, cum_ll, tokens, parents, cum_out);
   return hipGetLastError();
 }

@@ -352,7 +352,7 @@ hipError_t launch_stats(const float* logits, int B, int R, int V, const int32_t*
   P->pbi = reinterpret_cast<int*>(P->pbv + n);
   P->pd = reinterpret_cast<float*>(P->pbi + n);
   ProfScope prof(prof_name, stream);
-  verify_stats_kernel<<<dim3(splits, B * R), kVerifyThreads, 0, stream>>>(
+  klaunch(verify_stats_kernel, dim3(splits, B * R), kVerifyThreads, 0, stream, 
       logits, V, seg, c, drafted, Kd, R, P->pm, P->ps, P->pbv, P->pbi, P->pd);
   return hipGetLastError();
 }
@@ -371,7 +371,7 @@ hipError_t launch_verify(const float* logits, int B, int K, int R, int V, const 
   hipError_t e = launch_stats(logits, B, R, V, drafted, K, c, ws, L, stream, &P, "verify_stats");
   if (e != hipSuccess) return e;
   ProfScope prof("verify_scan", stream);
-  verify_scan_kernel<<<B, kScanThreads, 0, stream>>>(K, R, L.splits, r, c, P.pm, P.ps, P.pbv, P.pbi, P.pd,
+  klaunch(verify_scan_kernel, B, kScanThreads, 0, stream, K, R, L.splits, r, c, P.pm, P.ps, P.pbv, P.pbi, P.pd,
                                             accept_len, next_token, p_draft);
   return hipGetLastError();
 }
@@ -388,7 +388,7 @@ hipError_t launch_tree_verify(const float* logits, int B, int K, int W, int V, i
   hipError_t e = launch_stats(logits, B, R, V, tokens, K * W, c, ws, L, stream, &P, "tree_stats");
   if (e != hipSuccess) return e;
   ProfScope prof("tree_scan", stream);
-  tree_scan_kernel<<<B, kScanThreads, 0, stream>>>(K, W, bonus, parents, L.splits, r, c, P.pm, P.ps, P.pbv,
+  klaunch(tree_scan_kernel, B, kScanThreads, 0, stream, K, W, bonus, parents, L.splits, r, c, P.pm, P.ps, P.pbv,
                                           P.pbi, P.pd, best_leaf, accept_len, next_token, q);
   return hipGetLastError();
 }

@@ -131,3 +131,29 @@ def test_calibration_matches_oracle(sr):
         t_gpu = float(host(sr.sirius_cats_calibrate(dev_f32(xc), dev_bf16(wg), q))[0])
         t_ref = oracle.calibrate_threshold(xc, wg, q)
         assert abs(t_gpu - t_ref) <= 1e-5 * t_ref, (t_gpu, t_ref)
+
+
+def test_kernel_timing_changes_nothing(sr):
+    """With per-kernel timing on, the kernels carry the events on their own dispatches: the
+    results are bitwise those of a plain launch and each kernel name records one launch with
+    a positive duration."""
+    (wg, wu, wd), W = _layer(107, TINY.d_model, TINY.d_ff, TINY.weight_std)
+    t = oracle.calibrate_threshold(calibration_inputs(107, 64, TINY.d_model), wg, 0.5)
+    x = dev_f32(decode_inputs(107, 1, TINY.d_model))
+    y0, idx0, cnt0 = sr.sirius_ffn_cats(x, *W, t)
+    sr.sirius_profile_reset()
+    sr.sirius_profile_enable(True)
+    try:
+        y1, idx1, cnt1 = sr.sirius_ffn_cats(x, *W, t)
+    finally:
+        sr.sirius_profile_enable(False)
+    for name in ("cats_decode", "cats_reduce"):
+        ms, n = sr.sirius_profile_query(name)
+        say(f"{name}: {n} launch, {ms * 1e3:.2f} us")
+        assert n == 1 and 0.0 < ms < 100.0
+    assert sr.sirius_profile_query("no_such_kernel") == (0.0, 0)
+    sr.sirius_profile_reset()
+    assert np.array_equal(host(y0), host(y1))
+    assert np.array_equal(host(cnt0), host(cnt1))
+    n0 = int(host(cnt0)[0])
+    assert np.array_equal(host(idx0)[0, :n0], host(idx1)[0, :n0])
