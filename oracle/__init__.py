@@ -15,6 +15,10 @@ A plain, slow, float64 NumPy statement of what the GPU library computes:
   * kv       -- attention over the KV cache shared by the sparse and the full
                 model, with the full model's direct rewrite of the drafted chunk's
                 rows and the rollback after the check (Algorithm 1);
+  * loop     -- the generation loop of Algorithm 1 on a small random-weight
+                decoder: drafting by the sparse model, the full model's
+                check with the direct cache rewrite, rollback and
+                interleaving of the corrected token;
   * apu      -- the efficiency bookkeeping of Sec. 2.2 and Sec. 2.3
                 (APU, effective density, speculative-decoding AAL).
 
@@ -52,3 +56,4 @@ from .verify import softmax_row_stats, verify_accept  # noqa: F401
 from .tree import log_softmax, tree_build_step, tree_paths, tree_verify  # noqa: F401
 from .apu import sd_aal, apu, effective_density  # noqa: F401
 from .kv import attn_kv, kv_rollback  # noqa: F401
+from . import loop  # noqa: F401

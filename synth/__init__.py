@@ -16,6 +16,10 @@ from .inputs import (  # noqa: F401
     tree_build_inputs,
     tree_verify_inputs,
     attn_inputs,
+    model_weights,
+    prompt_tokens,
+    ModelShape,
+    TINY_MODEL,
     TINY,
     LLAMA3_8B,
     LLAMA3_70B,

@@ -191,3 +191,52 @@ def attn_inputs(seed: int, batch: int, n: int, heads: int, kv_heads: int, head_d
     kc = bf16_bits(rng.standard_normal((batch, lmax, kv_heads, head_dim), dtype=np.float32))
     vc = bf16_bits(rng.standard_normal((batch, lmax, kv_heads, head_dim), dtype=np.float32))
     return q, kn, vn, kc, vc
+
+
+@dataclasses.dataclass(frozen=True)
+class ModelShape:
+    """A small Llama-style decoder for the generation loop (random weights, mechanics only)."""
+    name: str
+    n_layers: int
+    d_model: int
+    d_ff: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    vocab: int
+    max_len: int
+    lm_std: float  # logit scale: W_lm ~ N(0, lm_std^2 / d_model)
+
+
+TINY_MODEL = ModelShape("tiny-decoder", 2, 256, 688, 4, 2, 64, 1000, 256, 6.0)
+
+_STREAM_MODEL = 8
+
+
+def model_weights(seed: int, s: ModelShape) -> dict:
+    """bf16 bit patterns of a random decoder: embed [V, d] ~ N(0, 1); wq [L, H hd, d],
+    wk, wv [L, Hkv hd, d], w_gate, w_up, w_down [L, F, d] ~ N(0, 1/d); wo [L, d, H hd]
+    ~ N(0, 1/(H hd)); lm_head [V, d] ~ N(0, lm_std^2/d)."""
+    rng = _rng(seed, _STREAM_MODEL)
+    d, hq, hkv = s.d_model, s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+
+    def draw(shape, std):
+        w = rng.standard_normal(shape, dtype=np.float32)
+        w *= np.float32(std)
+        return bf16_bits(w)
+
+    out = {"embed": draw((s.vocab, d), 1.0)}
+    out["wq"] = draw((s.n_layers, hq, d), d ** -0.5)
+    out["wk"] = draw((s.n_layers, hkv, d), d ** -0.5)
+    out["wv"] = draw((s.n_layers, hkv, d), d ** -0.5)
+    out["wo"] = draw((s.n_layers, d, hq), hq ** -0.5)
+    for k in ("w_gate", "w_up", "w_down"):
+        out[k] = draw((s.n_layers, s.d_ff, d), d ** -0.5)
+    out["lm_head"] = draw((s.vocab, d), s.lm_std * d ** -0.5)
+    return out
+
+
+def prompt_tokens(seed: int, t: int, vocab: int) -> np.ndarray:
+    """t prompt token ids uniform in [0, vocab), int32."""
+    rng = _rng(seed, _STREAM_PROMPT)
+    return rng.integers(0, vocab, size=t, dtype=np.int64).astype(np.int32)
