@@ -289,6 +289,108 @@ int sirius_attn_kv(const float* q, const uint16_t* k_new, const uint16_t* v_new,
 int sirius_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n, void* stream);
 
 /*
+ * A small Llama-style decoder whose sparse model M_S and full model M_F share
+ * the weights and one KV cache (Algorithm 1). Every pointer but thresholds is
+ * a device pointer, 16-byte aligned; weights are bf16 bit patterns:
+ *   embed    [vocab, d_model]
+ *   wq       [n_layers, n_heads * head_dim, d_model]
+ *   wk, wv   [n_layers, n_kv_heads * head_dim, d_model]
+ *   wo       [n_layers, d_model, n_heads * head_dim]
+ *   w_gate, w_up, w_down [n_layers, d_ff, d_model] (neuron-major)
+ *   lm_head  [vocab, d_model]
+ *   k_cache, v_cache [n_layers, max_len, n_kv_heads, head_dim], the shared
+ *            cache, updated in place
+ *   thresholds HOST [n_layers]: M_S keeps FFN neuron i of layer l iff
+ *            |SiLU(gate_i)| > thresholds[l] (a negative value keeps all).
+ * Per layer: h += W_o attn(RMSNorm(h)) (grouped-query attention over the
+ * cache, as sirius_attn_kv, no positional rotation) and h += FFN(RMSNorm(h))
+ * (M_F: the dense FFN of sirius_ffn_dense, M_S: the threshold-sparse FFN of
+ * sirius_ffn_cats); logits = W_lm RMSNorm(h). RMSNorm has unit weight and
+ * epsilon norm_eps. Keys and values enter the cache as bf16 (round to
+ * nearest even); every product accumulates in fp32. Limits: d_model and
+ * n_heads * head_dim multiples of 8 up to 8192, head_dim a multiple of 8 up
+ * to 128, n_heads a multiple of n_kv_heads, d_ff <= 65536, vocab <= 2^24,
+ * max_len <= 2^20.
+ */
+typedef struct sirius_model {
+  int n_layers, d_model, d_ff, n_heads, n_kv_heads, head_dim, vocab, max_len;
+  float norm_eps;
+  const uint16_t* embed;
+  const uint16_t* wq;
+  const uint16_t* wk;
+  const uint16_t* wv;
+  const uint16_t* wo;
+  const uint16_t* w_gate;
+  const uint16_t* w_up;
+  const uint16_t* w_down;
+  const uint16_t* lm_head;
+  const float* thresholds;
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+} sirius_model;
+
+/* Workspace bytes of sirius_model_forward with up to max_tokens tokens and of
+ * sirius_generate with kernel size n = max_tokens (1 <= max_tokens <= 64);
+ * 0 for an invalid model. */
+size_t sirius_model_workspace_size(const sirius_model* model, int max_tokens);
+
+/*
+ * One pass of M_S (sparse != 0) or M_F over n tokens (device [n] int32; an id
+ * outside [0, vocab) embeds as zeros) at positions p .. p + n - 1, p =
+ * cache_pos[0] on the device (read only): the tokens' keys and values replace
+ * those cache rows in every layer and token i attends to rows 0 .. p + i.
+ *   logits      [n, vocab] fp32.
+ *   active_idx  [n_layers, n, d_ff] int32 and active_cnt [n_layers, n], or
+ *               both NULL (sparse only): the kept neurons of every token and
+ *               layer, ascending.
+ * The full model's FFN at n >= 8 runs on MFMA with its normalised input
+ * rounded to bf16 (as sirius_ffn_dense). With p + n > max_len the attention
+ * leaves the cache untouched and the logits are NaN.
+ * Errors: SIRIUS_EINVAL for an invalid model, n outside [1, min(64, max_len)],
+ * null pointers, a NaN threshold (sparse); SIRIUS_EWORKSPACE.
+ */
+int sirius_model_forward(const sirius_model* model, const int32_t* tokens, int n,
+                         const int32_t* cache_pos, int sparse, float* logits, int32_t* active_idx,
+                         int32_t* active_cnt, void* ws, size_t ws_bytes, void* stream);
+
+/* Optional per-period records of sirius_generate (device pointers, each may be
+ * NULL; active_idx and active_cnt go together). */
+typedef struct sirius_gen_trace {
+  int32_t* drafted;     /* [periods, n]: M_S's drafts */
+  int32_t* accept_len;  /* [periods]: the first rejected draft, n if none */
+  int32_t* next_token;  /* [periods]: the corrected token, -1 if none */
+  float* q;             /* [periods, n]: M_F's likelihood of each draft */
+  int32_t* active_idx;  /* [periods, n, n_layers, d_ff]: M_S's kept neurons per draft step */
+  int32_t* active_cnt;  /* [periods, n, n_layers] */
+} sirius_gen_trace;
+
+/*
+ * `periods` periods of the Sirius loop (Algorithm 1) with kernel size n,
+ * greedy drafting and greedy correction, all on the device:
+ *   drafting  M_S runs seq[i] at position P + i and drafts seq[i + 1] =
+ *             argmax of its logits (lowest index on ties), for i < n; P =
+ *             cache_pos[0] at the period's start;
+ *   check     the position winds back to P and M_F runs seq[0 .. n - 1] in
+ *             one pass, rewriting cache rows P .. P + n - 1; row i's softmax
+ *             gives the likelihood q_i of seq[i + 1]; j = the first i with
+ *             q_i < r, else n (sirius_verify_accept);
+ *   rollback  cache_pos[0] = P + min(j + 1, n) (sirius_kv_rollback);
+ *   interleave seq[1 .. j] and, when j < n, the corrected token argmax of
+ *             row j are appended to out_tokens at out_count[0] (which is
+ *             advanced); seq[0] becomes the corrected token, or seq[n].
+ * seq [n + 1] int32 on the device: seq[0] holds the first input (the last
+ * committed token, not yet in the cache) on entry and the next one on
+ * return. cache_pos [1], out_count [1] int32 on the device; out_tokens has
+ * room for periods * n tokens (never written past that). The caller keeps
+ * cache_pos[0] + periods * n <= max_len. Nothing synchronises with the host:
+ * the committed count is read from out_count afterwards.
+ * Errors: as sirius_model_forward, plus n outside [1, 64], periods < 0, r NaN.
+ */
+int sirius_generate(const sirius_model* model, int32_t* seq, int32_t* cache_pos, int n, float r,
+                    int periods, int32_t* out_tokens, int32_t* out_count,
+                    const sirius_gen_trace* trace, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * RMSNorm with unit weight, the layer-stack glue around the FFN:
  *   out[b] = h[b] / sqrt(mean(h[b]^2) + eps). out may alias h.
  * Errors: SIRIUS_EINVAL for null pointers, d_model < 1, eps < 0.

@@ -105,14 +105,15 @@ def new_cache(m: Model, max_len: int):
 
 
 def forward(m: Model, tokens, cache, pos: int, sparse: bool, *, active_sets=None,
-            full_ffn_input_bf16: bool = False):
+            full_ffn_input_bf16: bool = False, acts=None):
     """One pass of M_S (sparse=True) or M_F over tokens at positions pos .. pos + n - 1.
 
     The tokens' keys and values replace the cache rows at those positions (the cache list is
     updated in place) and token i attends to rows 0 .. pos + i. active_sets, when given,
     is [layer][token] -> the neuron set M_S uses instead of its threshold rule (so a caller
     can replay another implementation's sets). Returns (logits [n, V], sets) where sets is
-    [layer][token] -> the ascending neuron set used (M_S) or None (M_F).
+    [layer][token] -> the ascending neuron set used (M_S) or None (M_F). When acts is a list,
+    each layer's gate activations SiLU(g) [n, d_ff] are appended to it.
     """
     toks = np.asarray(tokens, dtype=np.int64)
     n = toks.shape[0]
@@ -135,6 +136,8 @@ def forward(m: Model, tokens, cache, pos: int, sparse: bool, *, active_sets=None
         g = xf @ m.w_gate[layer].T
         u = xf @ m.w_up[layer].T
         a = silu(g)
+        if acts is not None:
+            acts.append(a)
         hid = a * u
         if sparse:
             if active_sets is not None:
@@ -187,8 +190,8 @@ def _softmax_prob(row, tok: int) -> float:
 @dataclasses.dataclass
 class Period:
     """One period's record: inputs s_0 .. s_n, accept length j, corrected token (or -1),
-    the committed tokens, the positions before and after, and the drafting neuron sets
-    ([step][layer] -> set)."""
+    the committed tokens, the positions before and after, the full model's likelihoods q, the
+    drafting neuron sets ([step][layer] -> set) and gate activations ([step][layer] -> row)."""
     seq: list
     accept: int
     corrected: int
@@ -197,6 +200,7 @@ class Period:
     pos_after: int
     q: list
     draft_sets: list
+    draft_acts: list
 
 
 def sirius_period(m: Model, cache, pos: int, cur: int, n: int, r: float, *,
@@ -209,11 +213,13 @@ def sirius_period(m: Model, cache, pos: int, cur: int, n: int, r: float, *,
     plain oracle passes None and takes every decision itself.
     """
     seq = [int(cur)]
-    draft_sets = []
+    draft_sets, draft_acts = [], []
     for i in range(n):  # M_S drafts, writing rows pos + i
         sets = follow("sets", i, None, None) if follow else None
-        logits, used = forward(m, [seq[i]], cache, pos + i, True, active_sets=sets)
+        acts = []
+        logits, used = forward(m, [seq[i]], cache, pos + i, True, active_sets=sets, acts=acts)
         draft_sets.append([u[0] for u in used])
+        draft_acts.append([a[0] for a in acts])
         own = int(np.argmax(logits[0]))
         seq.append(follow("draft", i, own, logits[0]) if follow else own)
     # cache position wound back by n; M_F rewrites rows pos .. pos + n - 1 in one pass
@@ -235,7 +241,7 @@ def sirius_period(m: Model, cache, pos: int, cur: int, n: int, r: float, *,
         corrected = -1
         committed = seq[1:n + 1]
         pos_after = pos + n
-    return Period(seq, j, corrected, committed, pos, pos_after, q, draft_sets)
+    return Period(seq, j, corrected, committed, pos, pos_after, q, draft_sets, draft_acts)
 
 
 def prefill(m: Model, cache, prompt):

@@ -22,6 +22,10 @@ from ._lib import (  # noqa: F401
     sirius_attn_kv,
     sirius_kv_rollback,
     sirius_rmsnorm,
+    Model,
+    sirius_model_workspace_size,
+    sirius_model_forward,
+    sirius_generate,
     sirius_fill_normal_bf16,
     sirius_workspace_size,
     sirius_profile_enable,

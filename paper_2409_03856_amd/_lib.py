@@ -50,6 +50,9 @@ SIGNATURES = {
     "sirius_tree_verify": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_attn_kv": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _Z, _P]),
     "sirius_kv_rollback": (_I, [_P, _P, _I, _I, _P]),
+    "sirius_model_workspace_size": (_Z, [_P, _I]),
+    "sirius_model_forward": (_I, [_P, _P, _I, _P, _I, _P, _P, _P, _P, _Z, _P]),
+    "sirius_generate": (_I, [_P, _P, _P, _I, _F, _I, _P, _P, _P, _P, _Z, _P]),
     "sirius_rmsnorm": (_I, [_P, _I, _I, _F, _P, _P]),
     "sirius_fill_normal_bf16": (_I, [_P, _Z, ctypes.c_uint64, _F, _F, _P]),
     "sirius_profile_enable": (_I, [_I]),
@@ -433,3 +436,126 @@ def sirius_workspace_size(op, a, b, c, d=0, e=0):
 
 def sirius_version() -> str:
     return lib().sirius_version().decode()
+
+
+# ---------------------------------------------------------------- small decoder and the loop
+
+class _ModelC(ctypes.Structure):
+    """struct sirius_model of include/sirius.h."""
+    _fields_ = [(n, ctypes.c_int) for n in ("n_layers", "d_model", "d_ff", "n_heads", "n_kv_heads",
+                                            "head_dim", "vocab", "max_len")] + \
+               [("norm_eps", ctypes.c_float)] + \
+               [(n, ctypes.c_void_p) for n in ("embed", "wq", "wk", "wv", "wo", "w_gate", "w_up",
+                                               "w_down", "lm_head", "thresholds", "k_cache",
+                                               "v_cache")]
+
+
+class _TraceC(ctypes.Structure):
+    """struct sirius_gen_trace of include/sirius.h."""
+    _fields_ = [(n, ctypes.c_void_p) for n in ("drafted", "accept_len", "next_token", "q",
+                                               "active_idx", "active_cnt")]
+
+
+class Model:
+    """A sirius_model over caller-owned device tensors (kept alive here). weights maps
+    embed, wq, wk, wv, wo, w_gate, w_up, w_down, lm_head to bf16 device tensors of the
+    shapes in include/sirius.h; the shared cache is allocated here (zeros)."""
+
+    def __init__(self, weights: dict, n_heads: int, n_kv_heads: int, head_dim: int, max_len: int,
+                 thresholds, norm_eps: float = 1e-5):
+        torch = _torch()
+        for k in ("embed", "wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head"):
+            _need(k in weights, f"missing weight {k}")
+            _bits16(weights[k])
+            _dev_check(weights[k])
+        self.weights = dict(weights)
+        L, F, d = (int(x) for x in weights["w_gate"].shape)
+        V = int(weights["embed"].shape[0])
+        dev = weights["embed"].device
+        shape = (L, max_len, n_kv_heads, head_dim)
+        self.k_cache = torch.zeros(shape, dtype=torch.bfloat16, device=dev)
+        self.v_cache = torch.zeros(shape, dtype=torch.bfloat16, device=dev)
+        self.thresholds = (ctypes.c_float * L)(*[float(t) for t in thresholds])
+        w = self.weights
+        self.c = _ModelC(L, d, F, n_heads, n_kv_heads, head_dim, V, max_len, float(norm_eps),
+                         *[w[k].data_ptr() for k in ("embed", "wq", "wk", "wv", "wo", "w_gate",
+                                                     "w_up", "w_down", "lm_head")],
+                         ctypes.cast(self.thresholds, ctypes.c_void_p).value,
+                         self.k_cache.data_ptr(), self.v_cache.data_ptr())
+        self.device = dev
+
+    @property
+    def ptr(self):
+        return ctypes.byref(self.c)
+
+
+def sirius_model_workspace_size(model: Model, max_tokens: int) -> int:
+    return int(lib().sirius_model_workspace_size(model.ptr, int(max_tokens)))
+
+
+def _model_ws(model: Model, n: int):
+    torch = _torch()
+    size = sirius_model_workspace_size(model, n)
+    _need(size > 0, "invalid model or token count for the workspace query")
+    return torch.empty(size, dtype=torch.uint8, device=model.device)
+
+
+def sirius_model_forward(model: Model, tokens, cache_pos, sparse: bool, *, logits=None, want_active=False,
+                         ws=None, stream=None):
+    """tokens [n] int32, cache_pos [1] int32 (device). Returns (logits [n, V] fp32, active_idx
+    [L, n, d_ff], active_cnt [L, n]) -- the lists None unless want_active (sparse only)."""
+    torch = _torch()
+    _need(tokens.dtype == torch.int32 and tokens.dim() == 1, "tokens must be int32 [n]")
+    _need(cache_pos.dtype == torch.int32 and tuple(cache_pos.shape) == (1,), "cache_pos must be int32 [1]")
+    n = int(tokens.shape[0])
+    c = model.c
+    if logits is None:
+        logits = torch.empty((n, c.vocab), dtype=torch.float32, device=model.device)
+    aidx = acnt = None
+    if want_active:
+        aidx = torch.empty((c.n_layers, n, c.d_ff), dtype=torch.int32, device=model.device)
+        acnt = torch.empty((c.n_layers, n), dtype=torch.int32, device=model.device)
+    _dev_check(tokens, cache_pos, logits, aidx, acnt)
+    if ws is None:
+        ws = _model_ws(model, n)
+    _check(lib().sirius_model_forward(model.ptr, _ptr(tokens), n, _ptr(cache_pos), 1 if sparse else 0,
+                                      _ptr(logits), _ptr(aidx), _ptr(acnt), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return logits, aidx, acnt
+
+
+def sirius_generate(model: Model, seq, cache_pos, n: int, r: float, periods: int, *, out_tokens=None,
+                    out_count=None, trace=False, trace_active=False, ws=None, stream=None):
+    """seq [n + 1] int32 (seq[0] = the first input), cache_pos [1] int32, both on the device and
+    updated. Returns (out_tokens [periods * n], out_count [1], trace dict or None); out_count is
+    zeroed here unless passed in."""
+    torch = _torch()
+    _need(seq.dtype == torch.int32 and tuple(seq.shape) == (n + 1,), "seq must be int32 [n + 1]")
+    _need(cache_pos.dtype == torch.int32 and tuple(cache_pos.shape) == (1,), "cache_pos must be int32 [1]")
+    dev = model.device
+    c = model.c
+    if out_tokens is None:
+        out_tokens = torch.full((max(periods * n, 1),), -1, dtype=torch.int32, device=dev)
+    if out_count is None:
+        out_count = torch.zeros((1,), dtype=torch.int32, device=dev)
+    tr = None
+    tc = None
+    if trace or trace_active:
+        tr = {"drafted": torch.full((periods, n), -1, dtype=torch.int32, device=dev),
+              "accept_len": torch.full((periods,), -1, dtype=torch.int32, device=dev),
+              "next_token": torch.full((periods,), -2, dtype=torch.int32, device=dev),
+              "q": torch.zeros((periods, n), dtype=torch.float32, device=dev),
+              "active_idx": None, "active_cnt": None}
+        if trace_active:
+            tr["active_idx"] = torch.empty((periods, n, c.n_layers, c.d_ff), dtype=torch.int32, device=dev)
+            tr["active_cnt"] = torch.empty((periods, n, c.n_layers), dtype=torch.int32, device=dev)
+        tc = _TraceC(*[None if tr[k] is None else tr[k].data_ptr()
+                       for k in ("drafted", "accept_len", "next_token", "q", "active_idx", "active_cnt")])
+    _dev_check(seq, cache_pos, out_tokens, out_count)
+    if ws is None:
+        ws = _model_ws(model, n)
+    _check(lib().sirius_generate(model.ptr, _ptr(seq), _ptr(cache_pos), int(n), float(r), int(periods),
+                                 _ptr(out_tokens), _ptr(out_count),
+                                 None if tc is None else ctypes.byref(tc), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return out_tokens, out_count, tr

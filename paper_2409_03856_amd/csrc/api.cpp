@@ -123,6 +123,10 @@ int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, co
 
 }  // namespace
 
+namespace sirius {
+void set_last_error(const char* msg) { g_last_error = msg; }
+}  // namespace sirius
+
 extern "C" {
 
 const char* sirius_last_error(void) { return g_last_error.c_str(); }

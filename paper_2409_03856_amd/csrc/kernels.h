@@ -9,6 +9,9 @@
 
 namespace sirius {
 
+// The calling thread's message for sirius_last_error (the C-ABI files set it on failure).
+void set_last_error(const char* msg);
+
 // FFN selection modes of the small-batch and batch-1 launchers
 constexpr int kFfnModeDense = 0;      // every neuron (dense and condensed)
 constexpr int kFfnModeThreshold = 1;  // |SiLU(gate)| > t per token
@@ -154,6 +157,27 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
                           const AttnLayout& L, hipStream_t stream);
 hipError_t launch_kv_rollback(int32_t* cache_pos, const int32_t* accept_len, int B, int n,
                               hipStream_t stream);
+
+// ---- small decoder and the generation loop (model.hip)
+// h[i] = E[tokens[i]] widened to fp32 (0 for an id outside [0, V)); d % 8 == 0.
+hipError_t launch_embed(const int32_t* tokens, int n, const uint16_t* E, int d, int V, float* out,
+                        hipStream_t s);
+// y[i][j] = x[i] . W[j] (+ resid[i][j]) for i < n, j < N; W [N][K] bf16; K % 8 == 0 and
+// K <= 16384. With y_bf16 the rows are written as bf16 instead (resid and y unused).
+hipError_t launch_linear(const float* x, int n, const uint16_t* W, int K, int N,
+                         const float* resid, float* y, uint16_t* y_bf16, hipStream_t s);
+// seq[slot] = argmax of the V logits (lowest index on ties); cache_pos[0] += pos_delta;
+// trace_drafted[slot - 1] = the token when given.
+hipError_t launch_draft_tail(const float* logits, int V, int32_t* seq, int slot,
+                             int32_t* cache_pos, int pos_delta, int32_t* trace_drafted,
+                             hipStream_t s);
+// After the check of an n-token chunk seq[0 .. n - 1] (drafts seq[1 .. n]): cache_pos +=
+// min(j + 1, n); out[count ..] += seq[1 .. j] and the corrected token when j < n (at most
+// out_cap entries in all); seq[0] = the next period's first input.
+hipError_t launch_period_tail(int32_t* seq, int n, const int32_t* accept_len,
+                              const int32_t* next_token, int32_t* cache_pos, int32_t* out,
+                              int32_t* out_count, int out_cap, int32_t* tr_accept,
+                              int32_t* tr_next, hipStream_t s);
 
 // ---- glue
 hipError_t launch_rmsnorm(const float* h, int B, int d, float eps, float* out, hipStream_t stream);

@@ -272,3 +272,52 @@ def test_workspace_sizes(L):
     assert f(7, 1, 16, 64, 128256, 0) > 0
     assert f(7, 1, 16, 64, 128256, 1) == 0
     assert f(7, 1, 4, 65, 128256, 0) == 0
+
+
+def _fake_model(**kw):
+    from paper_2409_03856_amd._lib import _ModelC
+    thr = (ctypes.c_float * 2)(0.1, 0.1)
+    vals = dict(n_layers=2, d_model=256, d_ff=688, n_heads=4, n_kv_heads=2, head_dim=64, vocab=1000,
+                max_len=256, norm_eps=1e-5)
+    ptrs = {k: FAKE.value for k in ("embed", "wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head",
+                                    "k_cache", "v_cache")}
+    ptrs["thresholds"] = ctypes.cast(thr, ctypes.c_void_p).value
+    vals.update(ptrs)
+    vals.update(kw)
+    m = _ModelC(**vals)
+    m._keep = thr
+    return m
+
+
+def test_model_argument_errors(L):
+    big = 1 << 30
+    m = _fake_model()
+    assert L.sirius_model_workspace_size(ctypes.byref(m), 16) > 0
+    assert L.sirius_model_workspace_size(ctypes.byref(m), 0) == 0
+    assert L.sirius_model_workspace_size(ctypes.byref(m), 65) == 0
+    assert L.sirius_model_workspace_size(None, 16) == 0
+    # model, tokens, n, cache_pos, sparse, logits, active_idx, active_cnt, ws, ws_bytes, stream
+    fwd = lambda mm, n=4, ws=big, **kw: L.sirius_model_forward(
+        ctypes.byref(mm), FAKE, n, FAKE, kw.get("sparse", 1), FAKE, kw.get("ai"), kw.get("ac"), FAKE, ws, None)
+    assert fwd(_fake_model(d_model=100)) == -1 and "d_model" in _err(L)
+    assert fwd(_fake_model(n_heads=3)) == -1 and "n_kv_heads" in _err(L)
+    assert fwd(_fake_model(head_dim=256)) == -1 and "head_dim" in _err(L)
+    assert fwd(_fake_model(wq=None)) == -1 and "wq" in _err(L)
+    assert fwd(_fake_model(k_cache=(1 << 20) + 4)) == -1 and "aligned" in _err(L)
+    assert fwd(_fake_model(thresholds=None)) == -1 and "thresholds" in _err(L)
+    assert fwd(_fake_model(thresholds=None), sparse=0, ws=16) == -2  # the full model needs none
+    assert fwd(m, n=0) == -1 and fwd(m, n=65) == -1
+    assert fwd(m, ai=FAKE) == -1 and "both" in _err(L)
+    assert fwd(m, sparse=0, ai=FAKE, ac=FAKE) == -1 and "sparse" in _err(L)
+    assert fwd(m, ws=16) == -2 and "workspace" in _err(L)
+    nan = (ctypes.c_float * 2)(float("nan"), 0.1)
+    assert fwd(_fake_model(thresholds=ctypes.cast(nan, ctypes.c_void_p).value)) == -1 and "NaN" in _err(L)
+    # model, seq, cache_pos, n, r, periods, out_tokens, out_count, trace, ws, ws_bytes, stream
+    gen = lambda n=16, r=0.1, periods=4, ws=big, seq=FAKE: L.sirius_generate(
+        ctypes.byref(m), seq, FAKE, n, r, periods, FAKE, FAKE, None, FAKE, ws, None)
+    assert gen(n=0) == -1 and gen(n=65) == -1
+    assert gen(periods=-1) == -1
+    assert gen(r=float("nan")) == -1 and "r is NaN" in _err(L)
+    assert gen(seq=None) == -1
+    assert gen(ws=16) == -2
+    assert gen(periods=0) == 0  # nothing to do

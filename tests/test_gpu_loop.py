@@ -1,0 +1,263 @@
+"""GPU parity: the small decoder's forward passes and the Sirius loop (Algorithm 1) against the
+loop oracle.
+
+Tolerances (derived in the design notes):
+  * logits of a forward pass whose FFN inputs are fp32 (fewer than 8 tokens): max-abs error
+    <= 1e-4 x RMS of the oracle's logits (fp32 accumulation; measured about 1e-6);
+  * logits of a full-model pass of 8 or more tokens, whose FFN runs on MFMA with its
+    normalised input rounded to bf16 (the oracle rounds too): <= 5e-3 x RMS. The GPU's fp32
+    input differs from the oracle's fp64 one by about 1e-6 relative, so about 5e-4 of the
+    rounded elements sit close enough to a rounding boundary to round the other way (one bf16
+    step, 0.4 %); each such flip moves the logits by up to a few 1e-4 x RMS through the
+    following layers and the LM head (measured 1.2e-3 at 8 tokens and 2.2e-3 at 24; without
+    the rounding the oracle is 9.5e-3 away);
+  * cache rows: within one bf16 step of the oracle's plus 1e-5 x RMS (keys and values are
+    rounded to bf16 from values that agree to about 1e-6), plus 5e-3 x RMS after MFMA passes;
+  * the sparse model's neuron sets: bit-exact outside |(|a| - t)| <= 1e-3 (the FFN guard band);
+    the oracle then computes with the GPU's set;
+  * loop decisions (drafts, accept lengths, corrected tokens) bit-exact, except where the
+    oracle's own decision has a margin under the guard: a top-2 logit gap under G_m x RMS of
+    the row, or |q - r| under G_q r, with (G_m, G_q) = (1e-3, 1e-3) when every pass has fp32
+    FFN inputs and (1e-2, 5e-2) when the check pass runs on MFMA (a logit error e moves q by
+    about 2e relative). There the oracle takes the GPU's decision and the case is counted and
+    reported;
+  * likelihoods q: within G_q relative (+1e-6).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import loop
+from synth import model_weights, prompt_tokens, TINY_MODEL
+from gpu_util import say, dev_bf16, dev_i32, host, CATS_BAND
+
+pytestmark = pytest.mark.gpu
+
+LOGIT_TOL_FP32 = 1e-4
+LOGIT_TOL_MFMA = 5e-3
+GUARDS_FP32 = (1e-3, 1e-3)
+GUARDS_MFMA = (1e-2, 5e-2)
+MFMA_MIN = 8
+S = TINY_MODEL
+
+
+@pytest.fixture(scope="module")
+def sr():
+    import paper_2409_03856_amd as sr
+    sr.lib()
+    return sr
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    bits = model_weights(21, S)
+    m = loop.model_from_bits(bits, S.n_heads, S.n_kv_heads, S.head_dim, np.zeros(S.n_layers))
+    m.thresholds = loop.calibrate_thresholds(m, prompt_tokens(121, 64, S.vocab), 0.5, S.max_len)
+    return bits, m
+
+
+def _gpu_model(sr, bits, thresholds):
+    w = {k: dev_bf16(v) for k, v in bits.items()}
+    return sr.Model(w, S.n_heads, S.n_kv_heads, S.head_dim, S.max_len, thresholds)
+
+
+def _rel(got, want):
+    want = np.asarray(want, dtype=np.float64)
+    rms = float(np.sqrt(np.mean(want * want)))
+    return float(np.max(np.abs(np.asarray(got, np.float64) - want))) / rms
+
+
+def _cache_close(gm, cache, upto, abs_tol):
+    """GPU cache rows 0 .. upto - 1 within one bf16 step of the oracle's, plus abs_tol x RMS
+    for the values' own difference before rounding (1e-5 when every pass had fp32 FFN
+    inputs; the logit tolerance of an MFMA pass otherwise)."""
+    for layer in range(S.n_layers):
+        for g, o in ((gm.k_cache, cache[layer][0]), (gm.v_cache, cache[layer][1])):
+            got = host(g[layer].float())[:upto]
+            want = o[0, :upto]
+            rms = float(np.sqrt(np.mean(want * want)))
+            step = np.abs(want) * 2.0 ** -7 + abs_tol * rms
+            assert np.all(np.abs(got - want) <= step), f"cache layer {layer}"
+
+
+def _check_sets(gpu_sets, acts_row, t):
+    """GPU kept set == the threshold rule outside the guard band; returns the boundary count."""
+    a = np.abs(acts_row)
+    rule = a > t
+    got = np.zeros_like(rule)
+    got[np.asarray(gpu_sets, dtype=np.int64)] = True
+    band = np.abs(a - t) <= CATS_BAND
+    assert np.array_equal(got[~band], rule[~band])
+    return int(band.sum())
+
+
+def test_forward_passes_match_oracle(sr, tiny):
+    import torch
+    bits, m = tiny
+    gm = _gpu_model(sr, bits, m.thresholds)
+    pos = torch.zeros(1, dtype=torch.int32, device="cuda")
+    # fp32 FFN inputs throughout: full model over 7 prompt tokens, then 4 at 7, then the
+    # sparse model over 1 token at 11 and 3 tokens at 12 (per-token sets)
+    cache = loop.new_cache(m, S.max_len)
+    for n, p, sparse in ((7, 0, False), (4, 7, False), (1, 11, True), (3, 12, True)):
+        say(f"forward: {'sparse' if sparse else 'full'} model, {n} tokens at {p}")
+        pos.fill_(p)
+        toks = prompt_tokens(5 + p, n, S.vocab)
+        lg, aidx, acnt = sr.sirius_model_forward(gm, dev_i32(toks), pos, sparse, want_active=sparse)
+        if sparse:
+            aidx, acnt = host(aidx), host(acnt)
+            gpu_sets = [[aidx[l, i, :acnt[l, i]] for i in range(n)] for l in range(S.n_layers)]
+            acts = []
+            want, _ = loop.forward(m, toks, cache, p, True, active_sets=gpu_sets, acts=acts)
+            nb = sum(_check_sets(gpu_sets[l][i], acts[l][i], m.thresholds[l])
+                     for l in range(S.n_layers) for i in range(n))
+        else:
+            want, _ = loop.forward(m, toks, cache, p, False)
+            nb = 0
+        err = _rel(host(lg), want)
+        say(f"  logits error {err:.2e} x RMS, {nb} boundary neurons")
+        assert err <= LOGIT_TOL_FP32
+    _cache_close(gm, cache, 15, 1e-5)
+    assert int(host(pos)[0]) == 12  # the cache position is only read
+    # the full model over 24 tokens at 0: MFMA FFN on bf16-rounded inputs
+    say("forward: full model, 24 tokens at 0 (MFMA FFN)")
+    pos.fill_(0)
+    prompt = prompt_tokens(5, 24, S.vocab)
+    lg, _, _ = sr.sirius_model_forward(gm, dev_i32(prompt), pos, False)
+    cache = loop.new_cache(m, S.max_len)
+    want, _ = loop.forward(m, prompt, cache, 0, False, full_ffn_input_bf16=True)
+    err = _rel(host(lg), want)
+    say(f"  logits error {err:.2e} x RMS")
+    assert err <= LOGIT_TOL_MFMA
+    _cache_close(gm, cache, 24, LOGIT_TOL_MFMA)
+
+
+class _Replay:
+    """The oracle's follow hook: take the GPU's decision only where the oracle's own has a
+    margin under the guard; count those cases."""
+
+    def __init__(self, tr, p, r, guards):
+        self.tr, self.p, self.r = tr, p, r
+        self.gm, self.gq = guards
+        self.ambiguous = 0
+
+    def __call__(self, kind, i, own, info):
+        tr, p = self.tr, self.p
+        if kind == "sets":
+            cnt = tr["active_cnt"][p, i]
+            return [[tr["active_idx"][p, i, l, :cnt[l]]] for l in range(len(cnt))]
+        if kind in ("draft", "corrected"):
+            gpu = int(tr["drafted"][p, i]) if kind == "draft" else int(tr["next_token"][p])
+            if gpu == own:
+                return own
+            row = np.asarray(info, dtype=np.float64)
+            top2 = np.sort(row)[-2:]
+            band = self.gm * np.sqrt(np.mean(row * row))
+            assert top2[1] - top2[0] <= band, f"period {p} {kind} {i}: gpu {gpu} oracle {own}"
+            assert row[gpu] >= top2[1] - band
+            self.ambiguous += 1
+            return gpu
+        if kind == "accept":
+            gpu = int(tr["accept_len"][p])
+            if gpu == own:
+                return own
+            k = min(gpu, own)
+            assert abs(info[k] - self.r) <= self.gq * self.r, f"period {p}: accept gpu {gpu} oracle {own}"
+            self.ambiguous += 1
+            return gpu
+        raise AssertionError(kind)
+
+
+def _prefill(sr, gm, m, prompt, chunk, pos):
+    """Full-model passes of `chunk` tokens over every prompt token but the last, on the GPU
+    and in the oracle; returns the oracle's cache."""
+    cache = loop.new_cache(m, S.max_len)
+    body = prompt[:-1]
+    for p in range(0, len(body), chunk):
+        toks = body[p:p + chunk]
+        pos.fill_(p)
+        sr.sirius_model_forward(gm, dev_i32(toks), pos, False)
+        loop.forward(m, toks, cache, p, False, full_ffn_input_bf16=len(toks) >= MFMA_MIN)
+    pos.fill_(len(prompt) - 1)
+    return cache
+
+
+@pytest.mark.parametrize("n,r,periods", [(16, 0.1, 6), (8, 0.3, 10), (4, 0.05, 12), (4, 0.3, 12),
+                                         (1, 0.1, 8)])
+def test_generate_matches_oracle_replay(sr, tiny, n, r, periods):
+    import torch
+    bits, m = tiny
+    gm = _gpu_model(sr, bits, m.thresholds)
+    prompt = prompt_tokens(31, 16, S.vocab)
+    mfma = n >= MFMA_MIN  # the check pass's FFN runs on MFMA with bf16 input
+    guards = GUARDS_MFMA if mfma else GUARDS_FP32
+    say(f"generate n={n} r={r} periods={periods}: prefill")
+    pos = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ref_cache = _prefill(sr, gm, m, prompt, 15 if mfma else 7, pos)
+    seq = torch.zeros(n + 1, dtype=torch.int32, device="cuda")
+    seq[0] = int(prompt[-1])
+    say("  loop")
+    out, cnt, tr = sr.sirius_generate(gm, seq, pos, n, r, periods, trace_active=True)
+    trh = {k: host(v) for k, v in tr.items()}
+    out, cnt, final_pos = host(out), int(host(cnt)[0]), int(host(pos)[0])
+    say(f"  committed {cnt}, accept lengths {trh['accept_len'].tolist()}")
+    # the oracle's replay
+    replays = []
+
+    def factory(p):
+        replays.append(_Replay(trh, p, r, guards))
+        return replays[-1]
+
+    refs, recs = [], []
+    ppos, cur = len(prompt) - 1, int(prompt[-1])
+    nb = 0
+    for p in range(periods):
+        rec = loop.sirius_period(m, ref_cache, ppos, cur, n, r, full_ffn_input_bf16=mfma,
+                                 follow=factory(p))
+        for i in range(n):
+            for l in range(S.n_layers):
+                nb += _check_sets(rec.draft_sets[i][l], rec.draft_acts[i][l], m.thresholds[l])
+        q = np.asarray(rec.q)
+        assert np.all(np.abs(trh["q"][p] - q) <= guards[1] * q + 1e-6), f"period {p} q"
+        refs.extend(rec.committed)
+        recs.append(rec)
+        ppos, cur = rec.pos_after, rec.committed[-1]
+    amb = sum(rp.ambiguous for rp in replays)
+    decisions = periods * (n + 2)
+    say(f"  oracle AAL {loop.aal(recs):.2f}; decisions taken from the GPU under the guard: {amb} "
+        f"of {decisions}; boundary neurons {nb}")
+    assert [rc.accept for rc in recs] == trh["accept_len"].tolist()
+    assert cnt == len(refs) and out[:cnt].tolist() == refs
+    assert np.all(out[cnt:] == -1)
+    assert final_pos == ppos
+    assert int(host(seq)[0]) == cur
+    assert amb <= max(2, decisions // 20)
+    _cache_close(gm, ref_cache, ppos, LOGIT_TOL_MFMA if mfma else 1e-5)
+
+
+def test_generate_reject_all_is_greedy_full_decoding(sr, tiny):
+    """r > 1: every draft is rejected, each period commits the full model's own token."""
+    import torch
+    bits, m = tiny
+    gm = _gpu_model(sr, bits, m.thresholds)
+    prompt = prompt_tokens(32, 8, S.vocab)
+    pos = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sr.sirius_model_forward(gm, dev_i32(prompt[:-1]), pos, False)
+    pos.fill_(len(prompt) - 1)
+    seq = torch.zeros(5, dtype=torch.int32, device="cuda")
+    seq[0] = int(prompt[-1])
+    say("generate r=2 (reject all)")
+    out, cnt, tr = sr.sirius_generate(gm, seq, pos, 4, 2.0, 10, trace=True)
+    assert int(host(cnt)[0]) == 10
+    assert host(tr["accept_len"]).tolist() == [0] * 10
+    assert int(host(pos)[0]) == len(prompt) - 1 + 10
+    # the oracle's greedy decoding with the full model, one token per step (every GPU pass
+    # here has fewer than 8 tokens: fp32 FFN inputs throughout)
+    cache = loop.new_cache(m, S.max_len)
+    loop.forward(m, prompt[:-1], cache, 0, False)
+    toks = host(out)[:10].tolist()
+    cur, p = int(prompt[-1]), len(prompt) - 1
+    for k in range(10):
+        lg, _ = loop.forward(m, [cur], cache, p, False)
+        cur, p = int(np.argmax(lg[0])), p + 1
+        assert toks[k] == cur, f"token {k}"
