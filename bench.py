@@ -25,6 +25,11 @@ batch, all inputs resident in HBM:
             key/value, head size 128; 2048 cached rows), writing its own row
   attn16    the full model's verification pass over a 16-token chunk at the same position:
             rewrite of the 16 rows + causal attention; then the device-side rollback
+  loop16    one period of the Sirius loop (Algorithm 1: 16 greedy drafts by the sparse model,
+            the full model's check of the chunk with the cache rewrite, rollback and the
+            corrected token) on a small random-weight decoder (2 layers, d_model 256, d_ff 688,
+            4/2 heads of 64, vocabulary 1000), replayed from a captured HIP graph; step s
+            restores the cache, position and first input of period s % 8 of a run from the prompt
   cats70b   sparse FFN decode, one token, one Llama-3-70B FFN layer (d_model 8192,
             d_ff 28672, 50% calibrated), four rotated copies (5.6 GB)
 The printed value is the sparse FFN decode time per token (rows.cats, from
@@ -61,6 +66,7 @@ N_DECODE = 64
 PROMPT_T = 512
 VERIFY_B, VERIFY_K, VERIFY_V = 8, 16, 128256
 TREE_K, TREE_W = 16, 4
+LOOP_N, LOOP_R, LOOP_STATES = 16, 0.1, 8
 ATT_H, ATT_HKV, ATT_HD, ATT_L, ATT_P = 32, 8, 128, 4096, 2048
 N_LOGIT_BUFS = 4
 
@@ -124,7 +130,7 @@ def main():
     import torch
     import paper_2409_03856_amd as sr
     from synth import (decode_inputs, calibration_inputs, griffin_prompt, verify_inputs, tree_build_inputs,
-                       tree_verify_inputs, attn_inputs)
+                       tree_verify_inputs, attn_inputs, model_weights, prompt_tokens, TINY_MODEL)
 
     assert torch.cuda.is_available()
     dev = torch.device("cuda", 0)
@@ -215,9 +221,46 @@ def main():
     att_out = torch.empty((1, 16, ATT_H, ATT_HD), dtype=torch.float32, device=dev)
     act_t = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
     cnt_t = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
+    log("setup: small decoder for the loop")
+    TM = TINY_MODEL
+    mw = {k: torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).to(dev)
+          for k, v in model_weights(21, TM).items()}
+    xcal_m = torch.from_numpy(calibration_inputs(7, 64, TM.d_model)).to(dev)
+    t_m = [float(sr.sirius_cats_calibrate(xcal_m, mw["w_gate"][l], 0.5).item()) for l in range(TM.n_layers)]
+    gm = sr.Model(mw, TM.n_heads, TM.n_kv_heads, TM.head_dim, TM.max_len, t_m)
+    m_prompt = prompt_tokens(31, 16, TM.vocab)
+    m_pos0 = torch.zeros(1, dtype=torch.int32, device=dev)
+    sr.sirius_model_forward(gm, torch.from_numpy(m_prompt[:-1]).to(dev), m_pos0, False)
+    m_pos0.fill_(len(m_prompt) - 1)
+    m_seq0 = torch.zeros(LOOP_N + 1, dtype=torch.int32, device=dev)
+    m_seq0[0] = int(m_prompt[-1])
+    m_pos, m_seq = m_pos0.clone(), m_seq0.clone()
+    m_out = torch.full((LOOP_N,), -1, dtype=torch.int32, device=dev)
+    m_cnt = torch.zeros(1, dtype=torch.int32, device=dev)
+    m_ws = torch.empty(sr.sirius_model_workspace_size(gm, LOOP_N), dtype=torch.uint8, device=dev)
+    # the states (shared cache, position, first input) at the start of the first LOOP_STATES
+    # periods from the prompt; step s replays the period from state s % LOOP_STATES
+    snaps = []
+    for _ in range(LOOP_STATES):
+        snaps.append((gm.k_cache.clone(), gm.v_cache.clone(), m_pos.clone(), m_seq.clone()))
+        sr.sirius_generate(gm, m_seq, m_pos, LOOP_N, LOOP_R, 1, out_tokens=m_out, out_count=m_cnt, ws=m_ws)
+        m_cnt.zero_()
+    torch.cuda.synchronize()
+    loop_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(loop_graph):
+        sr.sirius_generate(gm, m_seq, m_pos, LOOP_N, LOOP_R, 1, out_tokens=m_out, out_count=m_cnt, ws=m_ws)
+    torch.cuda.synchronize()
+
+    def loop_reset(s):
+        kc, vc, p0, q0 = snaps[s % LOOP_STATES]
+        gm.k_cache.copy_(kc)
+        gm.v_cache.copy_(vc)
+        m_pos.copy_(p0)
+        m_seq.copy_(q0)
+        m_cnt.zero_()
 
     rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "tree_build", "tree_verify",
-            "topk", "attn1", "attn16", "cats70b"]
+            "topk", "attn1", "attn16", "loop16", "cats70b"]
     stream = torch.cuda.current_stream()
 
     def step(s, ev=None, with70=True):
@@ -228,6 +271,7 @@ def main():
                 ev[i].record(stream)
 
         att_pos.fill_(ATT_P)  # every step's attention starts from the same cached prefix
+        loop_reset(s)  # and the loop period from one of the stored states
         mark(0)
         sr.sirius_ffn_cats(xs[s % N_DECODE: s % N_DECODE + 1], *layers[c], thresholds[c], y=y,
                            active_idx=act_idx, active_cnt=cnt_log[s:s + 1])
@@ -263,12 +307,14 @@ def main():
         sr.sirius_attn_kv(a[0], a[1], a[2], a[3], a[4], att_pos, out=att_out)
         sr.sirius_kv_rollback(att_pos, att_acc, 16)
         mark(12)
+        loop_graph.replay()
+        mark(13)
         if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
             return
         c70 = s % NCOPY70
         sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
                            active_idx=act70, active_cnt=cnt70[s:s + 1])
-        mark(13)
+        mark(14)
 
     log("warmup")
     for s in range(args.warmup):
@@ -310,6 +356,23 @@ def main():
             kern[name] = {"avg_us": round(tot * 1e3 / n, 3), "launches": n}
     sr.sirius_profile_reset()
 
+    # the same loop period launched eagerly (kernel by kernel from the host), for comparison
+    # with the graph replay, and the tokens one period commits
+    loop_tokens = []
+    for k in range(LOOP_STATES):
+        loop_reset(k)
+        loop_graph.replay()
+        loop_tokens.append(int(m_cnt.item()))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    eager_ms = []
+    for k in range(LOOP_STATES):
+        loop_reset(k)
+        e0.record(stream)
+        sr.sirius_generate(gm, m_seq, m_pos, LOOP_N, LOOP_R, 1, out_tokens=m_out, out_count=m_cnt, ws=m_ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        eager_ms.append(e0.elapsed_time(e1))
+
     counts = cnt_log[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64)
     mean_active = float(counts.mean())
     mean_active70 = float(cnt70[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64).mean())
@@ -320,6 +383,7 @@ def main():
     verify_bytes = VERIFY_B * VERIFY_K * VERIFY_V * 4
     griffin_bytes = 2 * D_FF * D_MODEL * 2 + PROMPT_T * D_MODEL * 2 + 6 * k_keep * D_MODEL * 2
     cats70_bytes = F70 * D70 * 2 + 2 * mean_active70 * D70 * 2 + 2 * D70 * 4
+    model_bytes = sum(int(w.numel()) * 2 for w in mw.values())  # one pass over the decoder's weights
     row_bytes = {"cats": cats_bytes, "rmsnorm": 2 * D_MODEL * 4, "griffin": griffin_bytes,
                  "condensed": cond_bytes, "dense": dense_bytes, "dense16": dense_bytes + 2 * VERIFY_K * D_MODEL * 4,
                  "verify": verify_bytes, "tree_build": TREE_W * VERIFY_V * 4 + 2 * TREE_W * 4,
@@ -328,6 +392,7 @@ def main():
                  "attn1": (ATT_P + 1) * ATT_HKV * ATT_HD * 2 * 2 + 2 * ATT_H * ATT_HD * 4,
                  "attn16": (ATT_P + 16) * ATT_HKV * ATT_HD * 2 * 2 + 16 * ATT_HKV * ATT_HD * 2 * 2
                  + 2 * 16 * ATT_H * ATT_HD * 4,
+                 "loop16": (LOOP_N + 1) * model_bytes,
                  "cats70b": cats70_bytes}
 
     def med(v):
@@ -368,6 +433,14 @@ def main():
             "llama3_70b_layer": {"d_model": D70, "d_ff": F70, "layer_copies_rotated": NCOPY70,
                                  "mean_active_neurons": round(mean_active70, 1),
                                  "realized_sparsity": round(1.0 - mean_active70 / F70, 4)},
+            "loop16": {"decoder": f"{TM.n_layers} layers, d_model {TM.d_model}, d_ff {TM.d_ff}, "
+                                  f"{TM.n_heads}/{TM.n_kv_heads} heads of {TM.head_dim}, vocab {TM.vocab}",
+                       "kernel_size": LOOP_N, "r": LOOP_R, "states": LOOP_STATES,
+                       "tokens_per_period": loop_tokens, "aal": round(float(np.mean(loop_tokens)), 3),
+                       "us_per_period_graph": round(float(np.mean(row_ms["loop16"])) * 1e3, 1),
+                       "us_per_period_eager": round(float(np.mean(eager_ms)) * 1e3, 1),
+                       "us_per_token_graph": round(float(np.mean(row_ms["loop16"])) * 1e3
+                                                   / max(float(np.mean(loop_tokens)), 1e-9), 2)},
         },
         "roofline": {
             "kernel": dom,

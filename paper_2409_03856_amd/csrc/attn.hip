@@ -10,14 +10,20 @@
 //
 //  attn_partial_kernel  grid (position chunk, key/value head x row group, batch), 256 threads.
 //                       The chunk's keys and values are staged 64 rows at a time in LDS as
-//                       fp32 (cache rows below p, the new rows from p on; the row-group-0
-//                       workgroup also writes the new rows into the cache: each is written by
-//                       exactly one workgroup and never read back from the cache in the
-//                       call). Scores in fp32 from register blocks (4 rows x 4 positions, or
-//                       4 rows x 1 position for up to 16 rows), causal mask, online softmax
-//                       (running max and sum per row), P.V into 4 x 4 register blocks; the
-//                       chunk's (max, sum, unnormalised output) per row go to the workspace.
-//  attn_combine_kernel  one workgroup per query row merges the chunks in order.
+//                       bf16, every load of a tile issued before the first is stored (cache
+//                       rows below p, the new rows from p on; the row-group-0 workgroup also
+//                       writes the new rows into the cache: each is written by exactly one
+//                       workgroup and never read back from the cache in the call). Scores in
+//                       fp32: with more than 16 query rows from 4 rows x 4 positions register
+//                       blocks, else each score's dot product split over four lanes; causal
+//                       mask, online softmax (running max and sum per row), P.V into 4 x 4
+//                       register blocks (with few rows, the tile's positions split over groups
+//                       of threads whose shares are summed in a fixed order); the chunk's
+//                       (max, sum, unnormalised output) per row go to the workspace. The score
+//                       tile reuses the key buffer once the scores are formed.
+//  attn_combine_kernel  one workgroup per query row: the chunks' weights exp(m_c - M) first
+//                       (one chunk per thread), then each thread sums its output column over
+//                       the chunks in order.
 //  kv_rollback_kernel   cache_pos[b] += min(accept_len[b] + 1, n).
 #include <math.h>
 

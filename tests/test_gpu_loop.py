@@ -261,3 +261,54 @@ def test_generate_reject_all_is_greedy_full_decoding(sr, tiny):
         lg, _ = loop.forward(m, [cur], cache, p, False)
         cur, p = int(np.argmax(lg[0])), p + 1
         assert toks[k] == cur, f"token {k}"
+
+
+def test_graph_replay_of_a_period_equals_eager_periods(sr, tiny):
+    """A period is a fixed launch sequence with its state in device memory, so one captured
+    period replayed K times equals K eager periods, bit for bit (checked after every replay,
+    with eager work and synchronisation between the replays)."""
+    import torch
+    bits, m = tiny
+    n, r, K = 16, 0.1, 5
+    prompt = prompt_tokens(33, 16, S.vocab)
+
+    def setup():
+        gm = _gpu_model(sr, bits, m.thresholds)
+        pos = torch.zeros(1, dtype=torch.int32, device="cuda")
+        sr.sirius_model_forward(gm, dev_i32(prompt[:-1]), pos, False)
+        pos.fill_(len(prompt) - 1)
+        seq = torch.zeros(n + 1, dtype=torch.int32, device="cuda")
+        seq[0] = int(prompt[-1])
+        out = torch.full((K * n,), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        return gm, pos, seq, out, cnt
+
+    say("graph: eager reference")
+    gm, pos, seq, out, cnt = setup()
+    snaps = []
+    for k in range(K):
+        sr.sirius_generate(gm, seq, pos, n, r, 1, out_tokens=out[k * n:], out_count=cnt)
+        c = int(host(cnt)[0])
+        snaps.append((host(out).copy(), c, int(host(pos)[0]), host(seq).copy()))
+        cnt.zero_()
+    say("graph: capture one period")
+    gm2, pos2, seq2, out2, cnt2 = setup()
+    ws = torch.empty(sr.sirius_model_workspace_size(gm2, n), dtype=torch.uint8, device="cuda")
+    slot = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sr.sirius_generate(gm2, seq2, pos2, n, r, 1, out_tokens=slot, out_count=cnt2, ws=ws)
+    for k in range(K):
+        say(f"graph: replay {k}")
+        g.replay()
+        torch.cuda.synchronize()
+        out2[k * n:(k + 1) * n].copy_(slot)  # eager work between the replays
+        c = int(host(cnt2)[0])
+        ref_out, ref_c, ref_pos, ref_seq = snaps[k]
+        assert c == ref_c
+        assert host(out2)[k * n:k * n + c].tolist() == ref_out[k * n:k * n + c].tolist()
+        assert int(host(pos2)[0]) == ref_pos
+        assert host(seq2).tolist() == ref_seq.tolist()
+        cnt2.zero_()
+        slot.fill_(-1)
