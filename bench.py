@@ -1,6 +1,6 @@
 """Benchmark of the Sirius hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--copy-mib N]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-sweep] [--copy-mib N]
 
 Workload (headline): one Llama-3-8B FFN layer (d_model 4096, d_ff 14336, bf16
 neuron-major weights ~ N(0, 0.02)), batch-1 decode with per-token threshold
@@ -36,14 +36,23 @@ The printed value is the sparse FFN decode time per token (rows.cats, from
 row-boundary HIP events in the timed region). The roofline object is for the
 sparse path's dominant kernel (cats_decode: gate GEMV, threshold, compaction,
 kept up rows and kept down rows in one pass; the other launch is the small
-fixed-order reduce), timed by the library's per-kernel HIP events in a second
-pass of the same K steps right after the timed region. Those events ride on the
-kernel's own dispatch packet (hipExtLaunchKernel), so they time the kernel from
-its start to its end, as a kernel trace does. Its `traffic` is the
+fixed-order reduce), timed in a second pass of the same K steps by the
+library's per-kernel HIP events, switched on for the cats call's own two
+dispatches only (events on a dispatch perturb the timeline, so the timed region
+carries none). Those events ride on the kernel's own dispatch packet
+(hipExtLaunchKernel), so they time the kernel from its start to its end, as a
+kernel trace does. A third pass with events on every dispatch gives the other
+kernels' times (`kernels`); there the host falls behind the GPU, which idles
+between kernels, so those times run slightly high. Its `traffic` is the
 HBM byte count per launch from the committed rocprofv3 counter summary under
 profiles/, reported only while that summary's kernel-source digest matches the
 current sources (`--copy-mib` adds the plain copy whose counters scale
 FETCH_SIZE/WRITE_SIZE).
+
+After the timed region, `sparsity_scaling` repeats the headline layer's decode
+at calibrated sparsities 0 (every neuron kept), 0.4, 0.5, 0.65 and 0.8 and fits
+decode time = fixed + slope x density: the fixed part is the dense gate GEMV,
+the slope the kept up and down rows, which should scale with 1 - s.
 """
 
 from __future__ import annotations
@@ -69,6 +78,8 @@ TREE_K, TREE_W = 16, 4
 LOOP_N, LOOP_R, LOOP_STATES = 16, 0.1, 8
 ATT_H, ATT_HKV, ATT_HD, ATT_L, ATT_P = 32, 8, 128, 4096, 2048
 N_LOGIT_BUFS = 4
+SWEEP = (0.0, 0.4, 0.5, 0.65, 0.8)
+SWEEP_CALLS = 40
 
 
 def log(*a):
@@ -82,6 +93,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--no-sweep", action="store_true",
+                   help="leave out the sparsity sweep (for profiler runs that average one kernel's launches)")
     p.add_argument("--copy-mib", type=int, default=0,
                    help="after setup, run one plain device-to-device copy of this many MiB (the reference "
                         "kernel that scales the HBM byte counters)")
@@ -263,7 +276,7 @@ def main():
             "topk", "attn1", "attn16", "loop16", "cats70b"]
     stream = torch.cuda.current_stream()
 
-    def step(s, ev=None, with70=True):
+    def step(s, ev=None, with70=True, time_cats=False):
         c = s % NCOPY
 
         def mark(i):
@@ -273,8 +286,12 @@ def main():
         att_pos.fill_(ATT_P)  # every step's attention starts from the same cached prefix
         loop_reset(s)  # and the loop period from one of the stored states
         mark(0)
+        if time_cats:  # events on the cats call's own two dispatches, nothing else
+            sr.sirius_profile_enable(True)
         sr.sirius_ffn_cats(xs[s % N_DECODE: s % N_DECODE + 1], *layers[c], thresholds[c], y=y,
                            active_idx=act_idx, active_cnt=cnt_log[s:s + 1])
+        if time_cats:
+            sr.sirius_profile_enable(False)
         mark(1)
         sr.sirius_rmsnorm(y, 1e-5, out=hn)
         mark(2)
@@ -330,6 +347,20 @@ def main():
         step(args.warmup + i, evs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+
+    # ------------------------------------------------------------------ dominant-kernel pass
+    # The same K steps again, with the library's per-kernel HIP events on the cats call's own
+    # two dispatches only: every other launch stays plain, so the host keeps ahead of the GPU
+    # and the kernel runs in the same surroundings as in the timed region.
+    sr.sirius_profile_reset()
+    for i in range(args.steps):
+        step(args.warmup + i, time_cats=True)
+    torch.cuda.synchronize()
+    live = {}
+    for name in ("cats_decode", "cats_reduce"):
+        tot, n = sr.sirius_profile_query(name)
+        live[name] = {"avg_us": round(tot * 1e3 / n, 3), "launches": n}
+    sr.sirius_profile_reset()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     row_ms = {r: [] for r in rows}
     for i in range(args.steps):
@@ -337,8 +368,10 @@ def main():
             row_ms[r].append(evs[i][j].elapsed_time(evs[i][j + 1]))
 
     # ------------------------------------------------------------------ per-kernel pass
-    # The same K steps again with the library's per-kernel HIP events (recorded on the
-    # stream each kernel runs on), for the roofline of the dominant kernel.
+    # The same K steps again with the library's per-kernel HIP events on every dispatch, for
+    # the breakdown of the other rows. With events on every launch the host falls behind and
+    # the GPU idles between kernels, so these times run a little high; the roofline uses the
+    # timed region's own measurement of the dominant kernel.
     sr.sirius_profile_reset()
     sr.sirius_profile_enable(True)
     for i in range(args.steps):
@@ -355,6 +388,48 @@ def main():
         if n:
             kern[name] = {"avg_us": round(tot * 1e3 / n, 3), "launches": n}
     sr.sirius_profile_reset()
+
+    # sparsity sweep of the headline layer: per-token CATS decode at several calibrated
+    # sparsities (0 = every neuron kept, through the same kernels), to check that the time of
+    # the kept up and down rows scales with the density 1 - s while the dense gate stays fixed
+    sweep = []
+    for s_t in (() if args.no_sweep else SWEEP):
+        ts = [-1.0] * NCOPY if s_t == 0.0 else \
+            [float(sr.sirius_cats_calibrate(x_cal, layers[c][0], s_t).item()) for c in range(NCOPY)]
+        cnt_s = torch.zeros((SWEEP_CALLS,), dtype=torch.int32, device=dev)
+        for i in range(4):
+            sr.sirius_ffn_cats(xs[i:i + 1], *layers[i % NCOPY], ts[i % NCOPY], y=y, active_idx=act_idx,
+                               active_cnt=cnt_s[i:i + 1])
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(SWEEP_CALLS):
+            sr.sirius_ffn_cats(xs[i % N_DECODE:i % N_DECODE + 1], *layers[i % NCOPY], ts[i % NCOPY], y=y,
+                               active_idx=act_idx, active_cnt=cnt_s[i:i + 1])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        call_us = e0.elapsed_time(e1) * 1e3 / SWEEP_CALLS
+        sr.sirius_profile_reset()
+        sr.sirius_profile_enable(True)
+        for i in range(SWEEP_CALLS):
+            sr.sirius_ffn_cats(xs[i % N_DECODE:i % N_DECODE + 1], *layers[i % NCOPY], ts[i % NCOPY], y=y,
+                               active_idx=act_idx, active_cnt=cnt_s[i:i + 1])
+        torch.cuda.synchronize()
+        sr.sirius_profile_enable(False)
+        tot, n = sr.sirius_profile_query("cats_decode")
+        sr.sirius_profile_reset()
+        dens = float(cnt_s.double().mean().item()) / D_FF
+        dec_us = tot * 1e3 / n
+        sb = D_FF * D_MODEL * 2 + 2 * dens * D_FF * D_MODEL * 2
+        sweep.append({"target": s_t, "realized_sparsity": round(1.0 - dens, 4), "call_us": round(call_us, 2),
+                      "decode_us": round(dec_us, 2), "decode_gbps": round(sb / (dec_us * 1e-6) / 1e9, 1)})
+    # least-squares line decode_us = gate_us + updown_us_at_density_1 * density
+    slope = icpt = resid_max = float("nan")
+    if sweep:
+        dn = np.array([1.0 - r["realized_sparsity"] for r in sweep])
+        tu = np.array([r["decode_us"] for r in sweep])
+        slope, icpt = np.polyfit(dn, tu, 1)
+        resid_max = float(np.max(np.abs(tu - (icpt + slope * dn))))
 
     # the same loop period launched eagerly (kernel by kernel from the host), for comparison
     # with the graph replay, and the tokens one period commits
@@ -407,7 +482,7 @@ def main():
 
     cats_us = float(np.mean(row_ms["cats"])) * 1e3
     dom = DOM_KERNEL  # everything but the final reduce
-    dom_us = kern[dom]["avg_us"]
+    dom_us = live[dom]["avg_us"]
     dom_bytes = D_FF * D_MODEL * 2 + 2 * mean_active * D_MODEL * 2 + D_MODEL * 4
     dom_gbps = dom_bytes / (dom_us * 1e-6) / 1e9
 
@@ -452,10 +527,18 @@ def main():
             "traffic": counted_traffic(),
             "alg_bytes_per_launch": int(dom_bytes),
             "avg_launch_us": dom_us,
-            "timing": "library per-kernel HIP events carried by the kernel dispatch itself (hipExtLaunchKernel) on the launch stream, separate K-step pass",
+            "launches": live[dom]["launches"],
+            "timing": "library per-kernel HIP events carried by the kernel dispatch itself (hipExtLaunchKernel) on the launch stream, in a second pass of the same K steps with events on the cats call only",
         },
         "rows": rows_out,
         "kernels": kern,
+        "kernels_dominant_pass": live,
+        "sparsity_scaling": None if not sweep else {
+            "layer": "llama3-8b FFN layer, batch 1, thresholds calibrated per copy on 256 N(0,1) inputs",
+            "calls_per_point": SWEEP_CALLS, "points": sweep,
+            "fit_decode_us": {"fixed_us": round(float(icpt), 2), "per_unit_density_us": round(float(slope), 2),
+                              "max_abs_residual_us": round(resid_max, 2)},
+        },
     }
 
     if not args.no_cpu_baseline:

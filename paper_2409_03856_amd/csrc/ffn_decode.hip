@@ -10,7 +10,10 @@
 //                    rows are in flight per wave (the next one is requested before the
 //                    current one is reduced); a = SiLU(W_gate[i].x), kept iff |a| > t;
 //                  * a wave ballot + popcount compacts the kept rows in ascending order;
-//                  * W_up rows of the kept neurons, h_i = a_i * (W_up[i].x), into LDS;
+//                  * W_up rows of the kept neurons, h_i = a_i * (W_up[i].x), into LDS
+//                    (dense with d_model <= 4096: every row is kept, so each wave takes the
+//                    gate and up rows of its neurons together, one pair in flight, and the
+//                    compaction and the separate up phase drop out);
 //                  * W_down rows of the kept neurons: thread (p, c) owns the eight output
 //                    columns of 16-byte chunk c and the kept rows p, p + P, ... with eight
 //                    row chunks in flight; the P row groups are summed in a fixed order
@@ -81,6 +84,9 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
   float* xs = reinterpret_cast<float*>(s_x4);
 
   constexpr int NB = CPL <= 8 ? 2 : 1;  // rows in flight per wave in the gate and up phases
+  // dense with d_model <= 4096: every row is kept, so a wave takes the gate and up rows of one
+  // neuron together (two rows in flight) and the separate up phase and the compaction go away
+  constexpr bool kFused = MODE == kModeDense && NB == 2;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int seg = blockIdx.x, G = gridDim.x;
   const int nch = d >> 3, nv4 = d >> 2;
@@ -89,6 +95,7 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
 
   uint4 wa[CPL], wb[CPL];
   load_row(wa, wg + (size_t)(r0 + wave) * nch, lane, nch, MODE != kModeKeyed && wave < nr);
+  if (kFused) load_row(wb, wu + (size_t)(r0 + wave) * nch, lane, nch, wave < nr);
 
   // ---- x into LDS, RMS-normalised when norm_eps >= 0
   float ss = 0.f;
@@ -136,7 +143,18 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
       s_keep[j] = topk_key(a, r0 + j) >= c0 ? 1 : 0;
     }
   }
-  for (int j = wave; MODE != kModeKeyed && j < nr; j += NB * kWaves) {
+  if (kFused) {
+    for (int j = wave; j < nr; j += kWaves) {
+      const int jn = j + kWaves;
+      const float a = silu(row_dot(wa, xs, lane, nch));
+      load_row(wa, wg + (size_t)(r0 + jn) * nch, lane, nch, jn < nr);
+      const float u = row_dot(wb, xs, lane, nch);
+      load_row(wb, wu + (size_t)(r0 + jn) * nch, lane, nch, jn < nr);
+      if (lane == 0) s_h[j] = a * u;  // kept list = the segment's rows in order
+    }
+    for (int j = tid; j < nr; j += kThreads) s_list[j] = j;
+  }
+  for (int j = wave; MODE != kModeKeyed && !kFused && j < nr; j += NB * kWaves) {
     if (NB == 2) {
       const int j1 = j + kWaves, j2 = j + 2 * kWaves;
       load_row(wb, wg + (size_t)(r0 + j1) * nch, lane, nch, j1 < nr);
@@ -152,27 +170,31 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
   __syncthreads();
 
   // ---- ascending compaction of the kept rows: wave ballot + popcount, wave offsets in LDS
-  const int keep = (tid < nr) ? s_keep[tid] : 0;
-  const unsigned long long m = __ballot(keep);
-  if (lane == 0) s_wc[wave] = __popcll(m);
-  __syncthreads();
-  int off = 0, nk = 0;
+  int nk = nr;
+  if (!kFused) {
+    const int keep = (tid < nr) ? s_keep[tid] : 0;
+    const unsigned long long m = __ballot(keep);
+    if (lane == 0) s_wc[wave] = __popcll(m);
+    __syncthreads();
+    int off = 0;
+    nk = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const int c = s_wc[w];
-    off += (w < wave) ? c : 0;
-    nk += c;
+    for (int w = 0; w < kWaves; ++w) {
+      const int c = s_wc[w];
+      off += (w < wave) ? c : 0;
+      nk += c;
+    }
+    if (keep) {
+      const int pos = off + __popcll(m & ((1ull << lane) - 1ull));
+      s_list[pos] = tid;
+      uidx[(size_t)seg * rmax + pos] = r0 + tid;
+    }
+    if (tid == 0) ucnt[seg] = nk;
+    __syncthreads();
   }
-  if (keep) {
-    const int pos = off + __popcll(m & ((1ull << lane) - 1ull));
-    s_list[pos] = tid;
-    uidx[(size_t)seg * rmax + pos] = r0 + tid;
-  }
-  if (tid == 0) ucnt[seg] = nk;
-  __syncthreads();
 
   // ---- W_up rows of the kept neurons: h = a * u
-  for (int k = wave; k < nk; k += NB * kWaves) {
+  for (int k = wave; !kFused && k < nk; k += NB * kWaves) {
     load_row(wa, wu + (size_t)(r0 + s_list[k]) * nch, lane, nch, true);
     const int k1 = k + kWaves;
     if (NB == 2) load_row(wb, wu + (size_t)(r0 + s_list[k1 < nk ? k1 : k]) * nch, lane, nch, k1 < nk);

@@ -52,7 +52,8 @@ constexpr int kListBlocks = 16;             // workgroups copying each token's a
 constexpr int kMaxSegs = 4096;              // row segments a down launch can take (d_ff / 16)
 constexpr int kRedOut4 = 16;                // float4 outputs per reduce workgroup
 constexpr int kRedGroups = 256 / kRedOut4;  // partial-row groups per reduce workgroup
-constexpr int kRedUnroll = 8;               // partial rows in flight per reduce thread
+constexpr int kRedUnroll = 16;              // partial rows in flight per reduce thread (one round
+                                            // for up to 256 partial rows)
 constexpr int kXLdsFloats = 32768;          // fp32 x staged in LDS: 128 KiB (LDS is 160 KiB)
 
 // kModeAct writes the signed gate activations and stops; kModeKeyed takes them (and a per-token
@@ -449,9 +450,24 @@ __global__ __launch_bounds__(256) void reduce_kernel(
     return;
   }
   // ---- ascending active list of token b: prefix over the segment counts, then every thread
-  // copies list positions tid, tid + 256, ... (segment found by binary search), 8 in flight
+  // copies list slots tid, tid + 256, ..., 8 in flight. The first slots are requested together
+  // with the counts: every slot lies inside the [ntiles, rmax] list buffer, so reading one that
+  // its segment did not fill is harmless, and whether it is kept is decided after the prefix.
   __shared__ int s_pref[kGateSegs + 1];
   const int b = (blockIdx.x - nred) / kListBlocks, part_k = (blockIdx.x - nred) % kListBlocks;
+  const int32_t* src = bidx + (size_t)b * ntiles * rmax;
+  const int nslot = ntiles * rmax;
+  const int q_lo = (int)(((long long)nslot * part_k) / kListBlocks);
+  const int q_hi = (int)(((long long)nslot * (part_k + 1)) / kListBlocks);
+  int v[8];
+  auto load_slots = [&](int q0) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int q = q0 + 256 * u;
+      v[u] = q < q_hi ? src[q] : -1;
+    }
+  };
+  load_slots(q_lo + tid);
   const int per = (ntiles + 255) / 256;
   const int beg = min(tid * per, ntiles), end = min(beg + per, ntiles);
   int local = 0;
@@ -465,22 +481,13 @@ __global__ __launch_bounds__(256) void reduce_kernel(
   if (tid == 0) s_pref[ntiles] = total;
   __syncthreads();
   // flattened (segment, slot) pairs: slot q = i * rmax + j holds entry j of segment i; this
-  // block copies slots [q_lo, q_hi) of token b
-  const int32_t* src = bidx + (size_t)b * ntiles * rmax;
-  const int nslot = ntiles * rmax;
-  const int q_lo = (int)(((long long)nslot * part_k) / kListBlocks);
-  const int q_hi = (int)(((long long)nslot * (part_k + 1)) / kListBlocks);
+  // block copies the filled slots among [q_lo, q_hi) of token b
   for (int q0 = q_lo + tid; q0 < q_hi; q0 += 8 * 256) {
-    int v[8];
+    if (q0 != q_lo + tid) load_slots(q0);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int q = q0 + 256 * u, i = q / rmax, j = q - i * rmax;
-      v[u] = (q < q_hi && j < s_pref[i + 1] - s_pref[i]) ? src[q] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int q = q0 + 256 * u, i = q / rmax, j = q - i * rmax;
-      if (v[u] >= 0) active_idx[(size_t)b * F + s_pref[i] + j] = v[u];
+      if (q < q_hi && j < s_pref[i + 1] - s_pref[i]) active_idx[(size_t)b * F + s_pref[i] + j] = v[u];
     }
   }
   if (tid == 0 && part_k == 0) active_cnt[b] = total;
