@@ -5,7 +5,12 @@
 // organised around full-line weight reads, and v_mfma_f32_16x16x32_bf16 does the arithmetic.
 //
 //  prep_x_kernel   x -> RMSNorm (optional) -> bf16, zero-padded to a multiple of 16 rows.
-//  gate_up_kernel  H = SiLU(X W_gate^T) * (X W_up^T). A two-wave workgroup owns 8 neurons
+//  gate_up_ring_kernel  H for one 16-token tile (the full model's check of a 16-token chunk):
+//                  one 512-thread workgroup per segment of at most 56 neurons, weights and x
+//                  moved into a four-slot LDS ring by direct global-to-LDS loads (three K
+//                  blocks in flight, no staging registers); see its definition.
+//  gate_up_kernel  H = SiLU(X W_gate^T) * (X W_up^T) for the other shapes (more than 16
+//                  tokens, d_model not a multiple of 128). A two-wave workgroup owns 8 neurons
 //                  (the MFMA tile's other 8 B-operand rows are zero), 7 workgroups per CU at
 //                  d_ff = 14336. Per 256-wide K block it stages the tile's gate and up rows and
 //                  the x rows in LDS with coalesced loads (512 contiguous bytes per row;
@@ -221,6 +226,155 @@ __global__ __launch_bounds__(128) void gate_up_kernel(
   }
 }
 
+// ---- gate/up for one 16-token tile (B <= 16, d_model % 128 == 0, at most 56 neurons per
+// segment): one 512-thread workgroup per segment of np neurons (56 at d_ff = 14336, one per
+// CU). Each 128-wide K block of the segment's gate rows, up rows and the 16 x rows is moved
+// into one slot of a four-slot LDS ring with direct global-to-LDS 16-byte loads, so three
+// blocks (84 KiB of weights per CU) are in flight without staging registers, and the x block
+// is fetched once per segment instead of once per 8 neurons. A wave instruction writes 64
+// consecutive 16-byte LDS slots, so the row layout is fixed at 256 bytes per row; each lane
+// therefore fetches the chunk that its slot should hold under an XOR swizzle of the chunk
+// index by the row (chunk c of row r sits at position c ^ (r & 7)), which keeps the MFMA
+// operand reads of 16 rows at one chunk free of bank conflicts beyond the two passes that
+// 256 bytes need anyway. Wave w multiplies tile w / 2 (16 neurons) of the gate (w even) or up
+// (w odd) rows: four v_mfma_f32_16x16x32_bf16 steps per block. Every lane issues every load
+// (rows past the segment fetch a valid row that is never used), so the wait counts are exact.
+constexpr int kRgThreads = 512;
+constexpr int kRgK = 128;                        // K per ring block: 256 bytes per row
+constexpr int kRgRowBytes = kRgK * 2;
+constexpr int kRgRows = 128;                     // 2 npad weight rows + 16 x rows (+ unused)
+constexpr int kRgSlotBytes = kRgRows * kRgRowBytes;              // 32 KiB
+constexpr int kRgLoads = kRgRows * (kRgK / 8) / kRgThreads;      // direct loads per thread per block
+constexpr int kRgMaxNeurons = (kRgRows - kMTile) / 2;            // 56
+static_assert(kRgLoads == 4, "the wait counts below assume four loads per thread per block");
+
+__device__ __forceinline__ int rg_pos(int row, int chunk) { return chunk ^ (row & 7); }
+
+// vmcnt(n) with the other counters left alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without the release fence of __syncthreads(), which would wait for every
+// direct-to-LDS load still in flight. The ring's own wait counts make this wave's loads of the
+// block complete before it; LDS needs no cache maintenance, and every ds_read of the previous
+// block has been consumed by its MFMA before the barrier in program order. The memory clobber
+// keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+__global__ __launch_bounds__(kRgThreads) void gate_up_ring_kernel(
+    const uint16_t* __restrict__ xb, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int F16, int np,
+    uint16_t* __restrict__ hhi, uint16_t* __restrict__ hlo) {
+  // four slots as four arrays, so that every LDS access names its slot
+  __shared__ __attribute__((aligned(16))) unsigned char s_r0[kRgSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_r1[kRgSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_r2[kRgSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_r3[kRgSlotBytes];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int fr = lane & 15, grp = lane >> 4;
+  const int npad = (np + 7) & ~7;
+  const int n0 = blockIdx.x * np;
+  const int nblk = d / kRgK;
+
+  // this thread's four loads of a block: slot position g = q * 512 + tid (row g / 16,
+  // position g % 16), holding logical chunk rg_pos(row, position) of that row
+  const uint16_t* src[kRgLoads];
+  int lds_off[kRgLoads];
+#pragma unroll
+  for (int q = 0; q < kRgLoads; ++q) {
+    const int g = q * kRgThreads + tid;
+    const int r = g >> 4, c = rg_pos(r, g & 15);
+    const uint16_t* base;
+    if (r < 2 * npad) {
+      const int j = r < npad ? r : r - npad;
+      const int n = min(n0 + min(j, np - 1), F - 1);  // rows past the segment or d_ff: any valid row
+      base = (r < npad ? wg : wu) + (size_t)n * d;
+    } else {
+      const int t = r - 2 * npad;
+      base = xb + (size_t)(t < kMTile ? t : 0) * d;  // unused rows: x row 0
+    }
+    src[q] = base + 8 * c;
+    lds_off[q] = (q * kRgThreads + wave * kWave) * 16;  // wave-uniform: lane l lands at + 16 l
+  }
+  auto issue = [&](unsigned char* slot, int blk) {
+#pragma unroll
+    for (int q = 0; q < kRgLoads; ++q) {
+      // a wave instruction covers four whole rows and 2 npad is a multiple of 16: the row
+      // kind is uniform over the wave (taken from lane 0, so the branch is scalar and each
+      // q issues exactly one load per wave)
+      const int w0 = q * kRgThreads + wave * kWave;
+      const bool weight = __builtin_amdgcn_readfirstlane(w0 >> 4) < 2 * npad;
+      const void* gp = src[q] + (size_t)blk * kRgK;
+      auto* lp = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<size_t>(slot + lds_off[q]));
+      if (weight)
+        __builtin_amdgcn_global_load_lds(gp, lp, 16, 0, 2);  // non-temporal: read once
+      else
+        __builtin_amdgcn_global_load_lds(gp, lp, 16, 0, 0);
+    }
+  };
+
+  const int tau = wave >> 1, mu = wave & 1;
+  const bool active = 16 * tau < np;
+  const int wrow = mu * npad + 16 * tau + fr;  // B operand row (past np: never stored)
+  const int xrow = 2 * npad + fr;              // A operand row
+  floatx4_t acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const unsigned char* slot) {
+    if (!active) return;
+#pragma unroll
+    for (int i = 0; i < kRgK / 32; ++i) {
+      const int c = 4 * i + grp;
+      const uint4 bw = *reinterpret_cast<const uint4*>(slot + wrow * kRgRowBytes + 16 * rg_pos(wrow, c));
+      const uint4 ax = *reinterpret_cast<const uint4*>(slot + xrow * kRgRowBytes + 16 * rg_pos(xrow, c));
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ax), as_bf16x8(bw), acc, 0, 0, 0);
+    }
+  };
+  // block b: wait for it (the blocks issued after it stay in flight), barrier, refill the slot
+  // freed by block b - 1 with block b + 3, multiply block b
+  auto step = [&](unsigned char* slot, unsigned char* refill, int b) {
+    const int later = min(2, nblk - 1 - b);
+    if (later >= 2) wait_vm<2 * kRgLoads>();
+    else if (later == 1) wait_vm<kRgLoads>();
+    else wait_vm<0>();
+    ring_barrier();
+    if (b + 3 < nblk) issue(refill, b + 3);
+    compute(slot);
+  };
+  issue(s_r0, 0);
+  if (nblk > 1) issue(s_r1, 1);
+  if (nblk > 2) issue(s_r2, 2);
+  for (int b = 0; b < nblk; b += 4) {
+    step(s_r0, s_r3, b);
+    if (b + 1 < nblk) step(s_r1, s_r0, b + 1);
+    if (b + 2 < nblk) step(s_r2, s_r1, b + 2);
+    if (b + 3 < nblk) step(s_r3, s_r2, b + 3);
+  }
+
+  // epilogue: the up wave of each tile hands its sums to the gate wave through LDS
+  __syncthreads();  // every wave is done with the ring
+  floatx4_t* s_up = reinterpret_cast<floatx4_t*>(s_r0);  // [tile][lane]
+  if (active && mu == 1) s_up[tau * kWave + lane] = acc;
+  __syncthreads();
+  if (active && mu == 0) {
+    const floatx4_t u4 = s_up[tau * kWave + lane];
+    const int j = 16 * tau + fr, n = n0 + j;
+    if (j < np && n < F16) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = 4 * grp + r;
+        // C layout: lane holds neuron fr and tokens 4 (lane / 16) + r; past d_ff: h = 0
+        const float h = n < F ? silu(acc[r]) * u4[r] : 0.f;
+        const uint32_t hi = f32_to_bf16(h);
+        const float lo = h - __uint_as_float(hi << 16);
+        hhi[(size_t)m * F16 + n] = (uint16_t)hi;
+        hlo[(size_t)m * F16 + n] = (uint16_t)f32_to_bf16(lo);
+      }
+    }
+  }
+}
+
 // Y_partial[rho][m][c] = sum over the neurons n of range rho of H[m][n] * W_down[n][c]
 template <int MT>
 __global__ __launch_bounds__(256) void down_kernel(
@@ -369,20 +523,29 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
   }
   {
     ProfScope prof("ffn_mfma_gate_up", stream);
-    const dim3 grid(L.f16 / kGuRows);  // every row below F16 is written (0 past d_ff)
+    // one 16-token tile with d_model a multiple of 128 and at most 56 neurons per segment
+    // (d_ff <= 14336 over 256 segments): the LDS-ring kernel; otherwise 8 neurons per workgroup
+    const int rg_seg = std::min(256, L.f16 / 8);
+    const int rg_np = ceil_div(L.f16, rg_seg);
+    if (mt == 1 && d % kRgK == 0 && rg_np <= kRgMaxNeurons) {
+      klaunch(gate_up_ring_kernel, ceil_div(L.f16, rg_np), kRgThreads, 0, stream, xb, wg, wu, d, F,
+              L.f16, rg_np, hhi, hlo);
+    } else {
+      const dim3 grid(L.f16 / kGuRows);  // every row below F16 is written (0 past d_ff)
 #define SIRIUS_GU(MTV)                                                                       \
   case MTV:                                                                                  \
     klaunch(gate_up_kernel<MTV>, grid, 128, 0, stream, xb, wg, wu, d, F, L.f16, hhi, hlo);        \
     break;
-    switch (mt) {
-      SIRIUS_GU(1)
-      SIRIUS_GU(2)
-      SIRIUS_GU(3)
-      SIRIUS_GU(4)
-      default:
-        return hipErrorInvalidValue;
-    }
+      switch (mt) {
+        SIRIUS_GU(1)
+        SIRIUS_GU(2)
+        SIRIUS_GU(3)
+        SIRIUS_GU(4)
+        default:
+          return hipErrorInvalidValue;
+      }
 #undef SIRIUS_GU
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   {

@@ -54,6 +54,24 @@ def test_ragged_shapes_norm_resid(sr, d, f, bsz):
     check_ffn(host(y), oracle.ffn_masked(xn, wg, wu, wd, sets), resid=res)
 
 
+@pytest.mark.parametrize("d,f", [(8, 1), (264, 1000), (512, 97), (1024, 3000), (2048, 4099), (4096, 33),
+                                 (4096, 5000), (8192, 300)])
+def test_batch1_dense_ragged_norm_resid(sr, d, f):
+    """Batch-1 dense decode (every neuron kept: the gate and up rows of a neuron are read together
+    for d_model <= 4096) at ragged shapes, with RMSNorm and residual, against the oracle; and
+    bitwise equal to the threshold path with t < 0, which reads them in separate phases."""
+    say(f"dense B=1 ragged d={d} f={f}")
+    (wg, wu, wd), W = _layer(400 + d + f, d, f, 1.0 / np.sqrt(d))
+    x = decode_inputs(9 + d, 1, d) * 3.0
+    res = decode_inputs(10 + d, 1, d)
+    xn = oracle.rmsnorm(x, 1e-5)
+    yd = sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res))
+    check_ffn(host(yd), oracle.ffn_dense(xn, wg, wu, wd), resid=res)
+    yc, idx, cnt = sr.sirius_ffn_cats(dev_f32(x), *W, -1.0, norm_eps=1e-5, resid=dev_f32(res))
+    assert int(host(cnt)[0]) == f
+    assert np.array_equal(host(yd), host(yc))
+
+
 @pytest.mark.parametrize("bsz", [1, 2, 4, 7])
 def test_negative_threshold_is_dense(sr, bsz):
     say(f"cats t<0 B={bsz}")

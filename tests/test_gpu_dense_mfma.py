@@ -34,7 +34,11 @@ def _layer(seed, d, f, std):
 
 @pytest.mark.parametrize("d,f,bsz", [(256, 688, 8), (264, 1000, 9), (256, 688, 16), (512, 97, 17),
                                      (4096, 40, 33), (8, 1, 8), (264, 1000, 64), (520, 33, 48),
-                                     (8192, 100, 16)])
+                                     (8192, 100, 16),
+                                     # one 16-token tile with d_model % 128 == 0: the LDS-ring gate/up
+                                     # kernel (ragged d_ff, partial last segments, a single K block)
+                                     (1024, 5000, 16), (4096, 14000, 13), (128, 8, 8), (256, 1000, 10),
+                                     (4096, 40, 16)])
 def test_ragged_batches(sr, d, f, bsz):
     say(f"dense mfma d={d} f={f} B={bsz}")
     (wg, wu, wd), W = _layer(500 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
