@@ -21,8 +21,13 @@
 //                  deeper prefetch and staggered K starts measured the same or slower.) The
 //                  two waves' sums are added in a fixed order. h is stored as a pair of bf16
 //                  values, hi = bf16(h) and lo = bf16(h - hi), token-major [Mpad, F16]
-//                  (F16 = d_ff rounded up to 16, padding 0): the down product takes both,
-//                  which keeps about 16 significant bits of h.
+//                  (F16 = d_ff rounded up to 64, a whole number of down blocks; padding
+//                  0): the down product takes both, which keeps about 16 significant bits
+//                  of h.
+//  down_ring_kernel  Y_partial for one 16-token tile with d_model % 256 == 0: one 576-thread
+//                  workgroup per (256-column tile, neuron range), 64-neuron blocks of W_down
+//                  and the matching h fragments moved into a four-slot LDS ring by direct
+//                  global-to-LDS loads; see its definition.
 //  down_kernel     Y_partial = H W_down over one neuron range and one 64-column tile.
 //                  W_down is neuron-major (columns contiguous) but the MFMA B operand wants
 //                  eight consecutive neurons of one column per lane, so each 64-neuron x
@@ -486,12 +491,154 @@ __global__ __launch_bounds__(256) void down_kernel(
   }
 }
 
+// ---- down product for one 16-token tile (B <= 16, d_model % 256 == 0): one workgroup per
+// (256-column tile, neuron range), the ranges' partials added by the reduce kernel in order.
+// W_down is neuron-major, so the MFMA B operand (eight consecutive neurons of one column per
+// lane) is gathered from LDS with 16-bit reads. Each 64-neuron block of the range -- its 64
+// W_down rows over the tile's 256 columns (32 KiB, 512 bytes per row) and the hi/lo h
+// fragments of the 16 tokens (4 KiB, already in A-operand lane order) -- is moved into one
+// slot of a four-slot LDS ring by direct global-to-LDS loads: 36 KiB = 2304 16-byte pieces,
+// four per thread of a 576-thread workgroup (eight MFMA waves and one wave that only loads),
+// so three blocks are in flight. A W_down row's 16-byte chunk c sits at position
+// c ^ 2 ((row / 8) % 4): the 16-bit gathers of one instruction (16 columns of four 8-row
+// groups) then touch 32 different banks.
+constexpr int kDrThreads = 576;
+constexpr int kDrCols = 256;
+constexpr int kDrRowBytes = kDrCols * 2;
+constexpr int kDrWBytes = kDnChunk * kDrRowBytes;                   // 32 KiB
+constexpr int kDrHBytes = 2 * kDnSteps * kWave * 16;                // 4 KiB
+constexpr int kDrSlotBytes = kDrWBytes + kDrHBytes;                 // 36 KiB
+constexpr int kDrLoads = kDrSlotBytes / 16 / kDrThreads;            // 4
+static_assert(kDrLoads * kDrThreads * 16 == kDrSlotBytes, "whole loads per thread");
+static_assert(kDrLoads == kRgLoads, "the ring wait counts assume four loads per block");
+static_assert((kDrWBytes / 16) % kWave == 0, "every wave instruction is all W_down or all h");
+
+__device__ __forceinline__ int dr_pos(int row, int chunk) { return chunk ^ (((row >> 3) & 3) << 1); }
+
+__global__ __launch_bounds__(kDrThreads) void down_ring_kernel(
+    const uint16_t* __restrict__ hhi, const uint16_t* __restrict__ hlo, int F16,
+    const uint16_t* __restrict__ wd, int d, int F, int B, int nchunk, float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) unsigned char s_d0[kDrSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_d1[kDrSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_d2[kDrSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char s_d3[kDrSlotBytes];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int c0 = blockIdx.x * kDrCols, rho = blockIdx.y, gr = gridDim.y;
+  const int ch_lo = (int)(((long long)nchunk * rho) / gr);
+  const int nblk = (int)(((long long)nchunk * (rho + 1)) / gr) - ch_lo;
+
+  // this thread's loads of a block: slot piece g = q * 576 + tid. Pieces below 2048 are W_down
+  // row g / 32 (of the block's 64), position g % 32, holding chunk dr_pos(row, position) of
+  // the tile's columns; the rest are h fragment (which, step, lane) = (hg / 128, hg / 64 % 2,
+  // hg % 64): token lane % 16, neurons 32 step + 8 (lane / 16) .. + 7 of the block.
+  const uint16_t* src[kDrLoads];
+  size_t stride[kDrLoads];  // elements to the same piece of the next block
+  bool wpiece[kDrLoads];
+  int lds_off[kDrLoads];
+#pragma unroll
+  for (int q = 0; q < kDrLoads; ++q) {
+    const int g = q * kDrThreads + tid;
+    const int g0 = __builtin_amdgcn_readfirstlane(q * kDrThreads + wave * kWave);
+    wpiece[q] = g0 < kDrWBytes / 16;
+    if (wpiece[q]) {
+      const int r = g >> 5, c = dr_pos(r, g & 31);
+      // rows past d_ff read row d_ff - 1 (finite); their h is 0 (F16 is a multiple of 64)
+      const int n = min(ch_lo * kDnChunk + r, F - 1);
+      src[q] = wd + (size_t)n * d + c0 + 8 * c;
+      stride[q] = (size_t)kDnChunk * d;
+    } else {
+      const int hg = g - kDrWBytes / 16;
+      const int which = hg >> 7, st = (hg >> 6) & 1, l = hg & 63;
+      src[q] = (which ? hlo : hhi) + (size_t)(l & 15) * F16 + ch_lo * kDnChunk + 32 * st + 8 * (l >> 4);
+      stride[q] = kDnChunk;
+    }
+    lds_off[q] = (q * kDrThreads + wave * kWave) * 16;
+  }
+  auto issue = [&](unsigned char* slot, int b) {
+#pragma unroll
+    for (int q = 0; q < kDrLoads; ++q) {
+      const uint16_t* gp = src[q] + (size_t)b * stride[q];
+      auto* lp = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<size_t>(slot + lds_off[q]));
+      if (wpiece[q]) {
+        // a W_down row past d_ff stays at row d_ff - 1 in every block
+        const uint16_t* gw = gp;
+        if (ch_lo * kDnChunk + b * kDnChunk + ((q * kDrThreads + tid) >> 5) >= F)
+          gw = wd + (size_t)(F - 1) * d + (src[q] - wd) % d;
+        __builtin_amdgcn_global_load_lds(gw, lp, 16, 0, 2);
+      } else {
+        __builtin_amdgcn_global_load_lds(gp, lp, 16, 0, 0);
+      }
+    }
+  };
+
+  const int nb = lane & 15, gq = lane >> 4;
+  floatx4_t acc[2] = {floatx4_t{0.f, 0.f, 0.f, 0.f}, floatx4_t{0.f, 0.f, 0.f, 0.f}};
+  auto compute = [&](const unsigned char* slot) {
+    if (wave >= 8) return;  // the load-only wave
+#pragma unroll
+    for (int st = 0; st < kDnSteps; ++st) {
+      const bf16x8_t ahi = as_bf16x8(*reinterpret_cast<const uint4*>(slot + kDrWBytes + 16 * (st * kWave + lane)));
+      const bf16x8_t alo = as_bf16x8(*reinterpret_cast<const uint4*>(slot + kDrWBytes + 16 * ((kDnSteps + st) * kWave + lane)));
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = 32 * wave + 16 * j + nb;
+        uint32_t bw[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int r0 = 32 * st + 8 * gq + 2 * jj, r1 = r0 + 1;
+          const uint32_t e0 = *reinterpret_cast<const uint16_t*>(
+              slot + r0 * kDrRowBytes + 16 * dr_pos(r0, col >> 3) + 2 * (col & 7));
+          const uint32_t e1 = *reinterpret_cast<const uint16_t*>(
+              slot + r1 * kDrRowBytes + 16 * dr_pos(r1, col >> 3) + 2 * (col & 7));
+          bw[jj] = e0 | (e1 << 16);
+        }
+        const bf16x8_t bop = as_bf16x8(make_uint4(bw[0], bw[1], bw[2], bw[3]));
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bop, acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bop, acc[j], 0, 0, 0);
+      }
+    }
+  };
+  auto step = [&](unsigned char* slot, unsigned char* refill, int b) {
+    const int later = min(2, nblk - 1 - b);
+    if (later >= 2) wait_vm<2 * kDrLoads>();
+    else if (later == 1) wait_vm<kDrLoads>();
+    else wait_vm<0>();
+    ring_barrier();
+    if (b + 3 < nblk) issue(refill, b + 3);
+    compute(slot);
+  };
+  if (nblk > 0) issue(s_d0, 0);
+  if (nblk > 1) issue(s_d1, 1);
+  if (nblk > 2) issue(s_d2, 2);
+  for (int b = 0; b < nblk; b += 4) {
+    step(s_d0, s_d3, b);
+    if (b + 1 < nblk) step(s_d1, s_d0, b + 1);
+    if (b + 2 < nblk) step(s_d2, s_d1, b + 2);
+    if (b + 3 < nblk) step(s_d3, s_d2, b + 3);
+  }
+
+  // C layout: lane holds column c0 + 32 wave + 16 j + lane % 16 and tokens 4 (lane / 16) + r
+  if (wave < 8) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c = c0 + 32 * wave + 16 * j + nb;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = 4 * gq + r;
+        if (m < B && c < d) part[((size_t)rho * B + m) * d + c] = acc[j][r];
+      }
+    }
+  }
+}
+
 }  // namespace
 
 MfmaLayout mfma_layout(int B, int d, int F) {
   MfmaLayout L{};
   L.mpad = ceil_div(B, kMTile) * kMTile;
-  L.ntiles = ceil_div(F, kMTile);
+  // h rows padded to whole 64-neuron down blocks (h = 0 past d_ff)
+  L.ntiles = ceil_div(F, kDnChunk) * (kDnChunk / kMTile);
   L.f16 = L.ntiles * kMTile;
   L.cs = ceil_div(d, kDnCols);
   L.nchunk = ceil_div(F, kDnChunk);
@@ -548,7 +695,13 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  {
+  if (mt == 1 && d % kDrCols == 0) {
+    // one 16-token tile: the LDS-ring down kernel, same partial layout
+    ProfScope prof("ffn_mfma_down", stream);
+    klaunch(down_ring_kernel, dim3(d / kDrCols, L.gr), kDrThreads, 0, stream, hhi, hlo, L.f16, wd, d,
+            F, B, L.nchunk, part);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
     ProfScope prof("ffn_mfma_down", stream);
     const dim3 grid(L.cs, L.gr);
 #define SIRIUS_DN(MTV)                                                                        \
