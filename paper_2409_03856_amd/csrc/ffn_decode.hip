@@ -1,6 +1,7 @@
 // Batch-1 SwiGLU FFN decode on gfx950 in one pass per row segment: dense, condensed,
 // per-token threshold sparsity (FSparse after CATS: the gate is read whole, W_up and W_down
-// only for the kept neurons) and the second pass of per-token top-k sparsity.
+// only for the kept neurons) and both passes of per-token top-k sparsity (the gate phase
+// alone writing the activations, then the kept up and down rows under the token's cut).
 //
 //  decode1_kernel  one 1024-thread workgroup (16 waves) per segment of contiguous neuron
 //                  rows, one workgroup per CU. In order:
@@ -42,7 +43,8 @@ constexpr int kDownUnroll = 8;            // W_down row chunks in flight per thr
 
 // kModeKeyed: per-token top-k; the gate activations come from a separate gate pass, and a
 // neuron is kept iff its top-k key reaches the token's cut (no W_gate read here).
-constexpr int kModeDense = 0, kModeSparse = 1, kModeKeyed = 2;
+// kModeAct: that gate pass: the gate phase alone, writing the signed activations.
+constexpr int kModeDense = 0, kModeSparse = 1, kModeKeyed = 2, kModeAct = 3;
 
 template <int CPL>
 __device__ __forceinline__ void load_row(uint4 (&w)[CPL], const uint4* row, int lane, int nch,
@@ -72,7 +74,8 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
     const float* __restrict__ x, const uint4* __restrict__ wg, const uint4* __restrict__ wu,
     const uint4* __restrict__ wd, int d, int F, float t, float norm_eps, int rmax,
     int32_t* __restrict__ uidx, int32_t* __restrict__ ucnt, float* __restrict__ part,
-    const float* __restrict__ act, const unsigned long long* __restrict__ cut) {
+    const float* __restrict__ act, const unsigned long long* __restrict__ cut,
+    float* __restrict__ act_out) {
   // x (normalised) during gate and up; the down phase's row-group partials afterwards
   __shared__ float4 s_x4[kMaxD / 4];
   __shared__ float s_a[kMaxRows];
@@ -131,6 +134,7 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
   auto gate_row = [&](const uint4(&w)[CPL], int j) {
     const float a = silu(row_dot(w, xs, lane, nch));
     if (lane == 0) {
+      if (MODE == kModeAct) act_out[r0 + j] = a;
       s_a[j] = a;
       s_keep[j] = (MODE == kModeDense || fabsf(a) > t) ? 1 : 0;
     }
@@ -167,6 +171,7 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
       load_row(wa, wg + (size_t)(r0 + j1) * nch, lane, nch, j1 < nr);
     }
   }
+  if (MODE == kModeAct) return;  // the activations are all this mode writes
   __syncthreads();
 
   // ---- ascending compaction of the kept rows: wave ballot + popcount, wave offsets in LDS
@@ -256,11 +261,11 @@ template <int MODE>
 hipError_t launch_mode(int cpl, int G, hipStream_t s, const float* x, const uint4* wg,
                        const uint4* wu, const uint4* wd, int d, int F, float t, float norm_eps,
                        int rmax, int32_t* uidx, int32_t* ucnt, float* part, const float* act,
-                       const unsigned long long* cut) {
+                       const unsigned long long* cut, float* act_out = nullptr) {
 #define SIRIUS_DECODE1(CPLV)                                                                    \
   case CPLV:                                                                                    \
     klaunch(decode1_kernel<CPLV, MODE>, G, kThreads, 0, s, x, wg, wu, wd, d, F, t, norm_eps, rmax,    \
-                                                      uidx, ucnt, part, act, cut);              \
+                                                      uidx, ucnt, part, act, cut, act_out);     \
     break;
   switch (cpl) {
     SIRIUS_DECODE1(1)
@@ -324,6 +329,16 @@ hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t
     return launch_reduce(part, L.nseg, 1, d, resid, y, stream, F, L.nseg, L.rmax, uidx, ucnt,
                          active_idx, active_cnt);
   return launch_reduce(part, L.nseg, 1, d, resid, y, stream);
+}
+
+hipError_t launch_decode1_act(const float* x, const uint16_t* wg, int d, int F, float norm_eps,
+                              float* act, hipStream_t stream) {
+  const Decode1Layout L = decode1_layout(d, F);
+  if (d > kMaxD || (d & 7) != 0 || L.rmax > kMaxRows || L.nseg > kSegs) return hipErrorInvalidValue;
+  ProfScope prof("topk_gate", stream);
+  return launch_mode<kModeAct>(pow2_cpl(d / 8), L.nseg, stream, x, reinterpret_cast<const uint4*>(wg),
+                               nullptr, nullptr, d, F, 0.f, norm_eps, L.rmax, nullptr, nullptr, nullptr,
+                               nullptr, nullptr, act);
 }
 
 }  // namespace sirius

@@ -517,13 +517,20 @@ __device__ __forceinline__ int dr_pos(int row, int chunk) { return chunk ^ (((ro
 
 __global__ __launch_bounds__(kDrThreads) void down_ring_kernel(
     const uint16_t* __restrict__ hhi, const uint16_t* __restrict__ hlo, int F16,
-    const uint16_t* __restrict__ wd, int d, int F, int B, int nchunk, float* __restrict__ part) {
+    const uint16_t* __restrict__ wd, int d, int F, int B, int nchunk, int gr,
+    float* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) unsigned char s_d0[kDrSlotBytes];
   __shared__ __attribute__((aligned(16))) unsigned char s_d1[kDrSlotBytes];
   __shared__ __attribute__((aligned(16))) unsigned char s_d2[kDrSlotBytes];
   __shared__ __attribute__((aligned(16))) unsigned char s_d3[kDrSlotBytes];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int c0 = blockIdx.x * kDrCols, rho = blockIdx.y, gr = gridDim.y;
+  // workgroups go to the eight XCDs in turn (id % 8); when the grid divides evenly, XCD j takes
+  // the consecutive (tile, range) indices [j N / 8, (j + 1) N / 8), so the column tiles of a
+  // neuron range share one L2 and its h fragments are fetched from HBM once
+  const int ncols = d / kDrCols, N = ncols * gr;
+  const int L = blockIdx.x;
+  const int idx = (N % 8 == 0) ? (L % 8) * (N / 8) + L / 8 : L;
+  const int c0 = (idx % ncols) * kDrCols, rho = idx / ncols;
   const int ch_lo = (int)(((long long)nchunk * rho) / gr);
   const int nblk = (int)(((long long)nchunk * (rho + 1)) / gr) - ch_lo;
 
@@ -698,8 +705,8 @@ hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint
   if (mt == 1 && d % kDrCols == 0) {
     // one 16-token tile: the LDS-ring down kernel, same partial layout
     ProfScope prof("ffn_mfma_down", stream);
-    klaunch(down_ring_kernel, dim3(d / kDrCols, L.gr), kDrThreads, 0, stream, hhi, hlo, L.f16, wd, d,
-            F, B, L.nchunk, part);
+    klaunch(down_ring_kernel, (d / kDrCols) * L.gr, kDrThreads, 0, stream, hhi, hlo, L.f16, wd, d, F,
+            B, L.nchunk, L.gr, part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
     ProfScope prof("ffn_mfma_down", stream);

@@ -64,6 +64,10 @@ struct Decode1Layout {
   int nseg, rmax;
   size_t uidx, ucnt, part, total;
 };
+// Batch-1 gate pass of per-token top-k: the signed activations SiLU(W_gate x) of one token
+// (x RMS-normalised when norm_eps >= 0) into act [F], by the decode kernel's gate phase.
+hipError_t launch_decode1_act(const float* x, const uint16_t* wg, int d, int F, float norm_eps,
+                              float* act, hipStream_t stream);
 Decode1Layout decode1_layout(int d, int F);
 hipError_t launch_ffn_decode1(const float* x, const uint16_t* wg, const uint16_t* wu,
                               const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,

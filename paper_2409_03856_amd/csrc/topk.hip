@@ -207,7 +207,8 @@ hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint
   float* act = reinterpret_cast<float*>(ws + L.act);
   unsigned long long* cut = reinterpret_cast<unsigned long long*>(ws + L.cut);
   char* fws = ws + L.ffn;
-  hipError_t e = launch_gate_act(x, B, wg, d, F, norm_eps, act, stream);
+  hipError_t e = B == 1 ? launch_decode1_act(x, wg, d, F, norm_eps, act, stream)
+                         : launch_gate_act(x, B, wg, d, F, norm_eps, act, stream);
   if (e != hipSuccess) return e;
   {
     ProfScope prof("topk_cut", stream);
