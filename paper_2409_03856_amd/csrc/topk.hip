@@ -4,8 +4,9 @@
 //
 // The k kept neurons depend on all d_ff gate activations of the token, so the pass splits in
 // three:
-//  1. gate_kernel (ffn_gemv.hip, activation mode): a = SiLU(W_gate xn) for every neuron into a
-//     [B, d_ff] buffer; the whole gate is read once, as in the threshold path.
+//  1. the gate pass: a = SiLU(W_gate xn) for every neuron into a [B, d_ff] buffer; the whole
+//     gate is read once, as in the threshold path (batch 1: the decode kernel's gate phase
+//     alone, ffn_decode.hip; larger batches: gate_kernel in activation mode, ffn_gemv.hip).
 //  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
 //     (|a| descending, then the lower index): a most-significant-digit radix select over the
 //     bits of |a| (the exponent byte, then mantissa bytes; LDS histograms, four copies per
