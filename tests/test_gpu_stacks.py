@@ -199,3 +199,18 @@ def test_llama3_70b_cats_stack(sr, stack70b, s):
     say(f"70B CATS stack s={s} B=1")
     kept = run_cats_stack(sr, stack70b, decode_inputs(8100, 1, LLAMA3_70B.d_model), s, (0, 39, 79))
     assert all(abs(k - (1.0 - s)) < 0.1 for k in kept), kept
+
+
+def test_llama3_70b_dense_verify_chunk_layers(sr, stack70b):
+    """The full model's 16-token pass over Llama-3-70B-shaped layers (MFMA path: 8 neuron ranges x
+    32 column tiles of the down product), with RMSNorm and residual, checked on three layers."""
+    bsz = 16
+    for l in (0, 39, 79):
+        say(f"70B dense B=16 layer {l}")
+        h_in = decode_inputs(8200 + l, bsz, LLAMA3_70B.d_model)
+        wg, wu, wd = stack70b.layers[l]
+        y = host(sr.sirius_ffn_dense(dev_f32(h_in), wg, wu, wd, norm_eps=EPS, resid=dev_f32(h_in)))
+        hwg, hwu, hwd = stack70b.host_layer(l)
+        xn = oracle.rmsnorm(h_in, EPS)
+        e, nb = check_ffn_rounded_norm(y, xn, hwg, hwu, hwd, resid=h_in)
+        say(f"  error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
