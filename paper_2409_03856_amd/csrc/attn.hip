@@ -21,9 +21,10 @@
 //                       of threads whose shares are summed in a fixed order); the chunk's
 //                       (max, sum, unnormalised output) per row go to the workspace. The score
 //                       tile reuses the key buffer once the scores are formed.
-//  attn_combine_kernel  one workgroup per query row: the chunks' weights exp(m_c - M) first
-//                       (one chunk per thread), then each thread sums its output column over
-//                       the chunks in order.
+//  attn_combine_kernel  one workgroup per query row: the chunks' (max, sum) and their first
+//                       outputs requested together, the weights exp(m_c - M) (one chunk per
+//                       thread), then each thread sums its output column over the chunks in
+//                       order.
 //  kv_rollback_kernel   cache_pos[b] += min(accept_len[b] + 1, n).
 #include <math.h>
 
@@ -370,56 +371,80 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   }
 }
 
-// One workgroup (hd threads) per query row: the chunks' maxima and weights first (one chunk
-// per thread, LDS), then each thread sums its output column over the chunks in order with the
-// loads issued ahead.
+// One workgroup (hd threads) per query row. Every thread requests its chunks' (max, sum) and
+// the first kCombBatch chunk outputs of its column together, so the row costs about one
+// memory round trip; the maximum over the chunks, the weights exp(m_c - M) (one chunk per
+// thread, LDS) and the denominator follow, then each thread sums its output column over the
+// chunks in order, the next batch requested before the current one is added. Chunks with no
+// visible position never write their outputs: those are read but replaced by 0 (a select, so
+// whatever the buffer holds there cannot reach the sum).
+constexpr int kCombBatch = 32;
+
 __global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
     int n, int H, int Hkv, int hd, int R, int nsplit, const float* __restrict__ pm,
     const float* __restrict__ pl, const float* __restrict__ po, float* __restrict__ out) {
-  __shared__ float s_m[kMaxSplits], s_w[kMaxSplits], s_red[kMaxHd / kWave];
+  __shared__ float s_w[kMaxSplits], s_red[kMaxHd / kWave];
   const int row = blockIdx.x;  // (b, kvh, r)
   const int r = row % R, bk = row / R, kvh = bk % Hkv, b = bk / Hkv;
   const int G = H / Hkv, i = r / G, h = kvh * G + (r - i * G);
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const float* m = pm + (size_t)row * nsplit;
   const float* l = pl + (size_t)row * nsplit;
-  float mx = -INFINITY;
-  for (int sp = tid; sp < nsplit; sp += kMaxHd) {
-    const float v = m[sp];
-    s_m[sp] = v;
-    mx = fmaxf(mx, v);
+  const float* o = po + (size_t)row * nsplit * hd + (tid < hd ? tid : 0);
+  constexpr int kPer = kMaxSplits / kMaxHd;  // chunks per thread for the max and the weights
+  static_assert(kMaxSplits % kMaxHd == 0, "whole chunks per thread");
+  float mv[kPer], lv[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int sp = tid + u * kMaxHd;
+    mv[u] = sp < nsplit ? m[sp] : -INFINITY;
+    lv[u] = sp < nsplit ? l[sp] : 0.f;
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
-  for (int k = 2; k < kWave; k <<= 1) mx = fmaxf(mx, __shfl_xor(mx, k, kWave));
+  float ov[kCombBatch];
+#pragma unroll
+  for (int u = 0; u < kCombBatch; ++u) ov[u] = u < nsplit ? o[(size_t)u * hd] : 0.f;
+
+  float mx = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) mx = fmaxf(mx, mv[u]);
+  for (int k = 1; k < kWave; k <<= 1) mx = fmaxf(mx, __shfl_xor(mx, k, kWave));
   if (lane == 0) s_red[wave] = mx;
   __syncthreads();
   float M = s_red[0];
   for (int w = 1; w < kMaxHd / kWave; ++w) M = fmaxf(M, s_red[w]);
   __syncthreads();
   float den = 0.f;
-  for (int sp = tid; sp < nsplit; sp += kMaxHd) {
-    const float w = (s_m[sp] > -INFINITY) ? expf(s_m[sp] - M) : 0.f;
-    s_w[sp] = w;
-    den = fmaf(l[sp], w, den);
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int sp = tid + u * kMaxHd;
+    if (sp < nsplit) {
+      const float w = (mv[u] > -INFINITY) ? expf(mv[u] - M) : 0.f;
+      s_w[sp] = w;
+      den = fmaf(lv[u], w, den);
+    }
   }
   for (int k = 1; k < kWave; k <<= 1) den += __shfl_xor(den, k, kWave);
   if (lane == 0) s_red[wave] = den;
   __syncthreads();
   den = 0.f;
   for (int w = 0; w < kMaxHd / kWave; ++w) den += s_red[w];
-  if (tid < hd) {
-    const float* o = po + (size_t)row * nsplit * hd + tid;
-    float num = 0.f;
-    for (int s0 = 0; s0 < nsplit; s0 += 8) {
-      float v[8];
+  float num = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kCombBatch) {
+    float nx[kCombBatch];
+    const int s1 = s0 + kCombBatch;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = (s0 + u < nsplit && s_w[s0 + u] > 0.f) ? o[(size_t)(s0 + u) * hd] : 0.f;
+    for (int u = 0; u < kCombBatch; ++u) nx[u] = s1 + u < nsplit ? o[(size_t)(s1 + u) * hd] : 0.f;
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (s0 + u < nsplit) num = fmaf(v[u], s_w[s0 + u], num);
+    for (int u = 0; u < kCombBatch; ++u) {
+      if (s0 + u < nsplit) {
+        const float w = s_w[s0 + u];
+        num = fmaf(w > 0.f ? ov[u] : 0.f, w, num);
+      }
     }
-    out[(((size_t)b * n + i) * H + h) * hd + tid] = num / den;
+#pragma unroll
+    for (int u = 0; u < kCombBatch; ++u) ov[u] = nx[u];
   }
+  if (tid < hd) out[(((size_t)b * n + i) * H + h) * hd + tid] = num / den;
 }
 
 __global__ void kv_rollback_kernel(int32_t* __restrict__ cache_pos,
