@@ -372,18 +372,20 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 }
 
 // One workgroup (hd threads) per query row. Every thread requests its chunks' (max, sum) and
-// the first kCombBatch chunk outputs of its column together, so the row costs about one
+// the first batch of chunk outputs of its column together, so the row costs about one
 // memory round trip; the maximum over the chunks, the weights exp(m_c - M) (one chunk per
 // thread, LDS) and the denominator follow, then each thread sums its output column over the
 // chunks in order, the next batch requested before the current one is added. Chunks with no
 // visible position never write their outputs: those are read but replaced by 0 (a select, so
-// whatever the buffer holds there cannot reach the sum).
-constexpr int kCombBatch = 32;
-
-__global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
-    int n, int H, int Hkv, int hd, int R, int nsplit, const float* __restrict__ pm,
-    const float* __restrict__ pl, const float* __restrict__ po, float* __restrict__ out) {
-  __shared__ float s_w[kMaxSplits], s_red[kMaxHd / kWave];
+// whatever the buffer holds there cannot reach the sum). NB chunk outputs are requested per
+// batch: 32 for long caches, 8 when there are at most 8 chunks (the small decoder's), where
+// unrolled guards for 32 would cost more than they save.
+template <int NB>
+__device__ __forceinline__ void combine_row(int n, int H, int Hkv, int hd, int R, int nsplit,
+                                            const float* __restrict__ pm,
+                                            const float* __restrict__ pl,
+                                            const float* __restrict__ po, float* __restrict__ out,
+                                            float* s_w, float* s_red) {
   const int row = blockIdx.x;  // (b, kvh, r)
   const int r = row % R, bk = row / R, kvh = bk % Hkv, b = bk / Hkv;
   const int G = H / Hkv, i = r / G, h = kvh * G + (r - i * G);
@@ -400,9 +402,9 @@ __global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
     mv[u] = sp < nsplit ? m[sp] : -INFINITY;
     lv[u] = sp < nsplit ? l[sp] : 0.f;
   }
-  float ov[kCombBatch];
+  float ov[NB];
 #pragma unroll
-  for (int u = 0; u < kCombBatch; ++u) ov[u] = u < nsplit ? o[(size_t)u * hd] : 0.f;
+  for (int u = 0; u < NB; ++u) ov[u] = u < nsplit ? o[(size_t)u * hd] : 0.f;
 
   float mx = -INFINITY;
 #pragma unroll
@@ -429,22 +431,32 @@ __global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
   den = 0.f;
   for (int w = 0; w < kMaxHd / kWave; ++w) den += s_red[w];
   float num = 0.f;
-  for (int s0 = 0; s0 < nsplit; s0 += kCombBatch) {
-    float nx[kCombBatch];
-    const int s1 = s0 + kCombBatch;
+  for (int s0 = 0; s0 < nsplit; s0 += NB) {
+    float nx[NB];
+    const int s1 = s0 + NB;
 #pragma unroll
-    for (int u = 0; u < kCombBatch; ++u) nx[u] = s1 + u < nsplit ? o[(size_t)(s1 + u) * hd] : 0.f;
+    for (int u = 0; u < NB; ++u) nx[u] = s1 + u < nsplit ? o[(size_t)(s1 + u) * hd] : 0.f;
 #pragma unroll
-    for (int u = 0; u < kCombBatch; ++u) {
+    for (int u = 0; u < NB; ++u) {
       if (s0 + u < nsplit) {
         const float w = s_w[s0 + u];
         num = fmaf(w > 0.f ? ov[u] : 0.f, w, num);
       }
     }
 #pragma unroll
-    for (int u = 0; u < kCombBatch; ++u) ov[u] = nx[u];
+    for (int u = 0; u < NB; ++u) ov[u] = nx[u];
   }
   if (tid < hd) out[(((size_t)b * n + i) * H + h) * hd + tid] = num / den;
+}
+
+__global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
+    int n, int H, int Hkv, int hd, int R, int nsplit, const float* __restrict__ pm,
+    const float* __restrict__ pl, const float* __restrict__ po, float* __restrict__ out) {
+  __shared__ float s_w[kMaxSplits], s_red[kMaxHd / kWave];
+  if (nsplit <= 8)
+    combine_row<8>(n, H, Hkv, hd, R, nsplit, pm, pl, po, out, s_w, s_red);
+  else
+    combine_row<32>(n, H, Hkv, hd, R, nsplit, pm, pl, po, out, s_w, s_red);
 }
 
 __global__ void kv_rollback_kernel(int32_t* __restrict__ cache_pos,
