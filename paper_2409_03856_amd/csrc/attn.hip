@@ -20,7 +20,9 @@
 //                       register blocks (with few rows, the tile's positions split over groups
 //                       of threads whose shares are summed in a fixed order); the chunk's
 //                       (max, sum, unnormalised output) per row go to the workspace. The score
-//                       tile reuses the key buffer once the scores are formed.
+//                       tile reuses the key buffer once the scores are formed. A cache of at
+//                       most 256 rows is one chunk per workgroup (its tiles in turn), and the
+//                       kernel writes the normalised output itself: no merge launch.
 //  attn_combine_kernel  one workgroup per query row: the chunks' (max, sum) and their first
 //                       outputs requested together, the weights exp(m_c - M) (one chunk per
 //                       thread), then each thread sums its output column over the chunks in
@@ -45,6 +47,7 @@ constexpr int kKVPitch8 = kMaxHd / 8 + 1; // bf16 key/value rows in 16-byte unit
 constexpr int kMaxOB = 2;                 // 4 x 4 output blocks per thread: 64 rows x 128 / 256 / 16
 constexpr int kStagePer = kTile * kMaxHd / 8 / kAttnThreads;  // 16-byte loads per thread and tile
 constexpr int kMaxSplits = 256;           // position chunks per call at most
+constexpr int kDirectMax = 256;           // caches up to this many rows: one chunk, no combine
 
 // BIG: up to 64 rows, scores in 4 x 4 register blocks; else up to 16 rows, each score's dot
 // product split over four lanes. Keys and values are staged as bf16; the score tile reuses
@@ -54,7 +57,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float* __restrict__ q, const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
     uint4* __restrict__ k_cache, uint4* __restrict__ v_cache, const int32_t* __restrict__ cache_pos,
     int n, int H, int Hkv, int hd, int Lmax, int chunk, int rgroups, int R, float scale,
-    float* __restrict__ pm, float* __restrict__ pl, float* __restrict__ po) {
+    float* __restrict__ pm, float* __restrict__ pl, float* __restrict__ po,
+    float* __restrict__ out) {
   constexpr int kRows = BIG ? kMaxRowsWg : 16;
   __shared__ float s_q[kRows * kPitch];
   __shared__ uint4 s_kp[kTile * kKVPitch8];  // keys (bf16), then the score tile [position][row]
@@ -74,8 +78,17 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   const int nr4 = (nr + 3) & ~3;
   const int hd4 = hd >> 2, hd8 = hd >> 3;
   const size_t rowbase = ((size_t)b * Hkv + kvh) * R + r0;  // partial row index of row r0
+  // one chunk per row (out != nullptr): the output itself, out[b][i][h][:] for row r0 + r
+  auto out_row = [&](int r) {
+    const int rr = r0 + r, i = rr / G, h = kvh * G + (rr - i * G);
+    return out + (((size_t)b * n + i) * H + h) * hd;
+  };
 
   if (!valid || c0 >= L) {  // nothing visible in this chunk (or a position outside the cache)
+    if (out != nullptr) {  // what the merge of empty chunks gives: 0 / 0
+      for (int e = tid; e < nr * hd; e += kAttnThreads) out_row(e / hd)[e % hd] = __builtin_nanf("");
+      return;
+    }
     if (tid < nr) {
       pm[(rowbase + tid) * nsplit + split] = -INFINITY;
       pl[(rowbase + tid) * nsplit + split] = 0.f;
@@ -324,9 +337,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       }
     }
   }
-  // ---- this chunk's partial: max, sum and the unnormalised output per row
+  // ---- this chunk's partial: max, sum and the unnormalised output per row (with one chunk,
+  // the output itself: the unnormalised output over the sum, as the merge computes it)
   __syncthreads();
-  if (tid < nr) {
+  if (tid < nr && out == nullptr) {
     pm[(rowbase + tid) * nsplit + split] = s_m[tid];
     pl[(rowbase + tid) * nsplit + split] = s_l[tid];
   }
@@ -339,8 +353,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
           const int r = 4 * rb + rr;
-          if (r < nr)
+          if (r < nr && out != nullptr) {
+            const float l = s_l[r];
+            const float4 a = acc[u][rr];
+            reinterpret_cast<float4*>(out_row(r))[d4] = make_float4(a.x / l, a.y / l, a.z / l, a.w / l);
+          } else if (r < nr) {
             reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = acc[u][rr];
+          }
         }
       }
     }
@@ -365,7 +384,12 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
           t.w += o.w;
         }
         const int r = 4 * rb + rr;
-        if (r < nr) reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = t;
+        if (r < nr && out != nullptr) {
+          const float l = s_l[r];
+          reinterpret_cast<float4*>(out_row(r))[d4] = make_float4(t.x / l, t.y / l, t.z / l, t.w / l);
+        } else if (r < nr) {
+          reinterpret_cast<float4*>(po + ((rowbase + r) * nsplit + split) * hd)[d4] = t;
+        }
       }
     }
   }
@@ -474,7 +498,8 @@ AttnLayout attn_layout(int B, int n, int H, int Hkv, int hd, int Lmax) {
   AttnLayout L{};
   const int R = (H / Hkv) * n;
   L.rgroups = ceil_div(R, kMaxRowsWg);
-  L.chunk = kTile * std::max(1, ceil_div(ceil_div(Lmax, kTile), kMaxSplits));
+  L.chunk = Lmax <= kDirectMax ? ceil_div(Lmax, kTile) * kTile
+                               : kTile * std::max(1, ceil_div(ceil_div(Lmax, kTile), kMaxSplits));
   L.nsplit = ceil_div(Lmax, L.chunk);
   const size_t rows = (size_t)B * Hkv * R;
   Carve c;
@@ -496,21 +521,23 @@ hipError_t launch_attn_kv(const float* q, const uint16_t* k_new, const uint16_t*
   float* po = reinterpret_cast<float*>(ws + L.po);
   const float scale = (float)(1.0 / sqrt((double)hd));
   const dim3 grid(L.nsplit, Hkv * L.rgroups, B);
+  const bool direct = L.nsplit == 1;  // the partial kernel writes the output; no merge
   {
     ProfScope prof("attn_partial", stream);
     if (R > 16)
       klaunch(attn_partial_kernel<true>, grid, kAttnThreads, 0, stream, 
           q, reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new),
           reinterpret_cast<uint4*>(k_cache), reinterpret_cast<uint4*>(v_cache), cache_pos, n, H,
-          Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po);
+          Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po, direct ? out : nullptr);
     else
       klaunch(attn_partial_kernel<false>, grid, kAttnThreads, 0, stream, 
           q, reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new),
           reinterpret_cast<uint4*>(k_cache), reinterpret_cast<uint4*>(v_cache), cache_pos, n, H,
-          Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po);
+          Hkv, hd, Lmax, L.chunk, L.rgroups, R, scale, pm, pl, po, direct ? out : nullptr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (direct) return hipSuccess;
   ProfScope prof("attn_combine", stream);
   klaunch(attn_combine_kernel, B * Hkv * R, kMaxHd, 0, stream, n, H, Hkv, hd, R, L.nsplit, pm, pl, po,
                                                           out);
