@@ -202,13 +202,13 @@ __device__ __forceinline__ void merge_rows(int b, int R, int Kd, int splits, flo
   const int S2 = 1 << lg, rpp = kWave >> lg;
   const int sub = lane & (S2 - 1), rsub = lane >> lg;
   const int npass = (R + rpp - 1) / rpp;
-  for (int p0 = wave; p0 < npass; p0 += 2 * nw) {
-    // two passes per iteration, both passes' loads issued before either merge
-    Stat a[2];
-    float lt[2];
-    int j[2];
+  constexpr int kPB = 2;  // passes per iteration, all their loads issued before any merge
+  for (int p0 = wave; p0 < npass; p0 += kPB * nw) {
+    Stat a[kPB];
+    float lt[kPB];
+    int j[kPB];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kPB; ++u) {
       j[u] = (p0 + u * nw) * rpp + rsub;
       a[u].m = -INFINITY;
       a[u].s = 0.0;
@@ -225,7 +225,7 @@ __device__ __forceinline__ void merge_rows(int b, int R, int Kd, int splits, flo
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kPB; ++u) {
       for (int msk = 1; msk < S2; msk <<= 1) {
         const Stat o = stat_shfl_xor(a[u], msk);
         stat_merge(a[u], o, c);
@@ -282,8 +282,11 @@ __global__ __launch_bounds__(kScanThreads) void tree_scan_kernel(
   __shared__ int s_path[kMaxRows];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int KW = K * W, R = KW + (bonus ? W : 0);
-  for (int j = tid; j < KW; j += blockDim.x) s_par[j] = parents[(size_t)b * KW + j];
+  // the parent links are requested before the merge's loads and stored after it (KW <= 1024,
+  // one per thread), so both round trips overlap
+  const int par = tid < KW ? parents[(size_t)b * KW + tid] : 0;
   merge_rows(b, R, KW, splits, c, pm, ps, pbv, pbi, pd, s_q, s_amax, q_out);
+  if (tid < KW) s_par[tid] = par;
   __syncthreads();
   if (tid < kWave) {  // wave 0: lane w walks leaf w's path (W <= 64)
     int adv = K, w = tid;
