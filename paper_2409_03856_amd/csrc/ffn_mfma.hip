@@ -41,6 +41,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "ring.h"
 
 namespace sirius {
 namespace {
@@ -255,18 +256,6 @@ static_assert(kRgLoads == 4, "the wait counts below assume four loads per thread
 
 __device__ __forceinline__ int rg_pos(int row, int chunk) { return chunk ^ (row & 7); }
 
-// vmcnt(n) with the other counters left alone (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Workgroup barrier without the release fence of __syncthreads(), which would wait for every
-// direct-to-LDS load still in flight. The ring's own wait counts make this wave's loads of the
-// block complete before it; LDS needs no cache maintenance, and every ds_read of the previous
-// block has been consumed by its MFMA before the barrier in program order. The memory clobber
-// keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void ring_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 __global__ __launch_bounds__(kRgThreads) void gate_up_ring_kernel(
     const uint16_t* __restrict__ xb, const uint16_t* __restrict__ wg,
