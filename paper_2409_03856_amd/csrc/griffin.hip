@@ -4,8 +4,7 @@
 //                         T prompt tokens: both products in one MFMA pass
 //                         (v_mfma_f32_16x16x32_bf16, exact bf16 products, fp32
 //                         accumulation). Workgroup tile 128 tokens x 64 neurons,
-//                         K staged through LDS in double-buffered 32-wide slices
-//                         (XOR-swizzled 64-byte rows);
+//                         K staged through LDS in double-buffered 32-wide slices;
 //                         the token tiles of a neuron tile run on one XCD together so
 //                         its weights are read from HBM once. For the plain statistic
 //                         the epilogue writes only per-tile sums of z^2 (fp64); the
@@ -32,17 +31,11 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 constexpr int kGT = 128;           // tokens per workgroup tile
 constexpr int kGN = 64;            // neurons per workgroup tile
 constexpr int kGK = 32;            // K slice per LDS stage
-constexpr int kLdsRow = kGK;       // LDS row (bf16 elements): 64 bytes, chunks XOR-swizzled
+constexpr int kLdsRow = kGK + 8;   // padded LDS row (bf16 elements) against bank conflicts
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkPer = 64;       // scores per top-k thread at most: d_ff <= 65536
 
 __device__ __forceinline__ int ceil_div_dev(int a, int b) { return (a + b - 1) / b; }
-
-// Element offset of 16-byte chunk c (8 bf16) of LDS row r: chunk c sits at position
-// c ^ ((r / 2) % 4) of the row's four, so the MFMA operand reads of 16 rows at one chunk and the
-// staging writes of 16 rows x 4 chunks touch the banks evenly (a padded row pitch left 29M
-// bank-conflict cycles per call in the hardware counters).
-__device__ __forceinline__ int lds_at(int r, int c) { return r * kLdsRow + 8 * (c ^ ((r >> 1) & 3)); }
 
 // 16-byte chunk (8 bf16) of row r at column k, zero outside the matrix.
 __device__ __forceinline__ uint4 load_chunk(const uint16_t* base, int rows, int d, int r, int k) {
@@ -107,10 +100,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int c = tid + 256 * j;
-      *reinterpret_cast<uint4*>(&sX[buf][lds_at(c >> 2, c & 3)]) = st.x[j];
+      *reinterpret_cast<uint4*>(&sX[buf][(c >> 2) * kLdsRow + 8 * (c & 3)]) = st.x[j];
     }
-    *reinterpret_cast<uint4*>(&sG[buf][lds_at(tid >> 2, tid & 3)]) = st.g;
-    *reinterpret_cast<uint4*>(&sU[buf][lds_at(tid >> 2, tid & 3)]) = st.u;
+    *reinterpret_cast<uint4*>(&sG[buf][(tid >> 2) * kLdsRow + 8 * (tid & 3)]) = st.g;
+    *reinterpret_cast<uint4*>(&sU[buf][(tid >> 2) * kLdsRow + 8 * (tid & 3)]) = st.u;
   };
 
   floatx4_t accg[4][2], accu[4][2];
@@ -121,16 +114,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
       accg[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
       accu[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     }
-  const int fr = lane & 15, fc = lane >> 4;  // fragment row and 16-byte chunk
+  const int fr = lane & 15, fk = 8 * (lane >> 4);  // fragment row and k offset
   auto compute = [&](int buf) {
     bf16x8_t a[4], bg[2], bu[2];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
-      a[mt] = *reinterpret_cast<const bf16x8_t*>(&sX[buf][lds_at(wm * 64 + mt * 16 + fr, fc)]);
+      a[mt] = *reinterpret_cast<const bf16x8_t*>(&sX[buf][(wm * 64 + mt * 16 + fr) * kLdsRow + fk]);
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      bg[nt] = *reinterpret_cast<const bf16x8_t*>(&sG[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
-      bu[nt] = *reinterpret_cast<const bf16x8_t*>(&sU[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
+      bg[nt] = *reinterpret_cast<const bf16x8_t*>(&sG[buf][(wn * 32 + nt * 16 + fr) * kLdsRow + fk]);
+      bu[nt] = *reinterpret_cast<const bf16x8_t*>(&sU[buf][(wn * 32 + nt * 16 + fr) * kLdsRow + fk]);
     }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
