@@ -4,7 +4,8 @@
 //                         T prompt tokens: both products in one MFMA pass
 //                         (v_mfma_f32_16x16x32_bf16, exact bf16 products, fp32
 //                         accumulation). Workgroup tile 128 tokens x 64 neurons,
-//                         K staged through LDS in double-buffered 32-wide slices;
+//                         K staged through LDS in double-buffered 32-wide slices
+//                         (XOR-swizzled 64-byte rows), four workgroups per CU;
 //                         the token tiles of a neuron tile run on one XCD together so
 //                         its weights are read from HBM once. For the plain statistic
 //                         the epilogue writes only per-tile sums of z^2 (fp64); the
@@ -31,11 +32,18 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 constexpr int kGT = 128;           // tokens per workgroup tile
 constexpr int kGN = 64;            // neurons per workgroup tile
 constexpr int kGK = 32;            // K slice per LDS stage
-constexpr int kLdsRow = kGK + 8;   // padded LDS row (bf16 elements) against bank conflicts
+constexpr int kLdsRow = kGK;       // LDS row (bf16 elements): 64 bytes, chunks XOR-swizzled
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkPer = 64;       // scores per top-k thread at most: d_ff <= 65536
 
 __device__ __forceinline__ int ceil_div_dev(int a, int b) { return (a + b - 1) / b; }
+
+// Element offset of 16-byte chunk c (8 bf16) of LDS row r: chunk c sits at position
+// c ^ ((r / 2) % 4) of the row's four, so the MFMA operand reads of 16 rows at one chunk and the
+// staging writes of 16 rows x 4 chunks touch the banks evenly (a padded row pitch left 29M
+// bank-conflict cycles per call in the hardware counters). The unpadded rows are also what
+// lets four workgroups share a CU's LDS (33 KiB each against 42 KiB padded).
+__device__ __forceinline__ int lds_at(int r, int c) { return r * kLdsRow + 8 * (c ^ ((r >> 1) & 3)); }
 
 // 16-byte chunk (8 bf16) of row r at column k, zero outside the matrix.
 __device__ __forceinline__ uint4 load_chunk(const uint16_t* base, int rows, int d, int r, int k) {
@@ -63,10 +71,13 @@ __device__ __forceinline__ void tile_of(int id, int ntn, int ntm, int* n_tile, i
 // Z tile (Z != nullptr) or, for the plain statistic, the tile's partial sums of z^2 over its
 // tokens per neuron (part[m_tile][n], fp64) without storing Z. Tile kGT tokens x kGN neurons,
 // four waves in a 2 x 2 layout, each wave 64 tokens x 32 neurons of both products; K in
-// slices of kGK staged through double-buffered LDS. The global loads of slice s + 2 are issued
-// while slice s is multiplied (two register sets), so each load has two slices of MFMA work
-// to arrive in: with one, every slice waited for its loads.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
+// slices of kGK staged through double-buffered LDS, the global loads of slice s + 1 issued
+// before slice s is multiplied. Occupancy is what sets its pace: at 126 VGPRs and 33 KiB of LDS
+// four workgroups share a CU, so the 896 tiles of a 512-token prompt at d_ff = 14336 run in one
+// round of the chip's 1024 slots. Loading two slices ahead needs a second register set, which
+// leaves room for three workgroups per CU only, and the 128 tiles past the first 768 then run
+// as a second, mostly empty round (about 225 us against 183 us).
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
                                                         const uint16_t* __restrict__ Wg,
                                                         const uint16_t* __restrict__ Wu, int d,
                                                         int F, float* __restrict__ Z,
@@ -100,10 +111,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int c = tid + 256 * j;
-      *reinterpret_cast<uint4*>(&sX[buf][(c >> 2) * kLdsRow + 8 * (c & 3)]) = st.x[j];
+      *reinterpret_cast<uint4*>(&sX[buf][lds_at(c >> 2, c & 3)]) = st.x[j];
     }
-    *reinterpret_cast<uint4*>(&sG[buf][(tid >> 2) * kLdsRow + 8 * (tid & 3)]) = st.g;
-    *reinterpret_cast<uint4*>(&sU[buf][(tid >> 2) * kLdsRow + 8 * (tid & 3)]) = st.u;
+    *reinterpret_cast<uint4*>(&sG[buf][lds_at(tid >> 2, tid & 3)]) = st.g;
+    *reinterpret_cast<uint4*>(&sU[buf][lds_at(tid >> 2, tid & 3)]) = st.u;
   };
 
   floatx4_t accg[4][2], accu[4][2];
@@ -114,16 +125,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
       accg[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
       accu[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     }
-  const int fr = lane & 15, fk = 8 * (lane >> 4);  // fragment row and k offset
+  const int fr = lane & 15, fc = lane >> 4;  // fragment row and 16-byte chunk
   auto compute = [&](int buf) {
     bf16x8_t a[4], bg[2], bu[2];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
-      a[mt] = *reinterpret_cast<const bf16x8_t*>(&sX[buf][(wm * 64 + mt * 16 + fr) * kLdsRow + fk]);
+      a[mt] = *reinterpret_cast<const bf16x8_t*>(&sX[buf][lds_at(wm * 64 + mt * 16 + fr, fc)]);
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      bg[nt] = *reinterpret_cast<const bf16x8_t*>(&sG[buf][(wn * 32 + nt * 16 + fr) * kLdsRow + fk]);
-      bu[nt] = *reinterpret_cast<const bf16x8_t*>(&sU[buf][(wn * 32 + nt * 16 + fr) * kLdsRow + fk]);
+      bg[nt] = *reinterpret_cast<const bf16x8_t*>(&sG[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
+      bu[nt] = *reinterpret_cast<const bf16x8_t*>(&sU[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
     }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
@@ -135,24 +146,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
   };
 
   const int nk = (d + kGK - 1) / kGK;
-  Stage s0, s1;  // register sets of slices 2j and 2j + 1
+  Stage s0;  // registers of slice ks + 1 while slice ks is multiplied
   gload(0, s0);
-  if (nk > 1) gload(kGK, s1);
   sstore(s0, 0);
   __syncthreads();
-  // slice ks: its loads went into set ks % 2; this set is reloaded with slice ks + 2 as soon
-  // as it has been stored, and the other set (slice ks + 1) is stored after the MFMAs
-  for (int ks = 0; ks < nk; ks += 2) {
-    if (ks + 2 < nk) gload((ks + 2) * kGK, s0);
-    compute(0);
-    if (ks + 1 < nk) sstore(s1, 1);
+  for (int ks = 0; ks < nk; ++ks) {
+    if (ks + 1 < nk) gload((ks + 1) * kGK, s0);
+    compute(ks & 1);
+    if (ks + 1 < nk) sstore(s0, (ks + 1) & 1);
     __syncthreads();
-    if (ks + 1 < nk) {  // uniform over the block
-      if (ks + 3 < nk) gload((ks + 3) * kGK, s1);
-      compute(1);
-      if (ks + 2 < nk) sstore(s0, 0);
-      __syncthreads();
-    }
   }
 
   // C layout: lane holds column (neuron) lane % 16 and rows (tokens) 4*(lane/16) + i.
