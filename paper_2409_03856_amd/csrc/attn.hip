@@ -24,9 +24,9 @@
 //                       most 256 rows is one chunk per workgroup (its tiles in turn), and the
 //                       kernel writes the normalised output itself: no merge launch.
 //  attn_combine_kernel  one workgroup per query row: the chunks' (max, sum) and their first
-//                       outputs requested together, the weights exp(m_c - M) (one chunk per
-//                       thread), then each thread sums its output column over the chunks in
-//                       order.
+//                       outputs (all of them, up to 64 chunks) requested together, the
+//                       weights exp(m_c - M) (one chunk per thread), then each thread sums
+//                       its output column over the chunks in order.
 //  kv_rollback_kernel   cache_pos[b] += min(accept_len[b] + 1, n).
 #include <math.h>
 
@@ -48,6 +48,7 @@ constexpr int kMaxOB = 2;                 // 4 x 4 output blocks per thread: 64 
 constexpr int kStagePer = kTile * kMaxHd / 8 / kAttnThreads;  // 16-byte loads per thread and tile
 constexpr int kMaxSplits = 256;           // position chunks per call at most
 constexpr int kDirectMax = 256;           // caches up to this many rows: one chunk, no combine
+constexpr int kOneBatchMax = 64;          // merges of at most this many chunks: one load batch
 
 // BIG: up to 64 rows, scores in 4 x 4 register blocks; else up to 16 rows, each score's dot
 // product split over four lanes. Keys and values are staged as bf16; the score tile reuses
@@ -402,8 +403,9 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 // chunks in order, the next batch requested before the current one is added. Chunks with no
 // visible position never write their outputs: those are read but replaced by 0 (a select, so
 // whatever the buffer holds there cannot reach the sum). NB chunk outputs are requested per
-// batch: 32 for long caches, 8 when there are at most 8 chunks (the small decoder's), where
-// unrolled guards for 32 would cost more than they save.
+// batch: 8 when there are at most 8 chunks (the small decoder's), where unrolled guards for
+// more would cost more than they save; all of them, in one batch and one memory round trip,
+// up to 64 chunks (a 4096-row cache); else 32 per batch.
 template <int NB>
 __device__ __forceinline__ void combine_row(int n, int H, int Hkv, int hd, int R, int nsplit,
                                             const float* __restrict__ pm,
@@ -417,6 +419,7 @@ __device__ __forceinline__ void combine_row(int n, int H, int Hkv, int hd, int R
   const float* m = pm + (size_t)row * nsplit;
   const float* l = pl + (size_t)row * nsplit;
   const float* o = po + (size_t)row * nsplit * hd + (tid < hd ? tid : 0);
+  constexpr bool kOneBatch = NB == kOneBatchMax;  // every chunk's output in the first batch
   constexpr int kPer = kMaxSplits / kMaxHd;  // chunks per thread for the max and the weights
   static_assert(kMaxSplits % kMaxHd == 0, "whole chunks per thread");
   float mv[kPer], lv[kPer];
@@ -458,8 +461,10 @@ __device__ __forceinline__ void combine_row(int n, int H, int Hkv, int hd, int R
   for (int s0 = 0; s0 < nsplit; s0 += NB) {
     float nx[NB];
     const int s1 = s0 + NB;
+    if constexpr (!kOneBatch) {
 #pragma unroll
-    for (int u = 0; u < NB; ++u) nx[u] = s1 + u < nsplit ? o[(size_t)(s1 + u) * hd] : 0.f;
+      for (int u = 0; u < NB; ++u) nx[u] = s1 + u < nsplit ? o[(size_t)(s1 + u) * hd] : 0.f;
+    }
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
       if (s0 + u < nsplit) {
@@ -467,8 +472,10 @@ __device__ __forceinline__ void combine_row(int n, int H, int Hkv, int hd, int R
         num = fmaf(w > 0.f ? ov[u] : 0.f, w, num);
       }
     }
+    if constexpr (!kOneBatch) {
 #pragma unroll
-    for (int u = 0; u < NB; ++u) ov[u] = nx[u];
+      for (int u = 0; u < NB; ++u) ov[u] = nx[u];
+    }
   }
   if (tid < hd) out[(((size_t)b * n + i) * H + h) * hd + tid] = num / den;
 }
@@ -479,6 +486,8 @@ __global__ __launch_bounds__(kMaxHd) void attn_combine_kernel(
   __shared__ float s_w[kMaxSplits], s_red[kMaxHd / kWave];
   if (nsplit <= 8)
     combine_row<8>(n, H, Hkv, hd, R, nsplit, pm, pl, po, out, s_w, s_red);
+  else if (nsplit <= kOneBatchMax)
+    combine_row<kOneBatchMax>(n, H, Hkv, hd, R, nsplit, pm, pl, po, out, s_w, s_red);
   else
     combine_row<32>(n, H, Hkv, hd, R, nsplit, pm, pl, po, out, s_w, s_red);
 }
