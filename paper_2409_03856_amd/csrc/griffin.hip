@@ -76,7 +76,7 @@ __device__ __forceinline__ void tile_of(int id, int ntn, int ntm, int* n_tile, i
 // four workgroups share a CU, so the 896 tiles of a 512-token prompt at d_ff = 14336 run in one
 // round of the chip's 1024 slots. Loading two slices ahead needs a second register set, which
 // leaves room for three workgroups per CU only, and the 128 tiles past the first 768 then run
-// as a second, mostly empty round (about 225 us against 183 us).
+// as a second, mostly empty round (about 225 us against 180 us).
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
                                                         const uint16_t* __restrict__ Wg,
                                                         const uint16_t* __restrict__ Wu, int d,
