@@ -3,9 +3,10 @@
 //  griffin_z_kernel       z[t, i] = SiLU(x_t . W_gate[i]) * (x_t . W_up[i]) for the
 //                         T prompt tokens: both products in one MFMA pass
 //                         (v_mfma_f32_16x16x32_bf16, exact bf16 products, fp32
-//                         accumulation). Workgroup tile 128 tokens x 64 neurons,
-//                         K staged through LDS in double-buffered 32-wide slices
-//                         (XOR-swizzled 64-byte rows), four workgroups per CU;
+//                         accumulation). Workgroup tile 128 tokens x 128 neurons
+//                         (eight waves), K staged through LDS in double-buffered
+//                         32-wide slices (XOR-swizzled 64-byte rows), two slices in
+//                         flight, two workgroups per CU;
 //                         the token tiles of a neuron tile run on one XCD together so
 //                         its weights are read from HBM once. For the plain statistic
 //                         the epilogue writes only per-tile sums of z^2 (fp64); the
@@ -30,7 +31,8 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 
 constexpr int kGT = 128;           // tokens per workgroup tile
-constexpr int kGN = 64;            // neurons per workgroup tile
+constexpr int kGN = 128;           // neurons per workgroup tile
+constexpr int kGThreads = 512;     // eight waves: 2 (tokens) x 4 (neurons) wave tiles
 constexpr int kGK = 32;            // K slice per LDS stage
 constexpr int kLdsRow = kGK;       // LDS row (bf16 elements): 64 bytes, chunks XOR-swizzled
 constexpr int kTopkThreads = 1024;
@@ -41,8 +43,7 @@ __device__ __forceinline__ int ceil_div_dev(int a, int b) { return (a + b - 1) /
 // Element offset of 16-byte chunk c (8 bf16) of LDS row r: chunk c sits at position
 // c ^ ((r / 2) % 4) of the row's four, so the MFMA operand reads of 16 rows at one chunk and the
 // staging writes of 16 rows x 4 chunks touch the banks evenly (a padded row pitch left 29M
-// bank-conflict cycles per call in the hardware counters). The unpadded rows are also what
-// lets four workgroups share a CU's LDS (33 KiB each against 42 KiB padded).
+// bank-conflict cycles per call in the hardware counters).
 __device__ __forceinline__ int lds_at(int r, int c) { return r * kLdsRow + 8 * (c ^ ((r >> 1) & 3)); }
 
 // 16-byte chunk (8 bf16) of row r at column k, zero outside the matrix.
@@ -70,14 +71,17 @@ __device__ __forceinline__ void tile_of(int id, int ntn, int ntm, int* n_tile, i
 
 // Z tile (Z != nullptr) or, for the plain statistic, the tile's partial sums of z^2 over its
 // tokens per neuron (part[m_tile][n], fp64) without storing Z. Tile kGT tokens x kGN neurons,
-// four waves in a 2 x 2 layout, each wave 64 tokens x 32 neurons of both products; K in
-// slices of kGK staged through double-buffered LDS, the global loads of slice s + 1 issued
-// before slice s is multiplied. Occupancy is what sets its pace: at 126 VGPRs and 33 KiB of LDS
-// four workgroups share a CU, so the 896 tiles of a 512-token prompt at d_ff = 14336 run in one
-// round of the chip's 1024 slots. Loading two slices ahead needs a second register set, which
-// leaves room for three workgroups per CU only, and the 128 tiles past the first 768 then run
-// as a second, mostly empty round (about 225 us against 180 us).
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
+// eight waves in a 2 x 4 layout, each wave 64 tokens x 32 neurons of both products; K in
+// slices of kGK staged through double-buffered LDS, each thread moving one 16-byte chunk of
+// X, W_gate and W_up per slice. The global loads of slice s + 2 are issued while slice s is
+// multiplied (two register sets), so each load has two slices of MFMA work to arrive in.
+// Occupancy and loads in flight set its pace: at 128 VGPRs and 50 KiB of LDS two workgroups
+// share a CU, so the 448 tiles of a 512-token prompt at d_ff = 14336 run in one round of the
+// chip's 512 slots, with 96 KiB in flight per CU. (Four-wave 128 x 64 tiles: at two slices
+// ahead three workgroups fit per CU and 128 of the 896 tiles run as a second, mostly empty
+// round, about 225 us; at one slice ahead four fit, one round, about 183 us; this layout about
+// 168 us.)
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(4))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
                                                         const uint16_t* __restrict__ Wg,
                                                         const uint16_t* __restrict__ Wu, int d,
                                                         int F, float* __restrict__ Z,
@@ -91,28 +95,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void g
   int n_tile, m_tile;
   tile_of(blockIdx.x, ceil_div_dev(F, kGN), ceil_div_dev(T, kGT), &n_tile, &m_tile);
   const int t0 = m_tile * kGT, n0 = n_tile * kGN;
-  const int wm = wave >> 1, wn = wave & 1;  // wave tile: 64 tokens x 32 neurons
+  const int wm = wave >> 2, wn = wave & 3;  // wave tile: 64 tokens x 32 neurons
 
   // global -> LDS per slice: X 128 rows x 4 chunks of 16 bytes (two per thread), W_gate and
   // W_up 64 rows x 4 chunks (one each per thread)
   struct Stage {
-    uint4 x[2], g, u;
+    uint4 x, g, u;
   };
   auto gload = [&](int k0, Stage& st) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int c = tid + 256 * j;
-      st.x[j] = load_chunk(X, T, d, t0 + (c >> 2), k0 + 8 * (c & 3));
-    }
+    st.x = load_chunk(X, T, d, t0 + (tid >> 2), k0 + 8 * (tid & 3));
     st.g = load_chunk(Wg, F, d, n0 + (tid >> 2), k0 + 8 * (tid & 3));
     st.u = load_chunk(Wu, F, d, n0 + (tid >> 2), k0 + 8 * (tid & 3));
   };
   auto sstore = [&](const Stage& st, int buf) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int c = tid + 256 * j;
-      *reinterpret_cast<uint4*>(&sX[buf][lds_at(c >> 2, c & 3)]) = st.x[j];
-    }
+    *reinterpret_cast<uint4*>(&sX[buf][lds_at(tid >> 2, tid & 3)]) = st.x;
     *reinterpret_cast<uint4*>(&sG[buf][lds_at(tid >> 2, tid & 3)]) = st.g;
     *reinterpret_cast<uint4*>(&sU[buf][lds_at(tid >> 2, tid & 3)]) = st.u;
   };
@@ -146,15 +142,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void g
   };
 
   const int nk = (d + kGK - 1) / kGK;
-  Stage s0;  // registers of slice ks + 1 while slice ks is multiplied
+  Stage s0, s1;  // register sets of slices 2j and 2j + 1
   gload(0, s0);
+  if (nk > 1) gload(kGK, s1);
   sstore(s0, 0);
   __syncthreads();
-  for (int ks = 0; ks < nk; ++ks) {
-    if (ks + 1 < nk) gload((ks + 1) * kGK, s0);
-    compute(ks & 1);
-    if (ks + 1 < nk) sstore(s0, (ks + 1) & 1);
+  // slice ks: its loads went into set ks % 2; this set is reloaded with slice ks + 2 as soon
+  // as it has been stored, and the other set (slice ks + 1) is stored after the MFMAs
+  for (int ks = 0; ks < nk; ks += 2) {
+    if (ks + 2 < nk) gload((ks + 2) * kGK, s0);
+    compute(0);
+    if (ks + 1 < nk) sstore(s1, 1);
     __syncthreads();
+    if (ks + 1 < nk) {  // uniform over the block
+      if (ks + 3 < nk) gload((ks + 3) * kGK, s1);
+      compute(1);
+      if (ks + 2 < nk) sstore(s0, 0);
+      __syncthreads();
+    }
   }
 
   // C layout: lane holds column (neuron) lane % 16 and rows (tokens) 4*(lane/16) + i.
@@ -397,7 +402,7 @@ hipError_t launch_griffin(const uint16_t* xp, int T, const uint16_t* wg, const u
   hipError_t e;
   {
     ProfScope prof("griffin_z", stream);
-    klaunch(griffin_z_kernel, ntn * ntm, 256, 0, stream, xp, T, wg, wu, d, F, Z, part);
+    klaunch(griffin_z_kernel, ntn * ntm, kGThreads, 0, stream, xp, T, wg, wu, d, F, Z, part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   float* sc = scores_out != nullptr ? scores_out : scores;
