@@ -53,6 +53,13 @@ def test_ragged(sr):
     _check(sr, 3, 1, 8, 5, 2, 0.5)
 
 
+@pytest.mark.parametrize("normalize", [False, True])
+def test_several_ragged_tiles(sr, normalize):
+    # three token tiles of 128 (the last ragged), nine neuron tiles of 128 (eight placed one per
+    # XCD and one left over, the last ragged), and a K tail of 8 past the last 32-wide slice
+    _check(sr, 7, 300, 520, 1100, 400, 1.0 / np.sqrt(520), normalize=normalize)
+
+
 def test_normalized_variant(sr):
     _check(sr, 4, 70, 256, 688, 300, TINY.weight_std, normalize=True)
 
