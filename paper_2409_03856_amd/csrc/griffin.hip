@@ -97,8 +97,8 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(4))) 
   const int t0 = m_tile * kGT, n0 = n_tile * kGN;
   const int wm = wave >> 2, wn = wave & 3;  // wave tile: 64 tokens x 32 neurons
 
-  // global -> LDS per slice: X 128 rows x 4 chunks of 16 bytes (two per thread), W_gate and
-  // W_up 64 rows x 4 chunks (one each per thread)
+  // global -> LDS per slice: X, W_gate and W_up 128 rows x 4 chunks of 16 bytes each, one chunk
+  // of each per thread
   struct Stage {
     uint4 x, g, u;
   };
