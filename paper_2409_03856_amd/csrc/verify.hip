@@ -27,7 +27,7 @@ namespace {
 
 constexpr int kVerifyThreads = 256;
 constexpr int kMinSegment = 2048;    // logits per workgroup at least
-constexpr int kTargetBlocks = 2048;  // enough workgroups to cover 256 CUs several times
+constexpr int kTargetBlocks = 512;   // two workgroups per CU, each streaming several passes
 constexpr int kMaxRows = 1024;       // R limit of the scan kernel
 constexpr int kChunk = 8;            // float4 loads in flight per stats thread
 constexpr int kScanThreads = 1024;   // scan workgroup: 16 waves
