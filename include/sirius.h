@@ -32,7 +32,7 @@
  *    call has launched nothing. sirius_last_error() returns a message for
  *    the calling thread's most recent failure.
  *  - B == 0 (empty batch) is a valid no-op that returns SIRIUS_OK.
- *  - Limits of this build: 8 <= d_model <= 8192, 1 <= d_ff <= 65536,
+ *  - Limits of this library: 8 <= d_model <= 8192, 1 <= d_ff <= 65536,
  *    B <= 64 for the FFN entry points.
  */
 #ifndef SIRIUS_H
