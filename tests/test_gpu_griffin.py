@@ -80,3 +80,33 @@ def test_llama3_8b_prompt512(sr):
     nb = _check(sr, 6, 512, LLAMA3_8B.d_model, LLAMA3_8B.d_ff, LLAMA3_8B.d_ff // 2, LLAMA3_8B.weight_std,
                 decode_b=1)
     say(f"8B griffin boundary neurons: {nb}")
+
+
+def test_long_prompt_full_width_sampled(sr):
+    """A 2000-token prompt at Llama-3-8B FFN width: 16 token tiles of 128 (the last ragged) over
+    112 neuron tiles. The oracle recomputes 64 sampled neurons' scores from their own rows; the
+    selection must be exactly the top-k of the returned scores (equal scores: lower index), and
+    sampled condensed rows must be the selected rows."""
+    import torch
+    d, f, t_n = LLAMA3_8B.d_model, LLAMA3_8B.d_ff, 2000
+    k = f // 2
+    say(f"griffin T={t_n} d={d} f={f} k={k} (sampled)")
+    ws = []
+    for m in range(3):
+        w = torch.empty((f, d), dtype=torch.bfloat16, device="cuda")
+        sr.sirius_fill_normal_bf16(w, 9100 + m, 0.0, LLAMA3_8B.weight_std)
+        ws.append(w)
+    xp = griffin_prompt(9103, t_n, d)
+    sel, scores, wgc, wuc, wdc = sr.sirius_griffin_select(dev_bf16(xp), *ws, k)
+    sel, scores = host(sel).astype(np.int64), host(scores)
+    np.testing.assert_array_equal(sel, oracle.griffin_topk(scores, k))
+    rng = np.random.default_rng(9104)
+    idx = np.sort(rng.choice(f, 64, replace=False))
+    rows = torch.from_numpy(idx).cuda()
+    s_ref = oracle.griffin_scores(xp, host(ws[0][rows]), host(ws[1][rows]))
+    np.testing.assert_allclose(scores[idx], s_ref, rtol=2e-5, atol=1e-30)
+    j = np.sort(rng.choice(k, 16, replace=False))
+    src = torch.from_numpy(sel[j]).cuda()
+    dst = torch.from_numpy(j).cuda()
+    for w, c in zip(ws, (wgc, wuc, wdc)):
+        assert torch.equal(c[dst], w[src])
