@@ -14,9 +14,14 @@ __device__ __forceinline__ void wait_vm() {
 
 // Workgroup barrier without the release fence of __syncthreads(), which would wait for every
 // direct-to-LDS load still in flight. The ring's own wait counts make this wave's loads of the
-// block complete before it; LDS needs no cache maintenance, and every ds_read of the previous
-// block has been consumed by its MFMA before the barrier in program order. The memory clobber
-// keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void ring_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// block complete before it; LDS needs no cache maintenance. The lgkmcnt(0) wait makes every
+// ds_read this wave issued (of the slot about to be refilled) return its data to registers
+// before the barrier, whatever the compiler did with the instructions that consume them: an
+// MFMA is not a memory operation, so it (and the wait the compiler places for its operands)
+// may be scheduled below the asm. vmcnt is left alone, so the ring's loads stay in flight. The
+// memory clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 }  // namespace sirius

@@ -102,3 +102,20 @@ def test_llama3_8b_verify_chunk(sr):
     e, nb = check_ffn_rounded_norm(y, xn, wg, wu, wd, resid=res)
     say(f"  error vs precision-matched oracle: {e:.2e} x RMS ({nb} inputs with ambiguous rounding)")
     assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
+
+
+@pytest.mark.parametrize("bsz", [64, 40])
+def test_llama3_8b_tree_pass(sr, bsz):
+    """The full model's pass over a drafted tree of about 64 nodes (kernel size 16 x width 4, the
+    paper's hardware-friendly tree) on one Llama-3-8B-shaped FFN layer, with RMSNorm and residual:
+    four (or a ragged two and a half) 16-token MFMA tiles over the full 4096 x 14336 layer."""
+    d, f = LLAMA3_8B.d_model, LLAMA3_8B.d_ff
+    say(f"8B dense mfma B={bsz}")
+    (wg, wu, wd), W = _layer(910 + bsz, d, f, LLAMA3_8B.weight_std)
+    x = decode_inputs(910 + bsz, bsz, d)
+    res = decode_inputs(911 + bsz, bsz, d)
+    y = host(sr.sirius_ffn_dense(dev_f32(x), *W, norm_eps=1e-5, resid=dev_f32(res)))
+    xn = oracle.rmsnorm(x, 1e-5)
+    e, nb = check_ffn_rounded_norm(y, xn, wg, wu, wd, resid=res)
+    say(f"  error vs precision-matched oracle: {e:.2e} x RMS ({nb} inputs with ambiguous rounding)")
+    assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL

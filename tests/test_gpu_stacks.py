@@ -183,6 +183,25 @@ def test_llama3_8b_dense_verify_chunk_stack(sr, stack8b):
         say(f"  layer {l}: error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
 
 
+def test_llama3_8b_dense_tree_pass_stack(sr, stack8b):
+    """The full model's pass over a 64-node drafted tree (kernel size 16 x width 4) through all
+    32 dense layers: four 16-token MFMA tiles per layer."""
+    say("8B dense stack B=64")
+    bsz = 64
+    h = dev_f32(decode_inputs(7500, bsz, LLAMA3_8B.d_model))
+    for l, (wg, wu, wd) in enumerate(stack8b.layers):
+        if l not in CHECK_8B:
+            sr.sirius_ffn_dense(h, wg, wu, wd, norm_eps=EPS, resid=h, y=h)
+            continue
+        h_in = host(h).copy()
+        sr.sirius_ffn_dense(h, wg, wu, wd, norm_eps=EPS, resid=h, y=h)
+        hwg, hwu, hwd = stack8b.host_layer(l)
+        xn = oracle.rmsnorm(h_in, EPS)
+        e, nb = check_ffn_rounded_norm(host(h), xn, hwg, hwu, hwd, resid=h_in)
+        say(f"  layer {l}: error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
+    assert np.all(np.isfinite(host(h)))
+
+
 # --------------------------------------------------------------------------------------- 70B
 
 @pytest.fixture(scope="module")
@@ -214,3 +233,18 @@ def test_llama3_70b_dense_verify_chunk_layers(sr, stack70b):
         xn = oracle.rmsnorm(h_in, EPS)
         e, nb = check_ffn_rounded_norm(y, xn, hwg, hwu, hwd, resid=h_in)
         say(f"  error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")
+
+
+@pytest.mark.parametrize("bsz", [32, 64])
+def test_llama3_70b_dense_tree_pass_layer(sr, stack70b, bsz):
+    """The full model's pass over a drafted tree of 32 or 64 nodes on a Llama-3-70B-shaped layer
+    (two or four 16-token MFMA tiles), with RMSNorm and residual."""
+    l = 40
+    say(f"70B dense B={bsz} layer {l}")
+    h_in = decode_inputs(8300 + bsz, bsz, LLAMA3_70B.d_model)
+    wg, wu, wd = stack70b.layers[l]
+    y = host(sr.sirius_ffn_dense(dev_f32(h_in), wg, wu, wd, norm_eps=EPS, resid=dev_f32(h_in)))
+    hwg, hwu, hwd = stack70b.host_layer(l)
+    xn = oracle.rmsnorm(h_in, EPS)
+    e, nb = check_ffn_rounded_norm(y, xn, hwg, hwu, hwd, resid=h_in)
+    say(f"  error {e:.2e} x RMS ({nb} inputs with ambiguous bf16 rounding)")

@@ -9,7 +9,8 @@ import pytest
 
 import oracle
 from synth import tree_build_inputs, tree_verify_inputs, verify_inputs
-from gpu_util import say, dev_f32, dev_i32, host, TREE_SCORE_BAND, VERIFY_BAND, check_tree_build
+from gpu_util import (say, dev_f32, dev_i32, host, TREE_SCORE_BAND, VERIFY_BAND, MAX_BOUNDARY_ROWS,
+                      check_tree_build)
 
 pytestmark = pytest.mark.gpu
 
@@ -125,6 +126,7 @@ def _verify_and_check(sr, lg, tk, pa, r, tau, bonus):
             skipped += 1  # a node's q within the guard band of r: the decision is not determined
             continue
         assert (best[b], acc[b], nxt[b]) == (best_o, acc_o, nxt_o), (b, best[b], acc[b], nxt[b], best_o, acc_o, nxt_o)
+    assert skipped <= MAX_BOUNDARY_ROWS, f"{skipped} trees with a q inside the guard band of r"
     return acc, skipped
 
 

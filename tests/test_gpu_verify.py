@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from synth import verify_inputs, VERIFY_TINY, VERIFY_8B
-from gpu_util import say, dev_f32, dev_i32, host, verify_boundary_rows
+from gpu_util import say, dev_f32, dev_i32, host, verify_boundary_rows, MAX_BOUNDARY_ROWS
 
 pytestmark = pytest.mark.gpu
 
@@ -28,6 +28,7 @@ def _run_and_check(sr, lg, dr, r, tau):
     acc, nxt, p = host(acc), host(nxt), host(p)
     acc_o, nxt_o, q_o = oracle.verify_accept(lg, dr, r, tau)
     skip = set(verify_boundary_rows(q_o, acc_o, r))
+    assert len(skip) <= MAX_BOUNDARY_ROWS, f"{len(skip)} rows inside the guard band of r"
     for b in range(lg.shape[0]):
         if b in skip:
             continue
