@@ -107,6 +107,27 @@ int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * sirius_ffn_cats without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
+ * arguments, semantics and results as sirius_ffn_cats (bit for bit: the same kernels run); the
+ * workspace is a fixed device array of SIRIUS_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends. The call allocates nothing: no hipMalloc, no
+ * hipFree, no events (per-kernel timing is not recorded for it).
+ * All calls on one GPU share that GPU's array: calls that overlap on one GPU (from two streams
+ * or two threads) race and must be ordered by the caller. The array's contents carry over from
+ * call to call; the kernels read only what the same call wrote.
+ * Errors: as sirius_ffn_cats, plus SIRIUS_EWORKSPACE when the call would need more than
+ * SIRIUS_NOALLOC_SCRATCH_BYTES (sirius_workspace_size(SIRIUS_OP_FFN_CATS, ...) tells; every
+ * batch up to 64 at d_model <= 8192 and d_ff <= 28672 fits), SIRIUS_EHIP when the array's device
+ * address cannot be obtained, and SIRIUS_EINVAL for a device index of 64 or more.
+ */
+#define SIRIUS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int sirius_ffn_cats_noalloc(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                            const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                            const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                            void* stream);
+
+/*
  * Per-token top-k sparse FFN, the paper's own fine-grained (FSparse)
  * implementation (Sec. 3, footnote on the fine-grained implementation): in
  * place of CATS's threshold, every token keeps exactly the k neurons of

@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     workspace,
     sirius_ffn_dense,
     sirius_ffn_cats,
+    sirius_ffn_cats_noalloc,
     sirius_ffn_topk,
     sirius_cats_calibrate,
     sirius_griffin_select,

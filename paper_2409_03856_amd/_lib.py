@@ -41,6 +41,7 @@ _Z = ctypes.c_size_t
 SIGNATURES = {
     "sirius_ffn_dense": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
     "sirius_ffn_cats": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "sirius_ffn_cats_noalloc": (_I, [_P, _I, _P, _P, _P, _I, _I, _F, _F, _P, _P, _P, _P, _P]),
     "sirius_ffn_topk": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "sirius_cats_calibrate": (_I, [_P, _I, _P, _I, _I, ctypes.c_double, _P, _P, _Z, _P]),
     "sirius_griffin_select": (_I, [_P, _I, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
@@ -204,6 +205,26 @@ def sirius_ffn_cats(x, w_gate, w_up, w_down, t, *, norm_eps=-1.0, resid=None, y=
     _check(lib().sirius_ffn_cats(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, float(t),
                                  float(norm_eps), _ptr(resid), _ptr(y), _ptr(active_idx), _ptr(active_cnt),
                                  _ptr(ws), ws.numel(), _stream(stream)))
+    return y, active_idx, active_cnt
+
+
+def sirius_ffn_cats_noalloc(x, w_gate, w_up, w_down, t, *, norm_eps=-1.0, resid=None, y=None, active_idx=None,
+                            active_cnt=None, want_active=True, stream=None):
+    """sirius_ffn_cats on the library's fixed device scratch (no workspace). Returns (y, active_idx,
+    active_cnt) as sirius_ffn_cats; pass y and the lists to allocate nothing here either."""
+    torch = _torch()
+    d, f = _w_dims(w_gate, w_up, w_down)
+    _need(x.dtype == torch.float32 and x.dim() == 2 and x.shape[1] == d, "x must be fp32 [B, d_model]")
+    bsz = int(x.shape[0])
+    if y is None:
+        y = torch.empty_like(x)
+    if want_active and active_idx is None:
+        active_idx = torch.empty((bsz, f), dtype=torch.int32, device=x.device)
+        active_cnt = torch.empty((bsz,), dtype=torch.int32, device=x.device)
+    _dev_check(x, w_gate, w_up, w_down, resid, y, active_idx, active_cnt)
+    _check(lib().sirius_ffn_cats_noalloc(_ptr(x), bsz, _ptr(w_gate), _ptr(w_up), _ptr(w_down), d, f, float(t),
+                                         float(norm_eps), _ptr(resid), _ptr(y), _ptr(active_idx),
+                                         _ptr(active_cnt), _stream(stream)))
     return y, active_idx, active_cnt
 
 

@@ -125,6 +125,31 @@ int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, co
 
 namespace sirius {
 void set_last_error(const char* msg) { g_last_error = msg; }
+
+int ffn_cats_validate(const char* fn, const float* x, int B, const uint16_t* w_gate,
+                      const uint16_t* w_up, const uint16_t* w_down, int d_model, int d_ff, float t,
+                      float norm_eps, const float* resid, const float* y,
+                      const int32_t* active_idx, const int32_t* active_cnt, size_t* need) {
+  int rc = check_ffn_dims(fn, B, d_model, d_ff);
+  if (rc) return rc;
+  if ((rc = check_ptrs(fn, {{x, "x"}, {w_gate, "w_gate"}, {w_up, "w_up"}, {w_down, "w_down"}, {y, "y"}})))
+    return rc;
+  if (resid != nullptr && !aligned16(resid)) return fail(SIRIUS_EINVAL, "%s: resid is not 16-byte aligned", fn);
+  if ((active_idx == nullptr) != (active_cnt == nullptr))
+    return fail(SIRIUS_EINVAL, "%s: active_idx and active_cnt must both be given or both be NULL", fn);
+  if (std::isnan(t)) return fail(SIRIUS_EINVAL, "%s: threshold t is NaN", fn);
+  if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
+  *need = B == 0 ? 0 : gemv_ws(B, d_model, d_ff);
+  return SIRIUS_OK;
+}
+
+int ffn_cats_run(const char* fn, const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                 const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                 const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
+                 void* stream) {
+  return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, kFfnModeThreshold, t, norm_eps,
+                      resid, y, active_idx, active_cnt, ws, static_cast<hipStream_t>(stream));
+}
 }  // namespace sirius
 
 extern "C" {
@@ -198,21 +223,17 @@ int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_
                     const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
                     void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "sirius_ffn_cats";
-  int rc = check_ffn_dims(fn, B, d_model, d_ff);
+  size_t need = 0;
+  int rc = sirius::ffn_cats_validate(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, t, norm_eps,
+                                     resid, y, active_idx, active_cnt, &need);
   if (rc) return rc;
-  if ((rc = check_ptrs(fn, {{x, "x"}, {w_gate, "w_gate"}, {w_up, "w_up"}, {w_down, "w_down"}, {y, "y"}, {ws, "ws"}})))
-    return rc;
-  if (resid != nullptr && !aligned16(resid)) return fail(SIRIUS_EINVAL, "%s: resid is not 16-byte aligned", fn);
-  if ((active_idx == nullptr) != (active_cnt == nullptr))
-    return fail(SIRIUS_EINVAL, "%s: active_idx and active_cnt must both be given or both be NULL", fn);
-  if (std::isnan(t)) return fail(SIRIUS_EINVAL, "%s: threshold t is NaN", fn);
-  if (std::isnan(norm_eps)) return fail(SIRIUS_EINVAL, "%s: norm_eps is NaN", fn);
+  if (ws == nullptr) return fail(SIRIUS_EINVAL, "%s: ws is NULL", fn);
+  if (!aligned16(ws)) return fail(SIRIUS_EINVAL, "%s: ws is not 16-byte aligned", fn);
   if (B == 0) return SIRIUS_OK;
-  const size_t need = gemv_ws(B, d_model, d_ff);
   if (ws_bytes < need)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
-  return run_ffn_gemv(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, sirius::kFfnModeThreshold, t, norm_eps, resid,
-                      y, active_idx, active_cnt, ws, static_cast<hipStream_t>(stream));
+  return sirius::ffn_cats_run(fn, x, B, w_gate, w_up, w_down, d_model, d_ff, t, norm_eps, resid, y,
+                              active_idx, active_cnt, ws, stream);
 }
 
 int sirius_ffn_topk(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,

@@ -12,6 +12,19 @@ namespace sirius {
 // The calling thread's message for sirius_last_error (the C-ABI files set it on failure).
 void set_last_error(const char* msg);
 
+// sirius_ffn_cats in two halves, shared by the entry points that differ only in where the
+// workspace comes from. ffn_cats_validate checks every argument but the workspace (and sets the
+// error message on failure) and stores the workspace bytes the call needs in *need (0 for an
+// empty batch); ffn_cats_run enqueues the call on a workspace of at least that size.
+int ffn_cats_validate(const char* fn, const float* x, int B, const uint16_t* w_gate,
+                      const uint16_t* w_up, const uint16_t* w_down, int d_model, int d_ff, float t,
+                      float norm_eps, const float* resid, const float* y,
+                      const int32_t* active_idx, const int32_t* active_cnt, size_t* need);
+int ffn_cats_run(const char* fn, const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
+                 const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
+                 const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
+                 void* stream);
+
 // FFN selection modes of the small-batch and batch-1 launchers
 constexpr int kFfnModeDense = 0;      // every neuron (dense and condensed)
 constexpr int kFfnModeThreshold = 1;  // |SiLU(gate)| > t per token

@@ -14,6 +14,7 @@
 namespace sirius {
 
 thread_local ProfScope* t_prof = nullptr;
+thread_local bool t_prof_off = false;
 
 namespace {
 
@@ -42,7 +43,7 @@ hipEvent_t take_event() {
 }  // namespace
 
 int prof_open(const char* name) {
-  if (!g_on.load(std::memory_order_relaxed)) return -1;
+  if (t_prof_off || !g_on.load(std::memory_order_relaxed)) return -1;
   std::lock_guard<std::mutex> lk(g_mu);
   Rec r{name, take_event(), take_event(), false};
   if (r.a == nullptr || r.b == nullptr) {

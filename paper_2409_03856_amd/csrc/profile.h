@@ -21,6 +21,17 @@ void prof_close(int id, bool launched);
 
 struct ProfScope;
 extern thread_local ProfScope* t_prof;
+extern thread_local bool t_prof_off;
+
+// While alive, the calling thread's kernels carry no timing events even if timing is on (for the
+// entry point that must create nothing).
+struct ProfSuppress {
+  bool prev;
+  ProfSuppress() : prev(t_prof_off) { t_prof_off = true; }
+  ~ProfSuppress() { t_prof_off = prev; }
+  ProfSuppress(const ProfSuppress&) = delete;
+  ProfSuppress& operator=(const ProfSuppress&) = delete;
+};
 
 // Times the kernels launched through klaunch while it is alive: ProfScope p("name", stream);
 struct ProfScope {
