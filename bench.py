@@ -80,6 +80,15 @@ ATT_H, ATT_HKV, ATT_HD, ATT_L, ATT_P = 32, 8, 128, 4096, 2048
 N_LOGIT_BUFS = 4
 SWEEP = (0.0, 0.4, 0.5, 0.65, 0.8)
 SWEEP_CALLS = 40
+BATCHED = (4, 16)          # batched threshold-sparse decode rows (tokens per call)
+TREE_TOKENS = 64           # the full model's pass over a drafted tree of kernel size 16 x width 4
+STACK8_LAYERS, STACK70_LAYERS = 32, 80
+STACK8_SPARSITY = (0.40, 0.50, 0.65)
+STACK70_SPARSITY = (0.50, 0.65)
+STACK_BATCH = (1, 4, 16)
+STACK_REPS = 5
+UNION_CALLS = 16           # calls per batch size for the union of the kept sets
+ACCEPT_BUFS = 6            # logit buffers per generator for the acceptance-length histograms
 
 
 def log(*a):
@@ -92,9 +101,11 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--cpu-seconds", type=float, default=8.0)
     p.add_argument("--no-sweep", action="store_true",
                    help="leave out the sparsity sweep (for profiler runs that average one kernel's launches)")
+    p.add_argument("--no-stacks", action="store_true",
+                   help="leave out the 32-layer / 80-layer stack timings and the acceptance histograms")
     p.add_argument("--copy-mib", type=int, default=0,
                    help="after setup, run one plain device-to-device copy of this many MiB (the reference "
                         "kernel that scales the HBM byte counters)")
@@ -169,19 +180,40 @@ def main():
     k_keep = D_FF // 2
     log("setup: prompt top-k per copy")
     cond = [sr.sirius_griffin_select(prompt, *layers[c], k_keep, want_scores=False)[2:] for c in range(NCOPY)]
-    log("setup: 70B layers")
-    layers70 = []
-    for c in range(NCOPY70):
+    log("setup: 70B stack (80 layers, 112.7 GB)")
+    stack70 = []
+    for l in range(STACK70_LAYERS):
         ws = []
         for m in range(3):
             w = torch.empty((F70, D70), dtype=torch.bfloat16, device=dev)
-            sr.sirius_fill_normal_bf16(w, 5000 + 3 * c + m, mean=0.0, std=0.02)
+            sr.sirius_fill_normal_bf16(w, 5000 + 3 * l + m, mean=0.0, std=0.02)
             ws.append(w)
-        layers70.append(ws)
+        stack70.append(ws)
+    layers70 = stack70[:NCOPY70]
     x_cal70 = torch.from_numpy(calibration_inputs(5, 256, D70)).to(dev)
-    t70 = [float(sr.sirius_cats_calibrate(x_cal70, layers70[c][0], 0.5).item()) for c in range(NCOPY70)]
+    t70s = {q: [float(sr.sirius_cats_calibrate(x_cal70, stack70[l][0], q).item()) for l in range(STACK70_LAYERS)]
+            for q in STACK70_SPARSITY}
+    t70 = t70s[0.50][:NCOPY70]
     del x_cal70
+    log("setup: 8B stack (32 layers) and its condensed layers")
+    stack8 = []
+    for l in range(STACK8_LAYERS):
+        ws = []
+        for m in range(3):
+            w = torch.empty((D_FF, D_MODEL), dtype=torch.bfloat16, device=dev)
+            sr.sirius_fill_normal_bf16(w, 2000 + 3 * l + m, mean=0.0, std=0.02)
+            ws.append(w)
+        stack8.append(ws)
+    t8s = {q: [float(sr.sirius_cats_calibrate(x_cal, stack8[l][0], q).item()) for l in range(STACK8_LAYERS)]
+           for q in STACK8_SPARSITY}
+    cond8 = []
+    for l in range(STACK8_LAYERS):
+        pr = torch.from_numpy(griffin_prompt(2500 + l, PROMPT_T, D_MODEL).view(np.int16)).view(torch.bfloat16).to(dev)
+        cond8.append(sr.sirius_griffin_select(pr, *stack8[l], k_keep, want_scores=False)[2:])
+    torch.cuda.synchronize()
     xs70 = torch.from_numpy(decode_inputs(6, N_DECODE, D70)).to(dev)
+    xb = {bsz: torch.from_numpy(decode_inputs(8 + bsz, N_DECODE, D_MODEL)).to(dev) for bsz in BATCHED}
+    x64 = torch.from_numpy(decode_inputs(9, TREE_TOKENS, D_MODEL)).to(dev)
     log("setup: logits")
     logits, drafted = [], []
     for i in range(N_LOGIT_BUFS):
@@ -214,6 +246,8 @@ def main():
     act_idx = torch.empty((1, D_FF), dtype=torch.int32, device=dev)
     cnt_log = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
     y70 = torch.empty((1, D70), dtype=torch.float32, device=dev)
+    yb = {bsz: torch.empty((bsz, D_MODEL), dtype=torch.float32, device=dev) for bsz in BATCHED}
+    y64 = torch.empty((TREE_TOKENS, D_MODEL), dtype=torch.float32, device=dev)
     act70 = torch.empty((1, F70), dtype=torch.int32, device=dev)
     cnt70 = torch.zeros((args.steps + args.warmup,), dtype=torch.int32, device=dev)
     g_sel = torch.empty(k_keep, dtype=torch.int32, device=dev)
@@ -273,8 +307,12 @@ def main():
         m_cnt.zero_()
 
     rows = ["cats", "rmsnorm", "griffin", "condensed", "dense", "dense16", "verify", "tree_build", "tree_verify",
-            "topk", "attn1", "attn16", "loop16", "cats70b"]
+            "topk", "attn1", "attn16", "loop16", "cats70b", "cats_b4", "cats_b16", "dense64"]
     stream = torch.cuda.current_stream()
+
+    def batched_window(bsz, s):
+        i0 = (s * bsz) % (N_DECODE - bsz + 1)
+        return xb[bsz][i0:i0 + bsz]
 
     def step(s, ev=None, with70=True, time_cats=False):
         c = s % NCOPY
@@ -326,12 +364,18 @@ def main():
         mark(12)
         loop_graph.replay()
         mark(13)
-        if not with70:  # the per-kernel pass leaves it out: it shares the cats kernels' names
+        if not with70:  # the per-kernel pass leaves these out: they share kernel names with the rows above
             return
         c70 = s % NCOPY70
         sr.sirius_ffn_cats(xs70[s % N_DECODE: s % N_DECODE + 1], *layers70[c70], t70[c70], y=y70,
                            active_idx=act70, active_cnt=cnt70[s:s + 1])
         mark(14)
+        for j, bsz in enumerate(BATCHED):
+            cb = (c + 1 + j) % NCOPY
+            sr.sirius_ffn_cats(batched_window(bsz, s), *layers[cb], thresholds[cb], y=yb[bsz], want_active=False)
+            mark(15 + j)
+        sr.sirius_ffn_dense(x64, *layers[(c + 7) % NCOPY], y=y64)
+        mark(15 + len(BATCHED))
 
     log("warmup")
     for s in range(args.warmup):
@@ -448,6 +492,34 @@ def main():
         torch.cuda.synchronize()
         eager_ms.append(e0.elapsed_time(e1))
 
+    # ------------------------------------------------------------------ union of the kept sets (batched rows)
+    # The batched calls read W_up and W_down rows of the union of the tokens' kept sets; its size,
+    # measured here over UNION_CALLS calls on the same inputs and layer copies as the rows, sets the
+    # rows' algorithmic bytes.
+    union = {}
+    for j, bsz in enumerate(BATCHED):
+        fr, kept = [], []
+        for s_u in range(UNION_CALLS):
+            cb = (s_u % NCOPY + 1 + j) % NCOPY
+            _, ai, ac = sr.sirius_ffn_cats(batched_window(bsz, s_u), *layers[cb], thresholds[cb])
+            ai, ac = ai.cpu().numpy(), ac.cpu().numpy()
+            u = np.zeros(D_FF, dtype=bool)
+            for b in range(bsz):
+                u[ai[b, :ac[b]]] = True
+            fr.append(u.mean())
+            kept.append(ac.mean() / D_FF)
+        union[bsz] = {"union_fraction": round(float(np.mean(fr)), 5), "kept_fraction_per_token": round(float(np.mean(kept)), 4),
+                      "independent_masks_expectation": round(1.0 - (1.0 - float(np.mean(kept))) ** bsz, 5)}
+
+    # ------------------------------------------------------------------ stacks
+    stacks = None if args.no_stacks else run_stacks(sr, torch, np, stream, stack8, t8s, cond8, stack70, t70s, k_keep)
+
+    # ------------------------------------------------------------------ acceptance-length histograms
+    accept = None if args.no_stacks else acceptance_histograms(sr, torch, np, dev, verify_inputs)
+
+    # ------------------------------------------------------------------ copy ceiling
+    copy_gbps = copy_ceiling(torch, dev, stream)
+
     counts = cnt_log[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64)
     mean_active = float(counts.mean())
     mean_active70 = float(cnt70[args.warmup:args.warmup + args.steps].cpu().numpy().astype(np.float64).mean())
@@ -468,7 +540,11 @@ def main():
                  "attn16": (ATT_P + 16) * ATT_HKV * ATT_HD * 2 * 2 + 16 * ATT_HKV * ATT_HD * 2 * 2
                  + 2 * 16 * ATT_H * ATT_HD * 4,
                  "loop16": (LOOP_N + 1) * model_bytes,
-                 "cats70b": cats70_bytes}
+                 "cats70b": cats70_bytes,
+                 "dense64": dense_bytes + 2 * TREE_TOKENS * D_MODEL * 4}
+    for bsz in BATCHED:
+        row_bytes[f"cats_b{bsz}"] = (D_FF * D_MODEL * 2 + 2 * union[bsz]["union_fraction"] * D_FF * D_MODEL * 2
+                                     + 2 * bsz * D_MODEL * 4)
 
     def med(v):
         return float(np.median(np.asarray(v)))
@@ -479,6 +555,11 @@ def main():
         gbps = row_bytes[r] / (us * 1e-6) / 1e9
         rows_out[r] = {"us": round(us, 2), "alg_bytes": int(row_bytes[r]), "gbps": round(gbps, 1),
                        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+    for bsz in BATCHED:
+        rows_out[f"cats_b{bsz}"].update(union[bsz])
+        rows_out[f"cats_b{bsz}"]["us_per_token"] = round(rows_out[f"cats_b{bsz}"]["us"] / bsz, 2)
+    rows_out["dense64"]["us_per_token"] = round(rows_out["dense64"]["us"] / TREE_TOKENS, 3)
+    rows_out["dense16"]["us_per_token"] = round(rows_out["dense16"]["us"] / VERIFY_K, 3)
 
     cats_us = float(np.mean(row_ms["cats"])) * 1e3
     dom = DOM_KERNEL  # everything but the final reduce
@@ -529,8 +610,16 @@ def main():
             "avg_launch_us": dom_us,
             "launches": live[dom]["launches"],
             "timing": "library per-kernel HIP events carried by the kernel dispatch itself (hipExtLaunchKernel) on the launch stream, in a second pass of the same K steps with events on the cats call only",
+            "call_frac": round(cats_bytes / (cats_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "call_note": "call_frac is the whole sparse-FFN call (decode kernel plus the fixed-order reduce launch) "
+                         "at the line's value; frac is the decode kernel alone",
+            "target_0p70_met": {"kernel": dom_gbps / HBM_PEAK_GBPS >= 0.70,
+                                "call": cats_bytes / (cats_us * 1e-6) / 1e9 / HBM_PEAK_GBPS >= 0.70},
+            "copy_ceiling_gbps": copy_gbps,
         },
         "rows": rows_out,
+        "stacks": stacks,
+        "acceptance": accept,
         "kernels": kern,
         "kernels_dominant_pass": live,
         "paper_context": {
@@ -551,12 +640,169 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers[0], thresholds[0], xs, args.cpu_seconds)
+        lg_v, dr_v = verify_inputs(10, VERIFY_B, VERIFY_K, VERIFY_V, 3.0)
+        extra = {"verify": (lg_v, dr_v), "x16": x16.cpu().numpy(), "condensed": cond[0],
+                 "layers70": [(stack70[l], t70s[0.50][l]) for l in (0, 39, 79)],
+                 "x70": xs70[:3].cpu().numpy()}
+        out["cpu_baseline"] = cpu_baseline(layers[0], thresholds[0], xs, args.cpu_seconds, extra)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(layer, t, xs, budget_s):
-    """The fp64 oracle's threshold-sparse decode of the same layer on the host cores."""
+def _median_pass_ms(torch, np, stream, prep, run, reps):
+    """Median time of `reps` passes of run() bracketed by events on the launch stream, each after an
+    untimed prep(); one untimed pass first."""
+    prep()
+    run()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        prep()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(np.asarray(ts)))
+
+
+def run_stacks(sr, torch, np, stream, stack8, t8s, cond8, stack70, t70s, k_keep):
+    """Per-token cost of whole FFN stacks, h <- h + FFN(RMSNorm(h)) layer after layer in place,
+    each layer one library call with the RMSNorm and residual fused: the Llama-3-8B stack (32
+    layers) with per-token threshold sparsity at 40 / 50 / 65 % and batch 1 / 4 / 16, the condensed
+    (prompt top-k) stack, the dense stack at 1, 16 and 64 tokens (one decode token; the full model's
+    pass over a 16-token chunk; over a 64-node tree), and the Llama-3-70B stack (80 layers, 112.7
+    GB) at 50 / 65 % and dense, batch 1. Kept and union fractions come from one more pass with the
+    kept lists written; the timed passes write none."""
+    from synth import decode_inputs
+    eps = 1e-5
+    out = {"llama3_8b_cats": [], "llama3_8b_condensed": [], "llama3_8b_dense": [], "llama3_70b_cats": [],
+           "llama3_70b_dense": []}
+
+    def entry(kind, d, f, nl, bsz, ms, alg_bytes, **kw):
+        us = ms * 1e3
+        gbps = alg_bytes / (us * 1e-6) / 1e9
+        e = {"batch": bsz, "us_per_pass": round(us, 1), "us_per_token": round(us / bsz, 2),
+             "us_per_layer": round(us / nl, 2), "alg_bytes": int(alg_bytes), "gbps": round(gbps, 1),
+             "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        e.update(kw)
+        out[kind].append(e)
+        log(f"stack {kind} B={bsz} {kw}: {us:.1f} us per pass")
+
+    def cats_stack(kind, stack, ts, d, f, bsz, q, seed):
+        nl = len(stack)
+        h0 = torch.from_numpy(decode_inputs(seed, bsz, d)).to(stream.device)
+        h = torch.empty_like(h0)
+        idx = torch.empty((bsz, f), dtype=torch.int32, device=h0.device)
+        cnt = torch.empty((bsz,), dtype=torch.int32, device=h0.device)
+
+        def run():
+            for l in range(nl):
+                sr.sirius_ffn_cats(h, *stack[l], ts[l], norm_eps=eps, resid=h, y=h, want_active=False)
+
+        ms = _median_pass_ms(torch, np, stream, lambda: h.copy_(h0), run, STACK_REPS)
+        h.copy_(h0)
+        kept, unions = [], []
+        for l in range(nl):
+            sr.sirius_ffn_cats(h, *stack[l], ts[l], norm_eps=eps, resid=h, y=h, active_idx=idx, active_cnt=cnt)
+            ai, ac = idx.cpu().numpy(), cnt.cpu().numpy()
+            u = np.zeros(f, dtype=bool)
+            for b in range(bsz):
+                u[ai[b, :ac[b]]] = True
+            kept.append(float(ac.mean()) / f)
+            unions.append(float(u.mean()))
+        alg = sum(f * d * 2 + 2 * u * f * d * 2 for u in unions) + nl * 3 * bsz * d * 4
+        entry(kind, d, f, nl, bsz, ms, alg, target_sparsity=q, kept_fraction=round(float(np.mean(kept)), 4),
+              union_fraction=round(float(np.mean(unions)), 5))
+
+    def dense_stack(kind, layers, d, f, bsz, seed, condensed=False):
+        nl = len(layers)
+        h0 = torch.from_numpy(decode_inputs(seed, bsz, d)).to(stream.device)
+        h = torch.empty_like(h0)
+        call = sr.sirius_ffn_condensed if condensed else sr.sirius_ffn_dense
+
+        def run():
+            for l in range(nl):
+                call(h, *layers[l], norm_eps=eps, resid=h, y=h)
+
+        ms = _median_pass_ms(torch, np, stream, lambda: h.copy_(h0), run, STACK_REPS)
+        entry(kind, d, f, nl, bsz, ms, nl * 3 * f * d * 2 + nl * 3 * bsz * d * 4)
+
+    for bsz in STACK_BATCH:
+        for q in STACK8_SPARSITY:
+            cats_stack("llama3_8b_cats", stack8, t8s[q], D_MODEL, D_FF, bsz, q, 3000 + bsz)
+        dense_stack("llama3_8b_condensed", cond8, D_MODEL, k_keep, bsz, 3100 + bsz, condensed=True)
+    for bsz in (1, VERIFY_K, TREE_TOKENS):
+        dense_stack("llama3_8b_dense", stack8, D_MODEL, D_FF, bsz, 3200 + bsz)
+    for q in STACK70_SPARSITY:
+        cats_stack("llama3_70b_cats", stack70, t70s[q], D70, F70, 1, q, 3300)
+    dense_stack("llama3_70b_dense", stack70, D70, F70, 1, 3400)
+
+    # sparse over dense per-token time at batch 1 (the FFN part of a decode step)
+    d8 = next(e for e in out["llama3_8b_dense"] if e["batch"] == 1)["us_per_token"]
+    d70 = out["llama3_70b_dense"][0]["us_per_token"]
+    out["ratio_to_dense_batch1"] = {
+        "llama3_8b": {f"cats_{int(e['target_sparsity'] * 100)}": round(e["us_per_token"] / d8, 4)
+                      for e in out["llama3_8b_cats"] if e["batch"] == 1},
+        "llama3_8b_condensed": round(next(e for e in out["llama3_8b_condensed"] if e["batch"] == 1)["us_per_token"] / d8, 4),
+        "llama3_70b": {f"cats_{int(e['target_sparsity'] * 100)}": round(e["us_per_token"] / d70, 4)
+                       for e in out["llama3_70b_cats"]},
+    }
+    return out
+
+
+def acceptance_histograms(sr, torch, np, dev, verify_inputs):
+    """Acceptance lengths of the correction check at the Llama-3 vocabulary (8 rows of 16 drafted
+    tokens plus a bonus row per buffer, logits N(0, 3)) for both logit generators: the literal one
+    (drafted logit boosted by U(0, 6)) and the calibrated one (drafted logit = row maximum + U(0, 6)).
+    tokens_per_check counts the accepted drafts plus the corrected (or bonus) token."""
+    out = {}
+    for gen, cal in (("literal", False), ("calibrated", True)):
+        bufs = []
+        for i in range(ACCEPT_BUFS):
+            lg, dr = verify_inputs(200 + i + (100 if cal else 0), VERIFY_B, VERIFY_K, VERIFY_V, 3.0,
+                                   rows=VERIFY_K + 1, calibrated=cal)
+            bufs.append((torch.from_numpy(lg).to(dev), torch.from_numpy(dr).to(dev)))
+        per_r = {}
+        for r in (0.05, 0.1, 0.3):
+            accs = []
+            for lg, dr in bufs:
+                acc, _, _ = sr.sirius_verify_accept(lg, dr, r, 1.0, want_p=False)
+                accs.append(acc.cpu().numpy())
+            a = np.concatenate(accs)
+            per_r[str(r)] = {"histogram_0_to_16": np.bincount(a, minlength=VERIFY_K + 1).tolist(),
+                             "mean_accept_len": round(float(a.mean()), 3),
+                             "tokens_per_check": round(float(a.mean()) + 1.0, 3)}
+        out[gen] = {"rows": len(bufs) * VERIFY_B, "by_r": per_r}
+        del bufs
+    return out
+
+
+def copy_ceiling(torch, dev, stream):
+    """A plain device-to-device copy of 1 GiB (torch's copy kernel), read plus write bytes per second:
+    the practical ceiling of one streaming kernel on this part."""
+    src = torch.ones((1 << 28,), dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = 10
+    e0.record(stream)
+    for _ in range(n):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gbps = 2 * src.numel() * 4 * n / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return round(gbps, 1)
+
+
+def cpu_baseline(layer, t, xs, budget_s, extra=None):
+    """The fp64 oracle on the host cores: the headline row (threshold-sparse decode of the 8B layer,
+    per token) and, within a bounded budget, the other headline configs: the correction check over
+    [8, 16, 128256] logits, the full model's 16-token dense pass and the condensed decode of the 8B
+    layer, and the threshold-sparse decode of three Llama-3-70B layers (per layer, and x 80 for the
+    80-layer stack). Weights are widened to fp64 beforehand (not timed)."""
     import numpy as np
     import torch
     import oracle
@@ -565,8 +811,9 @@ def cpu_baseline(layer, t, xs, budget_s):
         threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
     except Exception:
         threads = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    widen = lambda m: oracle.widen_bf16(m.view(torch.int16).cpu().numpy().view(np.uint16))
     log("cpu baseline: widening weights (not timed)")
-    w = [oracle.widen_bf16(m.view(torch.int16).cpu().numpy().view(np.uint16)) for m in layer]
+    w = [widen(m) for m in layer]
     x_host = xs.cpu().numpy()
     n = 0
     t0 = time.perf_counter()
@@ -576,9 +823,43 @@ def cpu_baseline(layer, t, xs, budget_s):
         el = time.perf_counter() - t0
         if (el >= budget_s and n >= 3) or n >= 400:
             break
-    return {"value": round(el / n * 1e6, 1), "unit": "us/token", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} batch-1 decode tokens of the 8B FFN layer (fp64 NumPy, weights widened beforehand, "
-                      f"untimed) in {el:.1f} s; affinity {len(os.sched_getaffinity(0))} cpus"}
+    res = {"value": round(el / n * 1e6, 1), "unit": "us/token", "cores": int(threads), "kind": "oracle",
+           "sample": f"{n} batch-1 decode tokens of the 8B FFN layer (fp64 NumPy, weights widened beforehand, "
+                     f"untimed) in {el:.1f} s; affinity {len(os.sched_getaffinity(0))} cpus"}
+    if extra is None:
+        return res
+    rows = {}
+
+    def timed(fn):
+        a = time.perf_counter()
+        fn()
+        return time.perf_counter() - a
+
+    lg, dr = extra["verify"]
+    sec = timed(lambda: oracle.verify_accept(lg, dr, 0.1, 1.0))
+    rows["verify_8x16x128256"] = {"us_per_call": round(sec * 1e6, 1), "sample": "one call, fp64 softmax per row"}
+    x16 = extra["x16"]
+    sec = timed(lambda: oracle.ffn_dense(x16, *w))
+    rows["dense16_8b"] = {"us_per_pass": round(sec * 1e6, 1), "us_per_token": round(sec * 1e6 / x16.shape[0], 1),
+                          "sample": f"one {x16.shape[0]}-token dense pass of the 8B layer"}
+    wc = [widen(m) for m in extra["condensed"]]
+    secs = [timed(lambda i=i: oracle.ffn_condensed(x_host[i:i + 1], *wc)) for i in range(3)]
+    rows["condensed_8b"] = {"us_per_token": round(float(np.median(secs)) * 1e6, 1),
+                            "sample": "median of 3 batch-1 tokens on the condensed 8B layer (k = d_ff / 2)"}
+    del wc, w
+    secs = []
+    for l, (lay, tl) in enumerate(extra["layers70"]):
+        log(f"cpu baseline: 70B layer {l} (widening not timed)")
+        w70 = [widen(m) for m in lay]
+        x70 = extra["x70"][l:l + 1]
+        secs.append(timed(lambda: oracle.ffn_cats(x70, *w70, tl)))
+        del w70
+    per_layer = float(np.mean(secs))
+    rows["cats_70b"] = {"us_per_layer": round(per_layer * 1e6, 1), "us_per_token_80_layers": round(per_layer * 80e6, 1),
+                        "sample": f"one batch-1 token on each of {len(secs)} Llama-3-70B layers (threshold sparsity "
+                                  f"50 %), the 80-layer figure is the mean per layer x 80"}
+    res["rows"] = rows
+    return res
 
 
 if __name__ == "__main__":
