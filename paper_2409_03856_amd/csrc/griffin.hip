@@ -3,14 +3,15 @@
 //  griffin_z_kernel       z[t, i] = SiLU(x_t . W_gate[i]) * (x_t . W_up[i]) for the
 //                         T prompt tokens: both products in one MFMA pass
 //                         (v_mfma_f32_16x16x32_bf16, exact bf16 products, fp32
-//                         accumulation). Workgroup tile 128 tokens x 128 neurons
-//                         (eight waves), K staged through LDS in double-buffered
-//                         32-wide slices (XOR-swizzled 64-byte rows), two slices in
-//                         flight, two workgroups per CU;
-//                         the token tiles of a neuron tile run on one XCD together so
-//                         its weights are read from HBM once. For the plain statistic
-//                         the epilogue writes only per-tile sums of z^2 (fp64); the
-//                         normalised variant stores Z.
+//                         accumulation). Workgroup tile 256 tokens x 112 neurons (eight
+//                         waves of 64 x 56, two per SIMD, one workgroup per CU: the 256
+//                         tiles of a 512-token prompt at d_ff = 14336 fill the chip once),
+//                         K through a four-slot LDS ring of 32-wide stages filled by direct
+//                         global-to-LDS loads, the next stage's operands read while the
+//                         current one is multiplied; the token tiles of a neuron tile run on
+//                         one XCD together so its weights are read from HBM once. For the
+//                         plain statistic the epilogue writes only per-tile sums of z^2
+//                         (fp64); the normalised variant stores Z.
 //  griffin_rownorm_kernel ||z_t||^2 per token (normalised variant only).
 //  griffin_score_kernel   s_i = sqrt(sum_t z_ti^2 / ||z_t||^2) (normalised variant only).
 //  griffin_tile_score_kernel  plain statistic: s_i = sqrt of the tile sums in order.
@@ -23,6 +24,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "ring.h"
 
 namespace sirius {
 namespace {
@@ -30,27 +32,41 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 
-constexpr int kGT = 128;           // tokens per workgroup tile
-constexpr int kGN = 128;           // neurons per workgroup tile
-constexpr int kGThreads = 512;     // eight waves: 2 (tokens) x 4 (neurons) wave tiles
-constexpr int kGK = 32;            // K slice per LDS stage
-constexpr int kLdsRow = kGK;       // LDS row (bf16 elements): 64 bytes, chunks XOR-swizzled
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkPer = 64;       // scores per top-k thread at most: d_ff <= 65536
 
+// griffin_z tile: 256 tokens x 112 neurons, both products (224 output columns), eight waves of
+// 64 tokens x 56 neurons each (4 x 2), one workgroup (two waves per SIMD) per CU.
+constexpr int kZT = 256;                  // tokens per workgroup tile
+constexpr int kZN = 112;                  // neurons per workgroup tile
+constexpr int kZWT = 64;                  // tokens per wave
+constexpr int kZWB = 7;                   // column blocks per wave: 7 x (8 gate + 8 up columns)
+constexpr int kZMB = kZWT / 16;           // 16-token blocks per wave
+constexpr int kZThreads = 512;
+constexpr int kZK = 32;                   // K per ring stage: one 64-byte LDS row per token or weight row
+constexpr int kZRowsW = 2 * kZN;          // 224 weight rows per stage (gate and up, interleaved by 8)
+constexpr int kZRows = kZT + kZRowsW;     // 480 rows per stage
+constexpr int kZSlotBytes = kZRows * 64;  // 30 KiB per stage
+constexpr int kZSlots = 5;                // ring depth: four stages in flight while one is multiplied
+constexpr int kZPieces = kZRows * 4;      // 16-byte pieces per stage: 1920
+// direct loads per thread per stage: pieces q * 512 + tid for q = 0..3; the fourth exists for
+// the first 384 threads only (waves 0..5), so the per-wave load count is 4 or 3 (wave-uniform)
+constexpr int kZLoads = (kZPieces + kZThreads - 1) / kZThreads;
+constexpr int kZFullWaves = (kZPieces - (kZLoads - 1) * kZThreads) / kWave;
+static_assert(kZLoads == 4 && kZFullWaves == 6, "the ring's wait counts assume four or three loads per thread");
+static_assert(kZSlots * kZSlotBytes <= 160 * 1024, "the ring fits in LDS");
+static_assert(kZSlots <= 5, "wait_later counts at most four later stages");
+
 __device__ __forceinline__ int ceil_div_dev(int a, int b) { return (a + b - 1) / b; }
 
-// Element offset of 16-byte chunk c (8 bf16) of LDS row r: chunk c sits at position
-// c ^ ((r / 2) % 4) of the row's four, so the MFMA operand reads of 16 rows at one chunk and the
-// staging writes of 16 rows x 4 chunks touch the banks evenly (a padded row pitch left 29M
-// bank-conflict cycles per call in the hardware counters).
-__device__ __forceinline__ int lds_at(int r, int c) { return r * kLdsRow + 8 * (c ^ ((r >> 1) & 3)); }
+// 16 zero bytes in global memory: the source of the K-tail chunks of griffin_z's direct loads
+__device__ __align__(16) uint4 g_zero_chunk[1] = {{0u, 0u, 0u, 0u}};
 
-// 16-byte chunk (8 bf16) of row r at column k, zero outside the matrix.
-__device__ __forceinline__ uint4 load_chunk(const uint16_t* base, int rows, int d, int r, int k) {
-  if (r < rows && k < d) return *reinterpret_cast<const uint4*>(base + (size_t)r * d + k);
-  return make_uint4(0u, 0u, 0u, 0u);
-}
+// Position of 16-byte chunk c of LDS row r among the row's four: c ^ ((r / 2) % 4). An MFMA operand
+// read (16 consecutive rows x the four chunks, one 16-byte chunk per lane) then touches the banks
+// evenly; a padded row pitch left 29M bank-conflict cycles per call in the hardware counters. The
+// map is its own inverse, so a direct load writing position p fetches chunk p ^ ((r / 2) % 4).
+__device__ __forceinline__ int z_pos(int r, int c) { return c ^ ((r >> 1) & 3); }
 
 // Workgroup id -> (neuron tile, token tile). Workgroups are dispatched to the eight XCDs in
 // turn (id % 8), and each XCD has its own L2: the token tiles of one neuron tile are given
@@ -70,132 +86,203 @@ __device__ __forceinline__ void tile_of(int id, int ntn, int ntm, int* n_tile, i
 }
 
 // Z tile (Z != nullptr) or, for the plain statistic, the tile's partial sums of z^2 over its
-// tokens per neuron (part[m_tile][n], fp64) without storing Z. Tile kGT tokens x kGN neurons,
-// eight waves in a 2 x 4 layout, each wave 64 tokens x 32 neurons of both products; K in
-// slices of kGK staged through double-buffered LDS, each thread moving one 16-byte chunk of
-// X, W_gate and W_up per slice. The global loads of slice s + 2 are issued while slice s is
-// multiplied (two register sets), so each load has two slices of MFMA work to arrive in.
-// Occupancy and loads in flight set its pace: at 128 VGPRs and 50 KiB of LDS two workgroups
-// share a CU, so the 448 tiles of a 512-token prompt at d_ff = 14336 run in one round of the
-// chip's 512 slots, with 96 KiB in flight per CU. (Four-wave 128 x 64 tiles: at two slices
-// ahead three workgroups fit per CU and 128 of the 896 tiles run as a second, mostly empty
-// round, about 225 us; at one slice ahead four fit, one round, about 183 us; this layout about
-// 168 us.)
-__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(4))) void griffin_z_kernel(const uint16_t* __restrict__ X, int T,
-                                                        const uint16_t* __restrict__ Wg,
-                                                        const uint16_t* __restrict__ Wu, int d,
-                                                        int F, float* __restrict__ Z,
-                                                        double* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) uint16_t sX[2][kGT * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t sG[2][kGN * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t sU[2][kGN * kLdsRow];
-  __shared__ double s_part[2][kGN];
+// tokens per neuron (part[m_tile][n], fp64) without storing Z.
+//
+// Tile kZT tokens x kZN neurons. The weight rows of the tile are interleaved in blocks of 16:
+// block j holds gate rows n0 + 8j .. + 7, then up rows n0 + 8j .. + 7, so that one 16-column
+// MFMA block carries the gate and up products of 8 neurons, the up product of neuron 8j + p in
+// the lane 8 above the gate product's. Wave (wm, wn) multiplies token rows 64 wm .. + 63 by
+// weight blocks 7 wn .. + 6: 4 x 7 v_mfma_f32_16x16x32_bf16 per K stage into 112 fp32
+// accumulators per lane. The two waves of a SIMD take turns on its MFMA unit.
+//
+// K goes through a five-slot LDS ring of 32-wide stages (30 KiB each) filled by direct
+// global-to-LDS 16-byte loads (three or four per thread per stage, no staging registers): while
+// stage b is multiplied, stages b + 2 .. b + 5 are in flight and the operands of stage b + 1 are
+// read from LDS into a second register set, so the LDS reads of the next stage overlap this
+// stage's MFMAs. One barrier per stage: after it, every wave has finished reading stage b (its
+// register copy is complete) and every load of stage b + 1 has landed, so stage b's slot is
+// refilled with stage b + 5.
+//
+// Rows past T or d_ff load a valid row (T - 1, d_ff - 1) whose products are never used; in a K
+// tail (d_model % 32 != 0) the chunks past d_model are loaded from a block of zeros.
+__global__ __launch_bounds__(kZThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void griffin_z_kernel(
+    const uint16_t* __restrict__ X, int T, const uint16_t* __restrict__ Wg,
+    const uint16_t* __restrict__ Wu, int d, int F, float* __restrict__ Z,
+    double* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) unsigned char s_ring[kZSlots * kZSlotBytes];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   int n_tile, m_tile;
-  tile_of(blockIdx.x, ceil_div_dev(F, kGN), ceil_div_dev(T, kGT), &n_tile, &m_tile);
-  const int t0 = m_tile * kGT, n0 = n_tile * kGN;
-  const int wm = wave >> 2, wn = wave & 3;  // wave tile: 64 tokens x 32 neurons
+  tile_of(blockIdx.x, ceil_div_dev(F, kZN), ceil_div_dev(T, kZT), &n_tile, &m_tile);
+  const int t0 = m_tile * kZT, n0 = n_tile * kZN;
+  const int wm = wave >> 1, wn = wave & 1;  // token quarter, neuron half
+  const int nblk = ceil_div_dev(d, kZK);
 
-  // global -> LDS per slice: X, W_gate and W_up 128 rows x 4 chunks of 16 bytes each, one chunk
-  // of each per thread
-  struct Stage {
-    uint4 x, g, u;
-  };
-  auto gload = [&](int k0, Stage& st) {
-    st.x = load_chunk(X, T, d, t0 + (tid >> 2), k0 + 8 * (tid & 3));
-    st.g = load_chunk(Wg, F, d, n0 + (tid >> 2), k0 + 8 * (tid & 3));
-    st.u = load_chunk(Wu, F, d, n0 + (tid >> 2), k0 + 8 * (tid & 3));
-  };
-  auto sstore = [&](const Stage& st, int buf) {
-    *reinterpret_cast<uint4*>(&sX[buf][lds_at(tid >> 2, tid & 3)]) = st.x;
-    *reinterpret_cast<uint4*>(&sG[buf][lds_at(tid >> 2, tid & 3)]) = st.g;
-    *reinterpret_cast<uint4*>(&sU[buf][lds_at(tid >> 2, tid & 3)]) = st.u;
-  };
-
-  floatx4_t accg[4][2], accu[4][2];
+  // this thread's loads of a stage: slot piece g = q * 512 + tid, row g / 4, position g % 4,
+  // holding chunk z_pos(row, position) of that row; a wave instruction covers 16 whole rows, so
+  // the row kind (token or weight) is uniform over it
+  const bool full_wave = wave < kZFullWaves;  // issues a fourth load per stage
+  const uint16_t* src[kZLoads];
+  int chunk_k[kZLoads];  // K offset of the chunk within a stage (elements)
+  int lds_off[kZLoads];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      accg[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-      accu[mt][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < kZLoads; ++q) {
+    const int g = min(q * kZThreads + tid, kZPieces - 1);  // past the last piece: never issued
+    const int r = g >> 2, c = z_pos(r, g & 3);
+    const uint16_t* row;
+    if (r < kZT) {
+      row = X + (size_t)min(t0 + r, T - 1) * d;
+    } else {
+      const int w = r - kZT, j = w >> 4, p = w & 15;
+      const int n = min(n0 + 8 * j + (p & 7), F - 1);
+      row = (p < 8 ? Wg : Wu) + (size_t)n * d;
     }
-  const int fr = lane & 15, fc = lane >> 4;  // fragment row and 16-byte chunk
-  auto compute = [&](int buf) {
-    bf16x8_t a[4], bg[2], bu[2];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-      a[mt] = *reinterpret_cast<const bf16x8_t*>(&sX[buf][lds_at(wm * 64 + mt * 16 + fr, fc)]);
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      bg[nt] = *reinterpret_cast<const bf16x8_t*>(&sG[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
-      bu[nt] = *reinterpret_cast<const bf16x8_t*>(&sU[buf][lds_at(wn * 32 + nt * 16 + fr, fc)]);
-    }
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        accg[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt], bg[nt], accg[mt][nt], 0, 0, 0);
-        accu[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt], bu[nt], accu[mt][nt], 0, 0, 0);
-      }
-  };
-
-  const int nk = (d + kGK - 1) / kGK;
-  Stage s0, s1;  // register sets of slices 2j and 2j + 1
-  gload(0, s0);
-  if (nk > 1) gload(kGK, s1);
-  sstore(s0, 0);
-  __syncthreads();
-  // slice ks: its loads went into set ks % 2; this set is reloaded with slice ks + 2 as soon
-  // as it has been stored, and the other set (slice ks + 1) is stored after the MFMAs
-  for (int ks = 0; ks < nk; ks += 2) {
-    if (ks + 2 < nk) gload((ks + 2) * kGK, s0);
-    compute(0);
-    if (ks + 1 < nk) sstore(s1, 1);
-    __syncthreads();
-    if (ks + 1 < nk) {  // uniform over the block
-      if (ks + 3 < nk) gload((ks + 3) * kGK, s1);
-      compute(1);
-      if (ks + 2 < nk) sstore(s0, 0);
-      __syncthreads();
-    }
+    src[q] = row;
+    chunk_k[q] = 8 * c;
+    lds_off[q] = (q * kZThreads + wave * kWave) * 16;  // wave-uniform: lane l lands at + 16 l
   }
+  auto issue = [&](unsigned char* slot, int b) {
+    const int k0 = b * kZK;
+    const bool tail = k0 + kZK > d;  // uniform: only the last stage of a K that is not a multiple of 32
+#pragma unroll
+    for (int q = 0; q < kZLoads; ++q) {
+      if (q == kZLoads - 1 && !full_wave) break;  // wave-uniform
+      const int k = k0 + chunk_k[q];
+      // past d_model (the K tail) the chunk comes from a zero block, so those products vanish
+      const void* gp = (tail && k >= d) ? static_cast<const void*>(g_zero_chunk) : static_cast<const void*>(src[q] + k);
+      auto* lp = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<size_t>(slot + lds_off[q]));
+      __builtin_amdgcn_global_load_lds(gp, lp, 16, 0, 0);
+    }
+  };
+  // wait until at most `later` stages of this thread's loads are still in flight
+  auto wait_later = [&](int later) {
+    if (full_wave) {
+      switch (later) {
+        case 0: wait_vm<0>(); break;
+        case 1: wait_vm<kZLoads>(); break;
+        case 2: wait_vm<2 * kZLoads>(); break;
+        case 3: wait_vm<3 * kZLoads>(); break;
+        default: wait_vm<4 * kZLoads>(); break;
+      }
+    } else {
+      switch (later) {
+        case 0: wait_vm<0>(); break;
+        case 1: wait_vm<kZLoads - 1>(); break;
+        case 2: wait_vm<2 * (kZLoads - 1)>(); break;
+        case 3: wait_vm<3 * (kZLoads - 1)>(); break;
+        default: wait_vm<4 * (kZLoads - 1)>(); break;
+      }
+    }
+  };
 
-  // C layout: lane holds column (neuron) lane % 16 and rows (tokens) 4*(lane/16) + i.
+  // operand fragments of one stage: lane l reads row R0 + l % 16, chunk l / 16 of each 16-row block
+  const int fr = lane & 15, fc = lane >> 4;
+  struct Frag {
+    bf16x8_t a[kZMB];  // token blocks
+    bf16x8_t b[kZWB];  // weight blocks
+  };
+  auto read_frag = [&](const unsigned char* slot, Frag& f) {
+#pragma unroll
+    for (int mt = 0; mt < kZMB; ++mt) {
+      const int r = wm * kZWT + 16 * mt + fr;
+      f.a[mt] = *reinterpret_cast<const bf16x8_t*>(slot + r * 64 + 16 * z_pos(r, fc));
+    }
+#pragma unroll
+    for (int nb = 0; nb < kZWB; ++nb) {
+      const int r = kZT + 16 * (kZWB * wn + nb) + fr;
+      f.b[nb] = *reinterpret_cast<const bf16x8_t*>(slot + r * 64 + 16 * z_pos(r, fc));
+    }
+  };
+
+  floatx4_t acc[kZMB][kZWB];
+#pragma unroll
+  for (int mt = 0; mt < kZMB; ++mt)
+#pragma unroll
+    for (int nb = 0; nb < kZWB; ++nb) acc[mt][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  auto mfma = [&](const Frag& f) {
+#pragma unroll
+    for (int nb = 0; nb < kZWB; ++nb)
+#pragma unroll
+      for (int mt = 0; mt < kZMB; ++mt)
+        acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[mt], f.b[nb], acc[mt][nb], 0, 0, 0);
+  };
+
+  // iteration b: fragments of stage b are in `cur`, stage b lives in slot b % kZSlots. Wait for
+  // this thread's loads of stage b + 1 (the loads of stages b + 2 .. b + kZSlots - 1 stay in
+  // flight), barrier, refill the slot of stage b with stage b + kZSlots, then multiply stage b
+  // while reading stage b + 1 into `nxt`. (Past the last stage the read of `nxt` takes a slot
+  // whose values go unused: no branch separates these reads from the MFMAs, so they stay in
+  // flight while the MFMAs issue.)
+  int slot_b = 0;  // slot of stage b
+  auto next_slot = [](int sl) { return sl + 1 == kZSlots ? 0 : sl + 1; };
+  auto step = [&](Frag& cur, Frag& nxt, int b) {
+    if (b + 1 < nblk) wait_later(min(kZSlots - 2, nblk - 2 - b));
+    ring_barrier();
+    const int slot_n = next_slot(slot_b);
+    if (b + kZSlots < nblk) issue(s_ring + slot_b * kZSlotBytes, b + kZSlots);
+    read_frag(s_ring + slot_n * kZSlotBytes, nxt);
+    mfma(cur);
+    slot_b = slot_n;
+  };
+  for (int p = 0; p < kZSlots; ++p)
+    if (p < nblk) issue(s_ring + p * kZSlotBytes, p);  // uniform
+  wait_later(min(kZSlots - 1, nblk - 1));  // stage 0 landed
+  ring_barrier();
+  Frag f0, f1;
+  read_frag(s_ring, f0);
+  int b = 0;
+  for (; b + 1 < nblk; b += 2) {
+    step(f0, f1, b);
+    step(f1, f0, b + 1);
+  }
+  if (b < nblk) step(f0, f1, b);
+
+  // C layout: lane l holds column l % 16 of each 16-column block (gate of neuron 8 nb + l % 16
+  // for l % 16 < 8, up of neuron 8 nb + l % 16 - 8 otherwise) and tokens 4 (l / 16) + i of each
+  // 16-token block; the up product of the gate lane's neuron sits 8 lanes above.
+  const bool gate_lane = (lane & 8) == 0;
   if (Z != nullptr) {
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int nb = 0; nb < kZWB; ++nb) {
+      const int n = n0 + 8 * (kZWB * wn + nb) + (lane & 7);
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const int n = n0 + wn * 32 + nt * 16 + (lane & 15);
+      for (int mt = 0; mt < kZMB; ++mt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int t = t0 + wm * 64 + mt * 16 + 4 * (lane >> 4) + i;
-          if (t < T && n < F) Z[(size_t)t * F + n] = silu(accg[mt][nt][i]) * accu[mt][nt][i];
+          const float g = acc[mt][nb][i];
+          const float u = __shfl_xor(g, 8, kWave);
+          const int t = t0 + wm * kZWT + 16 * mt + 4 * fc + i;
+          if (gate_lane && t < T && n < F) Z[(size_t)t * F + n] = silu(g) * u;
         }
-      }
+    }
     return;
   }
-  // sum of z^2 over this tile's tokens, per neuron, in a fixed order: the lane's 16 rows,
-  // then the four lane groups, then the two token halves of the tile. Tokens past T have zero
-  // inputs, so their z is 0.
+  // sum of z^2 over this tile's tokens, per neuron, in a fixed order: the lane's 16 tokens, then
+  // the four lane groups, then the four token quarters of the tile. Tokens past T are left out.
+  __syncthreads();  // every wave is done with the ring: its first slot holds the wave sums
+  double* s_part = reinterpret_cast<double*>(s_ring);  // [token quarter][kZN]
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    double acc = 0.0;
+  for (int nb = 0; nb < kZWB; ++nb) {
+    double sum = 0.0;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < kZMB; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const double z = (double)(silu(accg[mt][nt][i]) * accu[mt][nt][i]);
-        acc += z * z;
+        const float g = acc[mt][nb][i];
+        const float u = __shfl_xor(g, 8, kWave);
+        const int t = t0 + wm * kZWT + 16 * mt + 4 * fc + i;
+        const double z = (double)(silu(g) * u);
+        if (t < T) sum += z * z;
       }
-    acc += __shfl_xor(acc, 16, kWave);
-    acc += __shfl_xor(acc, 32, kWave);
-    if (lane < 16) s_part[wm][wn * 32 + nt * 16 + lane] = acc;
+    sum += __shfl_xor(sum, 16, kWave);
+    sum += __shfl_xor(sum, 32, kWave);
+    if (lane < 8) s_part[wm * kZN + 8 * (kZWB * wn + nb) + lane] = sum;
   }
   __syncthreads();
-  if (tid < kGN && n0 + tid < F) part[(size_t)m_tile * F + n0 + tid] = s_part[0][tid] + s_part[1][tid];
+  if (tid < kZN && n0 + tid < F)
+    part[(size_t)m_tile * F + n0 + tid] =
+        ((s_part[tid] + s_part[kZN + tid]) + s_part[2 * kZN + tid]) + s_part[3 * kZN + tid];
 }
 
 __global__ __launch_bounds__(256) void griffin_rownorm_kernel(const float* __restrict__ Z, int F,
@@ -383,7 +470,7 @@ GriffinLayout griffin_layout(int T, int d, int F) {
   Carve c;
   L.z = c.take((size_t)T * F * sizeof(float));  // used by the normalised variant only
   L.rownorm = c.take((size_t)T * sizeof(float));
-  L.part = c.take((size_t)ceil_div(T, kGT) * F * sizeof(double));
+  L.part = c.take((size_t)ceil_div(T, kZT) * F * sizeof(double));
   L.scores = c.take((size_t)F * sizeof(float));
   L.total = c.off;
   return L;
@@ -398,11 +485,11 @@ hipError_t launch_griffin(const uint16_t* xp, int T, const uint16_t* wg, const u
   float* rn2 = reinterpret_cast<float*>(ws + L.rownorm);
   double* part = reinterpret_cast<double*>(ws + L.part);
   float* scores = reinterpret_cast<float*>(ws + L.scores);
-  const int ntn = ceil_div(F, kGN), ntm = ceil_div(T, kGT);
+  const int ntn = ceil_div(F, kZN), ntm = ceil_div(T, kZT);
   hipError_t e;
   {
     ProfScope prof("griffin_z", stream);
-    klaunch(griffin_z_kernel, ntn * ntm, kGThreads, 0, stream, xp, T, wg, wu, d, F, Z, part);
+    klaunch(griffin_z_kernel, ntn * ntm, kZThreads, 0, stream, xp, T, wg, wu, d, F, Z, part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   float* sc = scores_out != nullptr ? scores_out : scores;

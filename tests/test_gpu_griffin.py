@@ -55,9 +55,13 @@ def test_ragged(sr):
 
 @pytest.mark.parametrize("normalize", [False, True])
 def test_several_ragged_tiles(sr, normalize):
-    # three token tiles of 128 (the last ragged), nine neuron tiles of 128 (eight placed one per
-    # XCD and one left over, the last ragged), and a K tail of 8 past the last 32-wide slice
+    # two token tiles of 256 (the last ragged), ten neuron tiles of 112 (eight placed one per
+    # XCD and two left over, the last ragged), and a K tail of 8 past the last 32-wide stage
     _check(sr, 7, 300, 520, 1100, 400, 1.0 / np.sqrt(520), normalize=normalize)
+    # three token tiles, eighteen neuron tiles (two rounds of eight, two left over), a K of
+    # fewer stages than the ring holds, and one of exactly one stage
+    _check(sr, 8, 600, 96, 2000, 1000, 1.0 / np.sqrt(96), normalize=normalize)
+    _check(sr, 9, 257, 32, 113, 50, 1.0 / np.sqrt(32), normalize=normalize)
 
 
 def test_normalized_variant(sr):
@@ -83,8 +87,8 @@ def test_llama3_8b_prompt512(sr):
 
 
 def test_long_prompt_full_width_sampled(sr):
-    """A 2000-token prompt at Llama-3-8B FFN width: 16 token tiles of 128 (the last ragged) over
-    112 neuron tiles. The oracle recomputes 64 sampled neurons' scores from their own rows; the
+    """A 2000-token prompt at Llama-3-8B FFN width: 8 token tiles of 256 (the last ragged) over
+    128 neuron tiles of 112. The oracle recomputes 64 sampled neurons' scores from their own rows; the
     selection must be exactly the top-k of the returned scores (equal scores: lower index), and
     sampled condensed rows must be the selected rows."""
     import torch
