@@ -423,8 +423,8 @@ def main():
     torch.cuda.synchronize()
     sr.sirius_profile_enable(False)
     kern = {}
-    for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down",
-                 "ffn_mfma_reduce",
+    for name in ["cats_decode", "cats_reduce", "dense_decode", "dense_reduce", "batch_prep", "batch_gate_up", "batch_down",
+                 "batch_reduce",
                  "verify_stats", "verify_scan", "tree_topw", "tree_select", "tree_stats", "tree_scan", "topk_gate", "topk_cut", "topk_decode",
                  "topk_reduce", "attn_partial", "attn_combine", "kv_rollback", "griffin_z", "griffin_topk", "griffin_score", "condense",
                  "select_hist", "select_pick", "select_init", "rmsnorm"]:

@@ -73,10 +73,14 @@ extern "C" {
  *   resid  [B, d_model] fp32 added to the output, or NULL. May alias y.
  *   y      [B, d_model] fp32 output. May alias resid, must not alias x
  *          unless resid == x == y (in-place residual layer).
- * For B >= 8 both products run on MFMA: the gate and up products take xn
- * rounded to bf16, the down product takes h as a pair of bf16 values
- * (hi = bf16(h), lo = bf16(h - hi): about 16 significant bits); products
- * are exact and accumulate in fp32. For B < 8 xn and h stay fp32.
+ * Precision by batch: B = 1 keeps xn and h in fp32 (bf16 weights times
+ * fp32 values, fp32 sums). For 2 <= B <= 64 with d_model % 256 == 0, and
+ * for B >= 8 at other shapes, both products run on MFMA and accumulate in
+ * fp32; the down product takes h as a pair of bf16 values (hi = bf16(h),
+ * lo = bf16(h - hi): about 16 significant bits). The gate and up products
+ * take xn rounded to bf16 when B >= 8, and for B < 8 xn split exactly into
+ * three bf16 pieces (hi + mid + lo = xn), so their products equal the fp32
+ * ones. At d_model % 256 != 0, B < 8 keeps xn and h in fp32.
  * Errors: SIRIUS_EINVAL for null pointers (resid may be NULL), d_model not
  * a multiple of 8 or outside [8, 8192], d_ff < 1, B < 0 or B > 64.
  */
@@ -97,7 +101,10 @@ int sirius_ffn_dense(const float* x, int B, const uint16_t* w_gate, const uint16
  *              row is left untouched. May be NULL together with active_cnt.
  *   active_cnt [B] int32 out: |A_b|.
  * The gate dot products, SiLU and the comparison are fp32 from the fp32
- * input (x is never rounded to bf16 here), for every B.
+ * input (x is never rounded to bf16 here), for every B; so are the up
+ * products. For 2 <= B <= 64 with d_model % 256 == 0 the down product
+ * takes h as a bf16 hi/lo pair, as in sirius_ffn_dense; B = 1 and other
+ * shapes keep h in fp32.
  * Errors: as sirius_ffn_dense, plus SIRIUS_EINVAL for NaN t or for exactly
  * one of active_idx / active_cnt being NULL.
  */
@@ -117,11 +124,12 @@ int sirius_ffn_cats(const float* x, int B, const uint16_t* w_gate, const uint16_
  * or two threads) race and must be ordered by the caller. The array's contents carry over from
  * call to call; the kernels read only what the same call wrote.
  * Errors: as sirius_ffn_cats, plus SIRIUS_EWORKSPACE when the call would need more than
- * SIRIUS_NOALLOC_SCRATCH_BYTES (sirius_workspace_size(SIRIUS_OP_FFN_CATS, ...) tells; every
- * batch up to 64 at d_model <= 8192 and d_ff <= 28672 fits), SIRIUS_EHIP when the array's device
- * address cannot be obtained, and SIRIUS_EINVAL for a device index of 64 or more.
+ * SIRIUS_NOALLOC_SCRATCH_BYTES, 96 MiB (sirius_workspace_size(SIRIUS_OP_FFN_CATS, ...) tells;
+ * every batch up to 64 at the Llama-3-8B FFN shape, 4096 x 14336, and at the 70B shape,
+ * 8192 x 28672, fits), SIRIUS_EHIP when the array's device address cannot be obtained, and
+ * SIRIUS_EINVAL for a device index of 64 or more.
  */
-#define SIRIUS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+#define SIRIUS_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
 int sirius_ffn_cats_noalloc(const float* x, int B, const uint16_t* w_gate, const uint16_t* w_up,
                             const uint16_t* w_down, int d_model, int d_ff, float t, float norm_eps,
                             const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
@@ -135,7 +143,8 @@ int sirius_ffn_cats_noalloc(const float* x, int B, const uint16_t* w_gate, const
  * read whole, W_up and W_down only for the kept neurons:
  *   y[b] = resid[b] + sum_{i in A_b} SiLU(W_gate[i].xn[b]) (W_up[i].xn[b]) W_down[i]
  * with xn as for sirius_ffn_dense. The gate activations are computed in
- * fp32 (bf16 weights x fp32 inputs), the selection is taken on those values.
+ * fp32 (bf16 weights x fp32 inputs), the selection is taken on those values;
+ * the up and down products have the precision of sirius_ffn_cats.
  *   x, resid, y   as for sirius_ffn_cats.
  *   active_idx    [B, d_ff] int32 out: row b starts with the ascending A_b
  *                 (k entries), or NULL (then active_cnt must be NULL too).

@@ -62,22 +62,42 @@ bool dims_ok(int d_model, int d_ff) {
   return d_model >= 8 && d_model <= kMaxDModel && (d_model % 8) == 0 && d_ff >= 1 && d_ff <= kMaxDFF;
 }
 
-// B == 1 runs the one-pass decode kernel; larger batches the small-batch kernels.
+// Input pieces of the batched MFMA path: the dense chunk/tree pass (8 or more tokens) takes x
+// rounded to bf16, every other batched call the exact fp32 input as three bf16 pieces.
+int batch_px(int B, int mode) {
+  return (mode == sirius::kFfnModeDense && B >= sirius::kMfmaMinBatch) ? 1 : 3;
+}
+
+// B == 1 runs the one-pass decode kernel; 2..64 tokens with d_model % 256 == 0 the batched MFMA
+// kernels; other shapes the small-batch kernels (CATS) or the older MFMA kernels (dense, B >= 8).
 size_t gemv_ws(int B, int d, int F) {
   if (B <= 1) return sirius::decode1_layout(d, F).total;
+  if (sirius::batch_path_ok(B, d, F)) return sirius::batch_layout(B, d, F, 3, true).total;
   return sirius::gemv_layout(B, d, F).total;
 }
 
 size_t ffn_ws(int B, int d, int F) {
+  if (B >= 2 && sirius::batch_path_ok(B, d, F))
+    return sirius::batch_layout(B, d, F, batch_px(B, sirius::kFfnModeDense),
+                                batch_px(B, sirius::kFfnModeDense) == 3).total;
   if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
-  return gemv_ws(B, d, F);
+  if (B <= 1) return sirius::decode1_layout(d, F).total;
+  return sirius::gemv_layout(B, d, F).total;
 }
 
-// Dense / condensed / sparse FFN through the small-batch kernels, batch in LDS-sized chunks.
+// Dense / condensed / sparse FFN: batch 1 on the one-pass decode kernel, batches of 2..64 on the
+// batched MFMA kernels when d_model % 256 == 0, else the small-batch kernels in LDS-sized chunks.
 int run_ffn_gemv(const char* fn, const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                  const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                  const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
                  hipStream_t s) {
+  if (B >= 2 && sirius::batch_path_ok(B, d, F)) {
+    const int px = batch_px(B, mode);
+    const sirius::BatchLayout L = sirius::batch_layout(B, d, F, px, px == 3);
+    return hip_status(sirius::launch_ffn_batch(x, B, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
+                                               active_idx, active_cnt, static_cast<char*>(ws), L, s),
+                      fn);
+  }
   if (B == 1) {
     const sirius::Decode1Layout L1 = sirius::decode1_layout(d, F);
     hipError_t e = sirius::launch_ffn_decode1(x, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
@@ -111,7 +131,7 @@ int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, co
   if (ws_bytes < need)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (B >= sirius::kMfmaMinBatch) {
+  if (B >= sirius::kMfmaMinBatch && !sirius::batch_path_ok(B, d, F)) {
     const sirius::MfmaLayout L = sirius::mfma_layout(B, d, F);
     return hip_status(sirius::launch_ffn_mfma(x, B, wg, wu, wd, d, F, norm_eps, resid, y,
                                               static_cast<char*>(ws), L, s),

@@ -1,9 +1,10 @@
 // Small-batch SwiGLU FFN decode on gfx950, dense and per-token threshold sparsity (FSparse
 // after CATS: the gate is read whole, up and down only for neurons some token keeps), and
-// the calibration pass. Threshold-sparse calls with 2 or more tokens run here in chunks of up
-// to 8 tokens, dense and condensed calls with 2 to 7 tokens; batch 1 runs the one-pass
-// kernel of ffn_decode.hip, and dense calls with 8 or more tokens the MFMA kernel of
-// ffn_mfma.hip, which reuses the down and reduce kernels below.
+// the calibration pass. Batched calls whose d_model is not a multiple of 256 run here in chunks
+// of up to 8 tokens (threshold sparsity and top-k at any batch, dense and condensed with 2 to 7
+// tokens); batch 1 runs the one-pass kernel of ffn_decode.hip, batches of 2..64 with d_model a
+// multiple of 256 the batched MFMA kernels of ffn_batch.hip, and the remaining dense calls
+// with 8 or more tokens the MFMA kernels of ffn_mfma.hip. The reduce kernel below serves all.
 //
 // Three kernels per call, HBM-bound (one bf16 weight per two flops per token). No grid-wide
 // barrier, atomics or fences: workgroups hand results to each other only through kernel
@@ -41,6 +42,7 @@ namespace {
 constexpr int kRPW = 2;                     // rows in flight per gate wave
 constexpr int kGateWaves = 4;
 constexpr int kGateSegs = 1024;             // gate workgroups: four per CU on a 256-CU part
+constexpr int kListSegs = 2048;             // per-segment kept lists the reduce kernel can join
 constexpr int kMaxSeg = 256;                // rows per gate workgroup at most (d_ff <= 65536)
 constexpr int kDownWaves = 4;
 constexpr int kDownUnroll = 16;             // full-row chunks in flight per down wave
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(256) void reduce_kernel(
   // copies list slots tid, tid + 256, ..., 8 in flight. The first slots are requested together
   // with the counts: every slot lies inside the [ntiles, rmax] list buffer, so reading one that
   // its segment did not fill is harmless, and whether it is kept is decided after the prefix.
-  __shared__ int s_pref[kGateSegs + 1];
+  __shared__ int s_pref[kListSegs + 1];
   const int b = (blockIdx.x - nred) / kListBlocks, part_k = (blockIdx.x - nred) % kListBlocks;
   const int32_t* src = bidx + (size_t)b * ntiles * rmax;
   const int nslot = ntiles * rmax;
@@ -644,7 +646,7 @@ hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* r
   const int n = B * d;
   const int nred = ceil_div(n, 4 * kRedOut4);
   const bool lists = active_idx != nullptr;
-  if (lists && nseg > kGateSegs) return hipErrorInvalidValue;
+  if (lists && nseg > kListSegs) return hipErrorInvalidValue;
   klaunch(reduce_kernel, nred + (lists ? B * kListBlocks : 0), 256, 0, stream, 
       part, gr, n, resid, y, nred, B, F, nseg, rmax, bidx, bcnt, active_idx, active_cnt);
   return hipGetLastError();

@@ -65,7 +65,7 @@ hipError_t launch_down(int B, int d, int nseg, int rmax, int gr, const uint16_t*
                        float* part, hipStream_t stream);
 // y[b] = sum_r part[r][b] (+ resid[b]) in a fixed order. With active_idx, B * 16 more
 // workgroups concatenate token b's per-segment lists bidx[b][seg][0 .. bcnt[b][seg]) (nseg
-// segments of rmax slots, nseg <= 1024) into active_idx[b][*] and write active_cnt[b].
+// segments of rmax slots, nseg <= 2048) into active_idx[b][*] and write active_cnt[b].
 hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* resid, float* y,
                          hipStream_t stream, int F = 0, int nseg = 0, int rmax = 0,
                          const int32_t* bidx = nullptr, const int32_t* bcnt = nullptr,
@@ -112,6 +112,34 @@ MfmaLayout mfma_layout(int B, int d, int F);
 hipError_t launch_ffn_mfma(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                            const uint16_t* wd, int d, int F, float norm_eps, const float* resid,
                            float* y, char* ws, const MfmaLayout& L, hipStream_t stream);
+
+// ---- batched FFN on MFMA rings (2 <= B <= 64, d_model % 256 == 0): dense / condensed with the
+// input as px bf16 pieces (1: rounded to bf16; 3: exact fp32), per-token threshold or top-k
+// sparsity (three pieces) reading up and down rows of the tokens' union only
+struct BatchLayout {
+  int mpad, px;      // tokens padded to whole 16-token tiles; input pieces
+  int nseg, np;      // gate/up segments and neurons per segment (<= 56)
+  int sp;            // positions per segment in the segment layout (16, 32 or 64)
+  int hs;            // h row stride (F16 dense; whole 64-position blocks of nseg * sp sparse)
+  int nblocks, gr;   // 64-row down blocks and down ranges
+  size_t xp, hhi, hlo, uidx, ucnt, bidx, bcnt, part, total;  // workspace offsets / size
+};
+bool batch_path_ok(int B, int d, int F);
+// sparse: the segment layout (per-segment union blocks), used by every call with px = 3
+BatchLayout batch_layout(int B, int d, int F, int px, bool sparse);
+// mode: kFfnMode*; with active_idx (sparse modes) the per-token kept lists are written; top-k
+// takes the activations act [B][F] and the per-token cut keys (launch_cut).
+hipError_t launch_ffn_batch(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                            const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                            const float* resid, float* y, int32_t* active_idx,
+                            int32_t* active_cnt, char* ws, const BatchLayout& L,
+                            hipStream_t stream, const float* act = nullptr,
+                            const unsigned long long* cut = nullptr);
+// Top-k gate pass of a batch: act [B][F] = SiLU(W_gate xn) from the exact (three-piece) input;
+// L = batch_layout(B, d, F, 3, true).
+hipError_t launch_batch_act(const float* x, int B, const uint16_t* wg, int d, int F,
+                            float norm_eps, float* act, char* ws, const BatchLayout& L,
+                            hipStream_t stream);
 
 // ---- radix select of the k-th largest non-negative float (ties resolved by index)
 hipError_t launch_select_kth_largest(const float* v, int n, int k, float* out_value,

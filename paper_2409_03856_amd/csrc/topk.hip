@@ -6,14 +6,17 @@
 // three:
 //  1. the gate pass: a = SiLU(W_gate xn) for every neuron into a [B, d_ff] buffer; the whole
 //     gate is read once, as in the threshold path (batch 1: the decode kernel's gate phase
-//     alone, ffn_decode.hip; larger batches: gate_kernel in activation mode, ffn_gemv.hip).
+//     alone, ffn_decode.hip; 2..64 tokens with d_model % 256 == 0: cats_ring_kernel's gate
+//     phase on the exact three-piece input, ffn_batch.hip; other batches: gate_kernel in
+//     activation mode, ffn_gemv.hip).
 //  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
 //     (|a| descending, then the lower index): a most-significant-digit radix select over the
 //     bits of |a| (the exponent byte, then mantissa bytes; LDS histograms, four copies per
 //     wave; a block scan over the 256 bins) until the digit holding it has few members, which
 //     are then gathered and ranked by counting on the full key; when every value bit is
 //     decided first, a block scan over the threads' contiguous index ranges settles the ties.
-//  3. the keyed FFN pass: decode1_kernel (batch 1) or gate_kernel + down_kernel (small
+//  3. the keyed FFN pass: decode1_kernel (batch 1), cats_ring_kernel + down_ring_kernel
+//     (batched, one pass over the tokens' union) or gate_kernel + down_kernel (other small
 //     batches) read the stored activations, keep a neuron iff its key reaches the token's cut,
 //     and stream W_up and W_down for the kept neurons only; reduce_kernel sums the partials
 //     and writes the ascending active lists.
@@ -195,7 +198,9 @@ TopkLayout topk_layout(int B, int d, int F) {
   Carve c;
   L.act = c.take((size_t)B * F * sizeof(float));
   L.cut = c.take((size_t)B * sizeof(unsigned long long));
-  L.ffn = c.take(B <= 1 ? decode1_layout(d, F).total : gemv_layout(B, d, F).total);
+  L.ffn = c.take(B <= 1 ? decode1_layout(d, F).total
+                        : (batch_path_ok(B, d, F) ? batch_layout(B, d, F, 3, true).total
+                                                  : gemv_layout(B, d, F).total));
   L.total = c.off;
   return L;
 }
@@ -208,7 +213,10 @@ hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint
   float* act = reinterpret_cast<float*>(ws + L.act);
   unsigned long long* cut = reinterpret_cast<unsigned long long*>(ws + L.cut);
   char* fws = ws + L.ffn;
+  const bool batch = B >= 2 && batch_path_ok(B, d, F);
+  const BatchLayout BL = batch ? batch_layout(B, d, F, 3, true) : BatchLayout{};
   hipError_t e = B == 1 ? launch_decode1_act(x, wg, d, F, norm_eps, act, stream)
+                 : batch ? launch_batch_act(x, B, wg, d, F, norm_eps, act, fws, BL, stream)
                          : launch_gate_act(x, B, wg, d, F, norm_eps, act, stream);
   if (e != hipSuccess) return e;
   {
@@ -218,6 +226,9 @@ hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint
   if (B == 1)
     return launch_ffn_decode1(x, wg, wu, wd, d, F, kFfnModeTopK, 0.f, norm_eps, resid, y,
                               active_idx, active_cnt, fws, decode1_layout(d, F), stream, act, cut);
+  if (batch)  // one pass over the batch: the up and down rows of the tokens' union
+    return launch_ffn_batch(x, B, wg, wu, wd, d, F, kFfnModeTopK, 0.f, norm_eps, resid, y,
+                            active_idx, active_cnt, fws, BL, stream, act, cut);
   const GemvLayout G = gemv_layout(B, d, F);
   for (int b0 = 0; b0 < B; b0 += G.bc) {
     const int nb = std::min(G.bc, B - b0);

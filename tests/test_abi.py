@@ -98,11 +98,16 @@ def test_cats_noalloc_argument_errors_and_scratch_size(L):
     rc = L.sirius_ffn_cats_noalloc(FAKE, 1, FAKE, FAKE, FAKE, 100, 64, 0.1, -1.0, None, FAKE, None, None, None)
     assert rc == -1 and "d_model" in _err(L)
     assert L.sirius_ffn_cats_noalloc(FAKE, 0, FAKE, FAKE, FAKE, 64, 64, 0.1, -1.0, None, FAKE, None, None, None) == 0
-    # the fixed scratch (32 MiB) covers every batch up to 64 at the Llama-3-8B and 70B widths
-    limit = 32 << 20
+    # the fixed scratch (96 MiB) covers every batch up to 64 at the Llama-3-8B and 70B shapes;
+    # a larger call is refused on the host, before anything is enqueued
+    limit = 96 << 20
     for d, f in ((4096, 14336), (8192, 28672), (256, 688)):
         for bsz in range(1, 65):
             assert 0 < L.sirius_workspace_size(1, bsz, d, f, 0, 0) <= limit, (d, f, bsz)
+    assert L.sirius_workspace_size(1, 64, 8192, 65536, 0, 0) > limit
+    rc = L.sirius_ffn_cats_noalloc(FAKE, 64, FAKE, FAKE, FAKE, 8192, 65536, 0.1, -1.0, None, FAKE, None, None,
+                                   None)
+    assert rc == -2 and "scratch" in _err(L)
 
 
 def test_topk_argument_errors(L):
