@@ -56,6 +56,22 @@ __device__ __forceinline__ void load_row(uint4 (&w)[CPL], const uint4* row, int 
   }
 }
 
+// The same with every lane issuing all CPL loads: a lane past the row's end re-reads its last
+// chunk, and a row that is not wanted (ok false) is read from `spare` (x: read by every
+// workgroup, resident in L2). The number of loads in flight is then fixed where each buffer is
+// used, so the wait for one row leaves the next one in flight (the predicated form above makes
+// the compiler wait for all of them).
+template <int CPL>
+__device__ __forceinline__ void load_row_all(uint4 (&w)[CPL], const uint4* row,
+                                             const uint4* spare, int lane, int nch, bool ok) {
+  const uint4* p = ok ? row : spare;
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const int c = lane + kWave * q;
+    w[q] = ld_stream(p + (c < nch ? c : nch - 1));
+  }
+}
+
 // W[i].x over the wave (every lane receives the sum); lane owns chunks lane + 64 q.
 template <int CPL>
 __device__ __forceinline__ float row_dot(const uint4 (&w)[CPL], const float* xs, int lane,
@@ -96,9 +112,14 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
   const int r0 = (int)(((long long)F * seg) / G);
   const int nr = (int)(((long long)F * (seg + 1)) / G) - r0;  // 1 <= nr <= rmax <= kMaxRows
 
+  const uint4* spare = reinterpret_cast<const uint4*>(x);
   uint4 wa[CPL], wb[CPL];
-  load_row(wa, wg + (size_t)(r0 + wave) * nch, lane, nch, MODE != kModeKeyed && wave < nr);
-  if (kFused) load_row(wb, wu + (size_t)(r0 + wave) * nch, lane, nch, wave < nr);
+  if (kFused) {
+    load_row_all(wa, wg + (size_t)(r0 + wave) * nch, spare, lane, nch, wave < nr);
+    load_row_all(wb, wu + (size_t)(r0 + wave) * nch, spare, lane, nch, wave < nr);
+  } else {
+    load_row(wa, wg + (size_t)(r0 + wave) * nch, lane, nch, MODE != kModeKeyed && wave < nr);
+  }
 
   // ---- x into LDS, RMS-normalised when norm_eps >= 0
   float ss = 0.f;
@@ -151,9 +172,9 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
     for (int j = wave; j < nr; j += kWaves) {
       const int jn = j + kWaves;
       const float a = silu(row_dot(wa, xs, lane, nch));
-      load_row(wa, wg + (size_t)(r0 + jn) * nch, lane, nch, jn < nr);
+      load_row_all(wa, wg + (size_t)(r0 + jn) * nch, spare, lane, nch, jn < nr);
       const float u = row_dot(wb, xs, lane, nch);
-      load_row(wb, wu + (size_t)(r0 + jn) * nch, lane, nch, jn < nr);
+      load_row_all(wb, wu + (size_t)(r0 + jn) * nch, spare, lane, nch, jn < nr);
       if (lane == 0) s_h[j] = a * u;  // kept list = the segment's rows in order
     }
     for (int j = tid; j < nr; j += kThreads) s_list[j] = j;

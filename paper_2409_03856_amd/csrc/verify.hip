@@ -141,19 +141,44 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stats_kernel(
   if ((V & 3) == 0) {
     // 16-byte loads, kChunk per thread in flight; seg is a multiple of 4 so lo is 16-byte
     // aligned. Groups of 4 logits in a chunk are folded with one rescale per chunk.
+    // Two chunks are in flight per thread: the next chunk's loads are issued before this one is
+    // folded, so the exps of one chunk overlap the loads of the next. Every lane issues every
+    // load (past the segment it re-reads the segment's last 16 bytes), which keeps the waits
+    // exact; the values past the segment are then replaced by -inf, which changes neither the
+    // max, the sum nor the argmax.
     const float4* L4 = reinterpret_cast<const float4*>(L);
     const int lo4 = lo >> 2, hi4 = (hi + 3) >> 2;  // hi is V or a multiple of 4
-    for (int i = lo4 + tid; i < hi4; i += kChunk * kVerifyThreads) {
-      float4 v[kChunk];
+    constexpr int kStep = kChunk * kVerifyThreads;
+    auto issue = [&](float4(&v)[kChunk], int i) {
+#pragma unroll
+      for (int g = 0; g < kChunk; ++g) {
+        const int k = i + g * kVerifyThreads;
+        v[g] = ld_stream(L4 + (k < hi4 ? k : hi4 - 1));
+      }
+    };
+    auto fold = [&](float4(&v)[kChunk], int i) {
       int i0[kChunk];
 #pragma unroll
       for (int g = 0; g < kChunk; ++g) {
         const int k = i + g * kVerifyThreads;
-        // past the segment: -inf logits change neither the max, the sum nor the argmax
-        v[g] = (k < hi4) ? ld_stream(L4 + k) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        const bool in = k < hi4;
+        v[g].x = in ? v[g].x : -INFINITY;
+        v[g].y = in ? v[g].y : -INFINITY;
+        v[g].z = in ? v[g].z : -INFINITY;
+        v[g].w = in ? v[g].w : -INFINITY;
         i0[g] = 4 * k;
       }
       stat_fold<kChunk>(st, v, i0, c);
+    };
+    float4 va[kChunk], vb[kChunk];
+    const int i_first = lo4 + tid;
+    issue(va, i_first);
+    for (int i = i_first; i < hi4; i += 2 * kStep) {
+      issue(vb, i + kStep);
+      fold(va, i);
+      if (i + kStep >= hi4) break;
+      issue(va, i + 2 * kStep);
+      fold(vb, i + kStep);
     }
   } else {
     for (int i = lo + tid; i < hi; i += kVerifyThreads) stat_fold1(st, L[i], i, c);
