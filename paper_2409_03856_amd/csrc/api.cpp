@@ -72,14 +72,13 @@ int batch_px(int B, int mode) {
 // kernels; other shapes the small-batch kernels (CATS) or the older MFMA kernels (dense, B >= 8).
 size_t gemv_ws(int B, int d, int F) {
   if (B <= 1) return sirius::decode1_layout(d, F).total;
-  if (sirius::batch_path_ok(B, d, F)) return sirius::batch_layout(B, d, F, 3, true).total;
+  if (sirius::batch_path_ok(B, d, F)) return sirius::batch_layout(B, d, F, 3).total;
   return sirius::gemv_layout(B, d, F).total;
 }
 
 size_t ffn_ws(int B, int d, int F) {
   if (B >= 2 && sirius::batch_path_ok(B, d, F))
-    return sirius::batch_layout(B, d, F, batch_px(B, sirius::kFfnModeDense),
-                                batch_px(B, sirius::kFfnModeDense) == 3).total;
+    return sirius::batch_layout(B, d, F, batch_px(B, sirius::kFfnModeDense)).total;
   if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
   if (B <= 1) return sirius::decode1_layout(d, F).total;
   return sirius::gemv_layout(B, d, F).total;
@@ -93,7 +92,7 @@ int run_ffn_gemv(const char* fn, const float* x, int B, const uint16_t* wg, cons
                  hipStream_t s) {
   if (B >= 2 && sirius::batch_path_ok(B, d, F)) {
     const int px = batch_px(B, mode);
-    const sirius::BatchLayout L = sirius::batch_layout(B, d, F, px, px == 3);
+    const sirius::BatchLayout L = sirius::batch_layout(B, d, F, px);
     return hip_status(sirius::launch_ffn_batch(x, B, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
                                                active_idx, active_cnt, static_cast<char*>(ws), L, s),
                       fn);

@@ -120,13 +120,13 @@ struct BatchLayout {
   int mpad, px;      // tokens padded to whole 16-token tiles; input pieces
   int nseg, np;      // gate/up segments and neurons per segment (<= 56)
   int sp;            // positions per segment in the segment layout (16, 32 or 64)
-  int hs;            // h row stride (F16 dense; whole 64-position blocks of nseg * sp sparse)
-  int nblocks, gr;   // 64-row down blocks and down ranges
+  int hs;            // h row stride: nseg * sp rounded up to whole 64-position down blocks
+  int nblocks, gr;   // 64-position down blocks and down ranges
   size_t xp, hhi, hlo, uidx, ucnt, bidx, bcnt, part, total;  // workspace offsets / size
 };
 bool batch_path_ok(int B, int d, int F);
 // sparse: the segment layout (per-segment union blocks), used by every call with px = 3
-BatchLayout batch_layout(int B, int d, int F, int px, bool sparse);
+BatchLayout batch_layout(int B, int d, int F, int px);
 // mode: kFfnMode*; with active_idx (sparse modes) the per-token kept lists are written; top-k
 // takes the activations act [B][F] and the per-token cut keys (launch_cut).
 hipError_t launch_ffn_batch(const float* x, int B, const uint16_t* wg, const uint16_t* wu,

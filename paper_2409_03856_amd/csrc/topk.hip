@@ -199,7 +199,7 @@ TopkLayout topk_layout(int B, int d, int F) {
   L.act = c.take((size_t)B * F * sizeof(float));
   L.cut = c.take((size_t)B * sizeof(unsigned long long));
   L.ffn = c.take(B <= 1 ? decode1_layout(d, F).total
-                        : (batch_path_ok(B, d, F) ? batch_layout(B, d, F, 3, true).total
+                        : (batch_path_ok(B, d, F) ? batch_layout(B, d, F, 3).total
                                                   : gemv_layout(B, d, F).total));
   L.total = c.off;
   return L;
@@ -214,7 +214,7 @@ hipError_t launch_ffn_topk(const float* x, int B, const uint16_t* wg, const uint
   unsigned long long* cut = reinterpret_cast<unsigned long long*>(ws + L.cut);
   char* fws = ws + L.ffn;
   const bool batch = B >= 2 && batch_path_ok(B, d, F);
-  const BatchLayout BL = batch ? batch_layout(B, d, F, 3, true) : BatchLayout{};
+  const BatchLayout BL = batch ? batch_layout(B, d, F, 3) : BatchLayout{};
   hipError_t e = B == 1 ? launch_decode1_act(x, wg, d, F, norm_eps, act, stream)
                  : batch ? launch_batch_act(x, B, wg, d, F, norm_eps, act, fws, BL, stream)
                          : launch_gate_act(x, B, wg, d, F, norm_eps, act, stream);

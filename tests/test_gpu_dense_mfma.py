@@ -119,3 +119,26 @@ def test_llama3_8b_tree_pass(sr, bsz):
     e, nb = check_ffn_rounded_norm(y, xn, wg, wu, wd, resid=res)
     say(f"  error vs precision-matched oracle: {e:.2e} x RMS ({nb} inputs with ambiguous rounding)")
     assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
+
+
+@pytest.mark.parametrize("d,f", [(256, 1000), (256, 97), (512, 3100)])
+@pytest.mark.parametrize("bsz,mode", [(4, "dense"), (16, "dense"), (64, "dense"), (16, "cats")])
+def test_segment_tail_on_dirty_workspace(sr, d, f, bsz, mode):
+    """Batched calls whose segment layout ends inside a 64-position down block (250 segments of
+    16 positions at d_ff = 1000, 25 at 97, 194 at 3100): the positions past the last segment must
+    read h = 0 whatever the workspace held. The workspace is filled with 0xFF bytes (NaN as bf16
+    and fp32) before the call."""
+    import torch
+    say(f"segment tail d={d} f={f} B={bsz} {mode}")
+    (wg, wu, wd), W = _layer(800 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
+    x = decode_inputs(80 + bsz, bsz, d)
+    op = sr.OP_FFN_DENSE if mode == "dense" else sr.OP_FFN_CATS
+    n = int(sr.lib().sirius_workspace_size(op, bsz, d, f, 0, 0))
+    ws = torch.full((n,), 255, dtype=torch.uint8, device="cuda")
+    if mode == "dense":
+        y = host(sr.sirius_ffn_dense(dev_f32(x), *W, ws=ws))
+    else:  # t < 0 keeps every neuron: the dense FFN on the exact input
+        y = host(sr.sirius_ffn_cats(dev_f32(x), *W, -1.0, want_active=False, ws=ws)[0])
+    assert np.all(np.isfinite(y))
+    x_ref = rounded_bf16(x) if (mode == "dense" and bsz >= 8) else x
+    check_ffn(y, oracle.ffn_dense(x_ref, wg, wu, wd), tol=FP32_PATH_TOL)
