@@ -10,11 +10,11 @@
 //     phase on the exact three-piece input, ffn_batch.hip; other batches: gate_kernel in
 //     activation mode, ffn_gemv.hip).
 //  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
-//     (|a| descending, then the lower index): a most-significant-digit radix select over the
-//     bits of |a| (the exponent byte, then mantissa bytes; LDS histograms, four copies per
-//     wave; a block scan over the 256 bins) until the digit holding it has few members, which
-//     are then gathered and ranked by counting on the full key; when every value bit is
-//     decided first, a block scan over the threads' contiguous index ranges settles the ties.
+//     (|a| descending, then the lower index) by a most-significant-digit radix select over the
+//     bits of |a| in digits of 11, 11 and 9 bits (LDS histograms in eight copies; a block scan
+//     over the bins) until the digit holding it has at most 128 members, which are placed by a
+//     block scan and ranked by counting on the full key; when every value bit is decided
+//     first, a block scan over the threads' contiguous index ranges settles the ties.
 //  3. the keyed FFN pass: decode1_kernel (batch 1), cats_ring_kernel + down_ring_kernel
 //     (batched, one pass over the tokens' union) or gate_kernel + down_kernel (other small
 //     batches) read the stored activations, keep a neuron iff its key reaches the token's cut,
@@ -30,9 +30,15 @@ namespace {
 
 constexpr int kCutThreads = 1024;
 constexpr int kCutWaves = kCutThreads / kWave;  // 16
-constexpr int kBins = 256;                      // 8-bit digits
-constexpr int kCopies = 4 * kCutWaves;          // histogram copies: four per wave
-constexpr int kGather = 512;                    // digit members ranked directly at most
+// Digits of the bits of |a| (bit 31, the sign, is 0), most significant first: 11, 11 and 9 bits.
+// The first digit is the exponent and three mantissa bits; activations crowd into a few
+// exponents, and near the median into a narrow band of them (SiLU's negative lobe piles |a| up
+// below 0.28), so a few hundred to a few thousand values can share the first digit.
+constexpr int kDigitBits[3] = {11, 11, 9};
+constexpr int kDigitShift[3] = {20, 9, 0};
+constexpr int kBinsMax = 2048;
+constexpr int kCopies = 8;        // histogram copies: (lane / 16) + 4 (wave % 2)
+constexpr int kRankMax = 128;     // digit members ranked directly on the full key at most
 
 // Inclusive scan of one int per thread over the 1024-thread workgroup; *total is the sum.
 __device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* total) {
@@ -58,23 +64,25 @@ __device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* t
 }
 
 // Thread t owns neurons [t * PER, t * PER + PER) of the token (contiguous, for the tie scan).
-// Digits of the bits of |a|, most significant first: the 8 exponent bits, then the mantissa in
-// 8, 8 and 7 bits (activations crowd into a few exponents, so the exponent digit comes
-// alone). Each wave keeps four histogram copies (one per 16 lanes) so that equal digits
-// collide less in the LDS atomics. As soon as the digit holding the k-th largest has at most
-// kGather members (usually after the second digit), they are gathered and ranked by counting
-// on the full key; only when every value bit is decided does an index scan settle the ties.
+// Each pass histograms one digit of the values that match the digits decided so far (LDS
+// atomics; the first pass in eight copies, so that equal digits of one wave instruction collide
+// less), and a
+// block scan over the bins (thread t holds the two digits 2^bits - 1 - 2t and the next one
+// down, so the scan counts the values at or above them) finds the digit holding the k-th
+// largest and its rank inside the digit. As soon as that digit has at most kRankMax members,
+// they are placed in LDS by a block scan of the per-thread member counts and ranked by counting
+// on the full key; when every value bit is decided first, a block scan over the threads'
+// contiguous index ranges settles the ties.
 template <int PER>
 __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __restrict__ act,
                                                                int F, int k,
                                                                unsigned long long* __restrict__ cut) {
-  __shared__ uint32_t s_hist[kCopies * kBins];
-  __shared__ unsigned long long s_cand[kGather];
+  __shared__ uint32_t s_hist[kCopies * kBinsMax];
+  __shared__ unsigned long long s_cand[kRankMax];
   __shared__ int s_w[kCutWaves];
   __shared__ int s_sel[3];
-  __shared__ int s_n;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int copy = wave * (kCopies / kCutWaves) + (lane >> 4);
+  const int copy = (lane >> 4) + 4 * (wave & 1);
   const int b = blockIdx.x;
   const float* a = act + (size_t)b * F;
   const int i0 = tid * PER;
@@ -94,62 +102,66 @@ __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __re
 #pragma unroll
     for (int j = 0; j < PER; ++j) v[j] = (i0 + j < F) ? __float_as_uint(fabsf(a[i0 + j])) : 0u;
   }
-  if (tid == 0) s_n = 0;
 
   uint32_t prefix = 0u, pmask = 0u;
   int kr = k;  // rank (1-based, descending) of the wanted key among those matching the prefix
 #pragma unroll 1
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = pass == 0 ? 23 : (pass == 1 ? 15 : (pass == 2 ? 7 : 0));
-    const uint32_t dmask = pass == 3 ? 127u : 255u;
-    for (int i = tid; i < kCopies * kBins; i += kCutThreads) s_hist[i] = 0u;
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = kDigitShift[pass], nb = 1 << kDigitBits[pass];
+    const uint32_t dmask = (uint32_t)nb - 1u;
+    // the later passes see only the values that share the first digit: one copy is enough
+    const int ncopy = pass == 0 ? kCopies : 1, my_copy = pass == 0 ? copy : 0;
+    for (int i = tid; i < ncopy * nb; i += kCutThreads) s_hist[i] = 0u;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < PER; ++j)
       if (i0 + j < F && (v[j] & pmask) == prefix)
-        atomicAdd(&s_hist[copy * kBins + ((v[j] >> shift) & dmask)], 1u);
+        atomicAdd(&s_hist[my_copy * nb + ((v[j] >> shift) & dmask)], 1u);
     __syncthreads();
-    // thread t < 256 holds digit 255 - t, so the inclusive scan counts the digits >= it
-    int c = 0;
-    if (tid < kBins) {
-#pragma unroll 16
-      for (int q = 0; q < kCopies; ++q) c += (int)s_hist[q * kBins + (kBins - 1 - tid)];
+    const int d1 = nb - 1 - 2 * tid, d2 = d1 - 1;
+    int c1 = 0, c2 = 0;
+    if (d2 >= 0) {
+      for (int q = 0; q < ncopy; ++q) {
+        c1 += (int)s_hist[q * nb + d1];
+        c2 += (int)s_hist[q * nb + d2];
+      }
     }
     int tot;
-    const int incl = block_inclusive_scan_1024(c, s_w, &tot);
-    if (tid < kBins && incl >= kr && incl - c < kr) {
-      s_sel[0] = kBins - 1 - tid;
-      s_sel[1] = kr - (incl - c);
-      s_sel[2] = c;
+    const int incl = block_inclusive_scan_1024(c1 + c2, s_w, &tot);
+    const int before = incl - c1 - c2;
+    if (before < kr && kr <= before + c1) {
+      s_sel[0] = d1;
+      s_sel[1] = kr - before;
+      s_sel[2] = c1;
+    } else if (before + c1 < kr && kr <= incl) {
+      s_sel[0] = d2;
+      s_sel[1] = kr - before - c1;
+      s_sel[2] = c2;
     }
     __syncthreads();
     prefix |= (uint32_t)s_sel[0] << shift;
     pmask |= dmask << shift;
     kr = s_sel[1];
-    if (pass < 3 && s_sel[2] <= kGather) {  // uniform: gather the digit's members, rank them
-      const int cnt = s_sel[2];
+    const int cnt = s_sel[2];
+    if (pass < 2 && cnt <= kRankMax) {  // uniform: place the digit's members, rank them
+      int nm = 0;
 #pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        if (i0 + j < F && (v[j] & pmask) == prefix) {
-          const int pos = atomicAdd(&s_n, 1);
-          s_cand[pos] = ((unsigned long long)v[j] << 32) | (unsigned)(~(unsigned)(i0 + j));
-        }
-      }
+      for (int j = 0; j < PER; ++j) nm += (i0 + j < F && (v[j] & pmask) == prefix) ? 1 : 0;
+      int pos = block_inclusive_scan_1024(nm, s_w, &tot) - nm;
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        if (i0 + j < F && (v[j] & pmask) == prefix)
+          s_cand[pos++] = ((unsigned long long)v[j] << 32) | (unsigned)(~(unsigned)(i0 + j));
       __syncthreads();
-      if (tid < cnt) {  // cnt <= kGather <= kCutThreads
+      if (tid < cnt) {  // cnt <= kRankMax <= kCutThreads; the keys are distinct
         const unsigned long long mine = s_cand[tid];
         int r = 0;
-        for (int j0 = 0; j0 < cnt; j0 += 16) {
-          unsigned long long o[16];
-#pragma unroll
-          for (int q = 0; q < 16; ++q) o[q] = s_cand[min(j0 + q, cnt - 1)];
-#pragma unroll
-          for (int q = 0; q < 16; ++q) r += (int)((j0 + q < cnt) & (o[q] > mine));
-        }
-        if (r == kr - 1) cut[b] = mine;  // keys are distinct: one member has this rank
+        for (int q = 0; q < cnt; ++q) r += (s_cand[q] > mine) ? 1 : 0;
+        if (r == kr - 1) cut[b] = mine;
       }
       return;
     }
+    __syncthreads();  // s_sel is read by every thread before the next pass writes it
   }
   // every value bit decided: prefix is the k-th largest |a|; the first kr neurons (by index)
   // equal to it are kept
