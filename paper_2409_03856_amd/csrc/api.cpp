@@ -62,58 +62,65 @@ bool dims_ok(int d_model, int d_ff) {
   return d_model >= 8 && d_model <= kMaxDModel && (d_model % 8) == 0 && d_ff >= 1 && d_ff <= kMaxDFF;
 }
 
+}  // namespace
+
+namespace sirius {
+
 // Input pieces of the batched MFMA path: the dense chunk/tree pass (8 or more tokens) takes x
 // rounded to bf16, every other batched call the exact fp32 input as three bf16 pieces.
-int batch_px(int B, int mode) {
-  return (mode == sirius::kFfnModeDense && B >= sirius::kMfmaMinBatch) ? 1 : 3;
+static int batch_px(int B, int mode) {
+  return (mode == kFfnModeDense && B >= kMfmaMinBatch) ? 1 : 3;
 }
 
 // B == 1 runs the one-pass decode kernel; 2..64 tokens with d_model % 256 == 0 the batched MFMA
-// kernels; other shapes the small-batch kernels (CATS) or the older MFMA kernels (dense, B >= 8).
-size_t gemv_ws(int B, int d, int F) {
-  if (B <= 1) return sirius::decode1_layout(d, F).total;
-  if (sirius::batch_path_ok(B, d, F)) return sirius::batch_layout(B, d, F, 3).total;
-  return sirius::gemv_layout(B, d, F).total;
+// kernels; other shapes the older MFMA kernels (dense, B >= 8) or the small-batch kernels in
+// LDS-sized chunks.
+size_t ffn_any_ws(int B, int d, int F, int mode) {
+  if (B <= 1) return decode1_layout(d, F).total;
+  if (batch_path_ok(B, d, F)) return batch_layout(B, d, F, batch_px(B, mode)).total;
+  if (mode == kFfnModeDense && B >= kMfmaMinBatch) return mfma_layout(B, d, F).total;
+  return gemv_layout(B, d, F).total;
 }
 
-size_t ffn_ws(int B, int d, int F) {
-  if (B >= 2 && sirius::batch_path_ok(B, d, F))
-    return sirius::batch_layout(B, d, F, batch_px(B, sirius::kFfnModeDense)).total;
-  if (B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
-  if (B <= 1) return sirius::decode1_layout(d, F).total;
-  return sirius::gemv_layout(B, d, F).total;
+hipError_t launch_ffn_any(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                          const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                          const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                          char* ws, hipStream_t s) {
+  if (B == 1)
+    return launch_ffn_decode1(x, wg, wu, wd, d, F, mode, t, norm_eps, resid, y, active_idx,
+                              active_cnt, ws, decode1_layout(d, F), s);
+  if (batch_path_ok(B, d, F))
+    return launch_ffn_batch(x, B, wg, wu, wd, d, F, mode, t, norm_eps, resid, y, active_idx,
+                            active_cnt, ws, batch_layout(B, d, F, batch_px(B, mode)), s);
+  if (mode == kFfnModeDense && B >= kMfmaMinBatch)
+    return launch_ffn_mfma(x, B, wg, wu, wd, d, F, norm_eps, resid, y, ws, mfma_layout(B, d, F), s);
+  const GemvLayout L = gemv_layout(B, d, F);
+  for (int b0 = 0; b0 < B; b0 += L.bc) {
+    const int nb = std::min(L.bc, B - b0);
+    hipError_t e = launch_ffn_gemv(
+        x + (size_t)b0 * d, nb, wg, wu, wd, d, F, mode, t, norm_eps,
+        resid ? resid + (size_t)b0 * d : nullptr, y + (size_t)b0 * d,
+        active_idx ? active_idx + (size_t)b0 * F : nullptr, active_cnt ? active_cnt + b0 : nullptr,
+        ws, L, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-// Dense / condensed / sparse FFN: batch 1 on the one-pass decode kernel, batches of 2..64 on the
-// batched MFMA kernels when d_model % 256 == 0, else the small-batch kernels in LDS-sized chunks.
+}  // namespace sirius
+
+namespace {
+
+size_t gemv_ws(int B, int d, int F) { return sirius::ffn_any_ws(B, d, F, sirius::kFfnModeThreshold); }
+size_t ffn_ws(int B, int d, int F) { return sirius::ffn_any_ws(B, d, F, sirius::kFfnModeDense); }
+
 int run_ffn_gemv(const char* fn, const float* x, int B, const uint16_t* wg, const uint16_t* wu,
                  const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
                  const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt, void* ws,
                  hipStream_t s) {
-  if (B >= 2 && sirius::batch_path_ok(B, d, F)) {
-    const int px = batch_px(B, mode);
-    const sirius::BatchLayout L = sirius::batch_layout(B, d, F, px);
-    return hip_status(sirius::launch_ffn_batch(x, B, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
-                                               active_idx, active_cnt, static_cast<char*>(ws), L, s),
-                      fn);
-  }
-  if (B == 1) {
-    const sirius::Decode1Layout L1 = sirius::decode1_layout(d, F);
-    hipError_t e = sirius::launch_ffn_decode1(x, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
-                                              active_idx, active_cnt, static_cast<char*>(ws), L1, s);
-    return e == hipSuccess ? SIRIUS_OK : hip_status(e, fn);
-  }
-  const sirius::GemvLayout L = sirius::gemv_layout(B, d, F);
-  for (int b0 = 0; b0 < B; b0 += L.bc) {
-    const int nb = std::min(L.bc, B - b0);
-    hipError_t e = sirius::launch_ffn_gemv(
-        x + (size_t)b0 * d, nb, wg, wu, wd, d, F, mode, t, norm_eps,
-        resid ? resid + (size_t)b0 * d : nullptr, y + (size_t)b0 * d,
-        active_idx ? active_idx + (size_t)b0 * F : nullptr, active_cnt ? active_cnt + b0 : nullptr,
-        static_cast<char*>(ws), L, s);
-    if (e != hipSuccess) return hip_status(e, fn);
-  }
-  return SIRIUS_OK;
+  return hip_status(sirius::launch_ffn_any(x, B, wg, wu, wd, d, F, mode, t, norm_eps, resid, y,
+                                           active_idx, active_cnt, static_cast<char*>(ws), s),
+                    fn);
 }
 
 int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, const uint16_t* wu,
@@ -129,15 +136,8 @@ int ffn_dense_impl(const char* fn, const float* x, int B, const uint16_t* wg, co
   const size_t need = ffn_ws(B, d, F);
   if (ws_bytes < need)
     return fail(SIRIUS_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (B >= sirius::kMfmaMinBatch && !sirius::batch_path_ok(B, d, F)) {
-    const sirius::MfmaLayout L = sirius::mfma_layout(B, d, F);
-    return hip_status(sirius::launch_ffn_mfma(x, B, wg, wu, wd, d, F, norm_eps, resid, y,
-                                              static_cast<char*>(ws), L, s),
-                      fn);
-  }
-  return run_ffn_gemv(fn, x, B, wg, wu, wd, d, F, /*mode=*/0, 0.f, norm_eps, resid, y, nullptr,
-                      nullptr, ws, s);
+  return run_ffn_gemv(fn, x, B, wg, wu, wd, d, F, sirius::kFfnModeDense, 0.f, norm_eps, resid, y,
+                      nullptr, nullptr, ws, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace

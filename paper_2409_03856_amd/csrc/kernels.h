@@ -125,6 +125,14 @@ struct BatchLayout {
   size_t xp, hhi, hlo, uidx, ucnt, bidx, bcnt, part, total;  // workspace offsets / size
 };
 bool batch_path_ok(int B, int d, int F);
+// One FFN call of any batch (dense or threshold mode): the decode kernel at B = 1, the batched
+// kernels above when the shape allows them, else the older MFMA (dense, B >= 8) or small-batch
+// kernels. Shared by the C entry points and the model's forward pass.
+size_t ffn_any_ws(int B, int d, int F, int mode);
+hipError_t launch_ffn_any(const float* x, int B, const uint16_t* wg, const uint16_t* wu,
+                          const uint16_t* wd, int d, int F, int mode, float t, float norm_eps,
+                          const float* resid, float* y, int32_t* active_idx, int32_t* active_cnt,
+                          char* ws, hipStream_t s);
 // sparse: the segment layout (per-segment union blocks), used by every call with px = 3
 BatchLayout batch_layout(int B, int d, int F, int px);
 // mode: kFfnMode*; with active_idx (sparse modes) the per-token kept lists are written; top-k

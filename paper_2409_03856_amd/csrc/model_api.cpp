@@ -40,9 +40,7 @@ struct ModelLayout {
 };
 
 size_t ffn_ws_any(int B, int d, int F, bool sparse) {
-  if (B <= 1) return sirius::decode1_layout(d, F).total;
-  if (!sparse && B >= sirius::kMfmaMinBatch) return sirius::mfma_layout(B, d, F).total;
-  return sirius::gemv_layout(B, d, F).total;
+  return sirius::ffn_any_ws(B, d, F, sparse ? sirius::kFfnModeThreshold : sirius::kFfnModeDense);
 }
 
 ModelLayout model_layout(const sirius_model* m, int nmax) {
@@ -118,23 +116,9 @@ hipError_t ffn_any(const float* x, int B, const uint16_t* wg, const uint16_t* wu
                    const uint16_t* wd, int d, int F, bool sparse, float t, float eps,
                    const float* resid, float* y, int32_t* aidx, int32_t* acnt, char* ws,
                    hipStream_t s) {
-  const int mode = sparse ? sirius::kFfnModeThreshold : sirius::kFfnModeDense;
-  if (B == 1)
-    return sirius::launch_ffn_decode1(x, wg, wu, wd, d, F, mode, t, eps, resid, y, aidx, acnt, ws,
-                                      sirius::decode1_layout(d, F), s);
-  if (!sparse && B >= sirius::kMfmaMinBatch)
-    return sirius::launch_ffn_mfma(x, B, wg, wu, wd, d, F, eps, resid, y, ws,
-                                   sirius::mfma_layout(B, d, F), s);
-  const sirius::GemvLayout L = sirius::gemv_layout(B, d, F);
-  for (int b0 = 0; b0 < B; b0 += L.bc) {
-    const int nb = std::min(L.bc, B - b0);
-    hipError_t e = sirius::launch_ffn_gemv(
-        x + (size_t)b0 * d, nb, wg, wu, wd, d, F, mode, t, eps, resid + (size_t)b0 * d,
-        y + (size_t)b0 * d, aidx ? aidx + (size_t)b0 * F : nullptr, acnt ? acnt + b0 : nullptr, ws,
-        L, s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  return sirius::launch_ffn_any(x, B, wg, wu, wd, d, F,
+                                sparse ? sirius::kFfnModeThreshold : sirius::kFfnModeDense, t, eps,
+                                resid, y, aidx, acnt, ws, s);
 }
 
 // One pass over n tokens at the device-held position. Active lists (sparse only) go to
