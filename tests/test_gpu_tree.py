@@ -203,3 +203,12 @@ def test_equal_advances_keep_the_lowest_slot(sr):
     best, acc, nxt, _ = sr.sirius_tree_verify(dev_f32(np.ascontiguousarray(lg[:, : k * w])), dev_i32(tk),
                                               dev_i32(pa), 0.5, 1.0, bonus=False)
     assert (int(host(best)[0]), int(host(acc)[0]), int(host(nxt)[0])) == (0, k, -1)
+
+
+@pytest.mark.parametrize("bsz", [256, 257])
+def test_many_trees(sr, bsz):
+    """Hundreds of trees (one scan workgroup each), two calls in a row."""
+    for rep in range(2):
+        lg, tk, pa = tree_verify_inputs(700 + bsz + rep, bsz, 3, 2, 300, 2.0, bonus=True)
+        say(f"tree verify B={bsz} rep={rep}")
+        _verify_and_check(sr, lg, tk, pa, 0.1, 1.0, True)

@@ -100,3 +100,13 @@ def test_long_rows_cap_the_segment_count(sr):
         say(f"verify V={v}")
         lg, dr = verify_inputs(40, 2, 1, v, 3.0, rows=rows, calibrated=True)
         _run_and_check(sr, lg, dr, 0.1, 1.0)
+
+
+@pytest.mark.parametrize("bsz", [255, 256, 257, 300])
+def test_many_batch_entries(sr, bsz):
+    """Hundreds of batch entries (one scan workgroup each), two calls in a row."""
+    k, v = VERIFY_TINY.k, VERIFY_TINY.vocab
+    for rep in range(2):
+        say(f"verify B={bsz} rep={rep}")
+        lg, dr = verify_inputs(900 + bsz + rep, bsz, k, v, VERIFY_TINY.logit_var, rows=k + 1)
+        _run_and_check(sr, lg, dr, 0.1, 1.0)
