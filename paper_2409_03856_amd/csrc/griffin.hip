@@ -6,7 +6,7 @@
 //                         accumulation). Workgroup tile 256 tokens x 112 neurons (eight
 //                         waves of 64 x 56, two per SIMD, one workgroup per CU: the 256
 //                         tiles of a 512-token prompt at d_ff = 14336 fill the chip once),
-//                         K through a four-slot LDS ring of 32-wide stages filled by direct
+//                         K through a five-slot LDS ring of 32-wide stages filled by direct
 //                         global-to-LDS loads, the next stage's operands read while the
 //                         current one is multiplied; the token tiles of a neuron tile run on
 //                         one XCD together so its weights are read from HBM once. For the
