@@ -15,15 +15,17 @@
 //  griffin_rownorm_kernel ||z_t||^2 per token (normalised variant only).
 //  griffin_score_kernel   s_i = sqrt(sum_t z_ti^2 / ||z_t||^2) (normalised variant only).
 //  griffin_tile_score_kernel  plain statistic: s_i = sqrt of the tile sums in order.
-//  griffin_topk_kernel    one workgroup: the k-th largest score by a bitwise search and
-//                         the k neurons of largest score (equal scores: lower index first)
-//                         in ascending index order.
+//  griffin_topk_kernel    one workgroup: the k-th largest score by a radix select (the bits
+//                         every score shares, then digits of at most 11 bits below them,
+//                         radix_select.h) and the k neurons of largest
+//                         score (equal scores: lower index first) in ascending index order.
 //  condense_kernel        copies the selected rows of the three matrices.
 #include <math.h>
 
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "radix_select.h"
 #include "ring.h"
 
 namespace sirius {
@@ -317,27 +319,6 @@ __global__ __launch_bounds__(256) void griffin_score_kernel(const float* __restr
   scores[i] = (float)sqrt(s);
 }
 
-// Block-wide exclusive scan for 1024 threads (16 waves).
-__device__ __forceinline__ int scan1024(int v, int* s_tmp, int* total) {
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-  int incl = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
-  if (lane == kWave - 1) s_tmp[wave] = incl;
-  __syncthreads();
-  int off = 0, tot = 0;
-  for (int w = 0; w < 16; ++w) {
-    if (w < wave) off += s_tmp[w];
-    tot += s_tmp[w];
-  }
-  *total = tot;
-  __syncthreads();
-  return off + incl - v;
-}
-
 // s_i = sqrt(sum over the token tiles, in order, of the tile sums of z^2): the plain
 // statistic, from the product kernel's partials (spread over many CUs: one CU cannot read
 // the partials quickly enough on its own).
@@ -351,33 +332,21 @@ __global__ __launch_bounds__(256) void griffin_tile_score_kernel(const double* _
   scores[i] = (float)sqrt(a);
 }
 
-// Block-wide sum over 1024 threads; s_tmp holds 16 ints and is written once per call, so
-// consecutive calls alternate between two such arrays.
-__device__ __forceinline__ int sum1024(int v, int* s_tmp) {
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
-  if (lane == 0) s_tmp[wave] = v;
-  __syncthreads();
-  int tot = 0;
-#pragma unroll
-  for (int w = 0; w < 16; ++w) tot += s_tmp[w];
-  return tot;
-}
-
 // The k-th largest score and the ascending top-k list in one workgroup. Wave w owns
 // neurons [w W, w W + W) (W = d_ff / 16 rounded up to 64) and its lane l the neurons
-// w W + l + 64 j (coalesced loads), all in registers (J = W / 64 <= PER). The k-th largest is
-// the largest bit pattern u with at least k scores at or above it (non-negative floats order
-// like their bit patterns), built one bit at a time from the top with a block-wide count per
-// bit. The list is then written in ascending order: per-wave totals give each wave's base,
+// w W + l + 64 j (coalesced loads), all in registers (J = W / 64 <= PER). The k-th largest
+// score comes from the radix select over the scores' bit patterns (non-negative floats order
+// like their bit patterns; the bits every score shares first, then digits right below them);
+// a 31-step bitwise search with a block-wide count per bit took 28 us at d_ff = 14336. The list is then written in ascending
+// order: per-wave totals give each wave's base,
 // and inside a wave ballots over the lanes, slot j after slot j - 1. Equal scores at the
 // k-th value are taken lowest index first.
 template <int PER>
 __global__ __launch_bounds__(kTopkThreads) void griffin_topk_kernel(const float* __restrict__ scores,
                                                                     int F, int k,
                                                                     int32_t* __restrict__ sel) {
-  __shared__ int s_tmp[2][16];
+  __shared__ uint32_t s_hist[kHistCopies * kBinsMax];
+  __shared__ int s_w[2 * kSelWaves], s_sel[3];
   __shared__ int s_gt[16], s_eq[16], s_take[16];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int W = ((F + 15) / 16 + kWave - 1) / kWave * kWave;
@@ -390,13 +359,23 @@ __global__ __launch_bounds__(kTopkThreads) void griffin_topk_kernel(const float*
     v[j] = (j < J && i < F) ? scores[i] : -1.0f;
   }
 
-  uint32_t prefix = 0u;
-  for (int b = 30; b >= 0; --b) {
-    const uint32_t cand = prefix | (1u << b);
-    int c = 0;
+  // the k-th largest score: three digit passes of the radix select settle every value bit
+  uint32_t u[PER];
+  bool ok[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) c += (v[j] >= 0.0f && __float_as_uint(v[j]) >= cand) ? 1 : 0;
-    if (sum1024(c, s_tmp[b & 1]) >= k) prefix = cand;  // uniform over the block
+  for (int j = 0; j < PER; ++j) {
+    ok[j] = v[j] >= 0.0f;
+    u[j] = __float_as_uint(v[j]);
+  }
+  uint32_t prefix, pmask;
+  int kr = k, cnt;
+  int hib = radix_common_bits<PER>(u, ok, prefix, pmask, s_w);  // highest bit still open
+#pragma unroll 1
+  for (int pass = 0; hib >= 0; ++pass) {
+    const int bits = min(kDigitBitsMax, hib + 1), shift = hib + 1 - bits;
+    radix_digit_pass<PER>(u, ok, shift, bits, pass == 0 ? kHistCopies : 1, prefix, pmask, kr,
+                          &cnt, s_hist, s_w, s_sel);
+    hib = shift - 1;
   }
   const float kth = __uint_as_float(prefix);
 

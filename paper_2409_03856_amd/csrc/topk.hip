@@ -11,8 +11,9 @@
 //     activation mode, ffn_gemv.hip).
 //  2. topk_cut_kernel: one 1024-thread workgroup per token finds the k-th largest top-k key
 //     (|a| descending, then the lower index) by a most-significant-digit radix select over the
-//     bits of |a| in digits of 11, 11 and 9 bits (LDS histograms in eight copies; a block scan
-//     over the bins) until the digit holding it has at most 128 members, which are placed by a
+//     bits of |a| in digits of 11, 11 and 9 bits (LDS histograms, eight copies on the first
+//     digit; a block scan over the bins) until the digit holding it has at most 128 members,
+//     which are placed by a
 //     block scan and ranked by counting on the full key; when every value bit is decided
 //     first, a block scan over the threads' contiguous index ranges settles the ties.
 //  3. the keyed FFN pass: decode1_kernel (batch 1), cats_ring_kernel + down_ring_kernel
@@ -23,6 +24,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "profile.h"
+#include "radix_select.h"
 #include "topk.h"
 
 namespace sirius {
@@ -30,64 +32,29 @@ namespace {
 
 constexpr int kCutThreads = 1024;
 constexpr int kCutWaves = kCutThreads / kWave;  // 16
-// Digits of the bits of |a| (bit 31, the sign, is 0), most significant first: 11, 11 and 9 bits.
-// The first digit is the exponent and three mantissa bits; activations crowd into a few
-// exponents, and near the median into a narrow band of them (SiLU's negative lobe piles |a| up
-// below 0.28), so a few hundred to a few thousand values can share the first digit.
-constexpr int kDigitBits[3] = {11, 11, 9};
-constexpr int kDigitShift[3] = {20, 9, 0};
-constexpr int kBinsMax = 2048;
-constexpr int kCopies = 8;        // histogram copies: (lane / 16) + 4 (wave % 2)
-constexpr int kRankMax = 128;     // digit members ranked directly on the full key at most
-
-// Inclusive scan of one int per thread over the 1024-thread workgroup; *total is the sum.
-__device__ __forceinline__ int block_inclusive_scan_1024(int v, int* s_w, int* total) {
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-  int incl = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
-  if (lane == kWave - 1) s_w[wave] = incl;
-  __syncthreads();
-  int off = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < kCutWaves; ++w) {
-    const int c = s_w[w];
-    off += (w < wave) ? c : 0;
-    tot += c;
-  }
-  __syncthreads();
-  *total = tot;
-  return off + incl;
-}
+constexpr int kRankMax = 128;  // digit members ranked directly on the full key at most
 
 // Thread t owns neurons [t * PER, t * PER + PER) of the token (contiguous, for the tie scan).
-// Each pass histograms one digit of the values that match the digits decided so far (LDS
-// atomics; the first pass in eight copies, so that equal digits of one wave instruction collide
-// less), and a
-// block scan over the bins (thread t holds the two digits 2^bits - 1 - 2t and the next one
-// down, so the scan counts the values at or above them) finds the digit holding the k-th
-// largest and its rank inside the digit. As soon as that digit has at most kRankMax members,
-// they are placed in LDS by a block scan of the per-thread member counts and ranked by counting
-// on the full key; when every value bit is decided first, a block scan over the threads'
-// contiguous index ranges settles the ties.
+// Digit passes (radix_select.h) from bit 30 down narrow the k-th largest |a| until its digit has
+// at most kRankMax
+// members, which are placed in LDS by a block scan of the per-thread member counts and ranked by
+// counting on the full key; when every value bit is decided first, a block scan over the
+// threads' contiguous index ranges settles the ties.
 template <int PER>
 __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __restrict__ act,
                                                                int F, int k,
                                                                unsigned long long* __restrict__ cut) {
-  __shared__ uint32_t s_hist[kCopies * kBinsMax];
+  __shared__ uint32_t s_hist[kHistCopies * kBinsMax];
   __shared__ unsigned long long s_cand[kRankMax];
   __shared__ int s_w[kCutWaves];
   __shared__ int s_sel[3];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int copy = (lane >> 4) + 4 * (wave & 1);
+  const int tid = threadIdx.x;
   const int b = blockIdx.x;
   const float* a = act + (size_t)b * F;
   const int i0 = tid * PER;
 
   uint32_t v[PER];  // bits of |a|: for non-negative floats the bit order is the value order
+  bool ok[PER];
   if ((PER & 3) == 0 && (F & 3) == 0) {  // rows start 16-byte aligned: whole float4s
     const float4* a4 = reinterpret_cast<const float4*>(a + i0);
 #pragma unroll
@@ -102,55 +69,29 @@ __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __re
 #pragma unroll
     for (int j = 0; j < PER; ++j) v[j] = (i0 + j < F) ? __float_as_uint(fabsf(a[i0 + j])) : 0u;
   }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) ok[j] = i0 + j < F;
 
-  uint32_t prefix = 0u, pmask = 0u;
+  // activations spread over many exponents: the digits start at bit 30 (bit 31, the sign of |a|,
+  // is 0) without first settling common bits, which cost a block reduction and gained nothing
+  uint32_t prefix = 0u, pmask = 0x80000000u;
   int kr = k;  // rank (1-based, descending) of the wanted key among those matching the prefix
+  int hib = 30;  // highest bit still open
 #pragma unroll 1
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = kDigitShift[pass], nb = 1 << kDigitBits[pass];
-    const uint32_t dmask = (uint32_t)nb - 1u;
-    // the later passes see only the values that share the first digit: one copy is enough
-    const int ncopy = pass == 0 ? kCopies : 1, my_copy = pass == 0 ? copy : 0;
-    for (int i = tid; i < ncopy * nb; i += kCutThreads) s_hist[i] = 0u;
-    __syncthreads();
+  for (int pass = 0; hib >= 0; ++pass) {
+    const int bits = min(kDigitBitsMax, hib + 1), shift = hib + 1 - bits;
+    int cnt;
+    radix_digit_pass<PER>(v, ok, shift, bits, pass == 0 ? kHistCopies : 1, prefix, pmask, kr, &cnt,
+                          s_hist, s_w, s_sel);
+    hib = shift - 1;
+    if (hib >= 0 && cnt <= kRankMax) {  // uniform: place the digit's members, rank them
+      int nm = 0, tot;
 #pragma unroll
-    for (int j = 0; j < PER; ++j)
-      if (i0 + j < F && (v[j] & pmask) == prefix)
-        atomicAdd(&s_hist[my_copy * nb + ((v[j] >> shift) & dmask)], 1u);
-    __syncthreads();
-    const int d1 = nb - 1 - 2 * tid, d2 = d1 - 1;
-    int c1 = 0, c2 = 0;
-    if (d2 >= 0) {
-      for (int q = 0; q < ncopy; ++q) {
-        c1 += (int)s_hist[q * nb + d1];
-        c2 += (int)s_hist[q * nb + d2];
-      }
-    }
-    int tot;
-    const int incl = block_inclusive_scan_1024(c1 + c2, s_w, &tot);
-    const int before = incl - c1 - c2;
-    if (before < kr && kr <= before + c1) {
-      s_sel[0] = d1;
-      s_sel[1] = kr - before;
-      s_sel[2] = c1;
-    } else if (before + c1 < kr && kr <= incl) {
-      s_sel[0] = d2;
-      s_sel[1] = kr - before - c1;
-      s_sel[2] = c2;
-    }
-    __syncthreads();
-    prefix |= (uint32_t)s_sel[0] << shift;
-    pmask |= dmask << shift;
-    kr = s_sel[1];
-    const int cnt = s_sel[2];
-    if (pass < 2 && cnt <= kRankMax) {  // uniform: place the digit's members, rank them
-      int nm = 0;
-#pragma unroll
-      for (int j = 0; j < PER; ++j) nm += (i0 + j < F && (v[j] & pmask) == prefix) ? 1 : 0;
+      for (int j = 0; j < PER; ++j) nm += (ok[j] && (v[j] & pmask) == prefix) ? 1 : 0;
       int pos = block_inclusive_scan_1024(nm, s_w, &tot) - nm;
 #pragma unroll
       for (int j = 0; j < PER; ++j)
-        if (i0 + j < F && (v[j] & pmask) == prefix)
+        if (ok[j] && (v[j] & pmask) == prefix)
           s_cand[pos++] = ((unsigned long long)v[j] << 32) | (unsigned)(~(unsigned)(i0 + j));
       __syncthreads();
       if (tid < cnt) {  // cnt <= kRankMax <= kCutThreads; the keys are distinct
@@ -161,7 +102,6 @@ __global__ __launch_bounds__(kCutThreads) void topk_cut_kernel(const float* __re
       }
       return;
     }
-    __syncthreads();  // s_sel is read by every thread before the next pass writes it
   }
   // every value bit decided: prefix is the k-th largest |a|; the first kr neurons (by index)
   // equal to it are kept
