@@ -337,9 +337,9 @@ __global__ __launch_bounds__(256) void griffin_tile_score_kernel(const double* _
 // w W + l + 64 j (coalesced loads), all in registers (J = W / 64 <= PER). The k-th largest
 // score comes from the radix select over the scores' bit patterns (non-negative floats order
 // like their bit patterns; the bits every score shares first, then digits right below them);
-// a 31-step bitwise search with a block-wide count per bit took 28 us at d_ff = 14336. The list is then written in ascending
-// order: per-wave totals give each wave's base,
-// and inside a wave ballots over the lanes, slot j after slot j - 1. Equal scores at the
+// a 31-step bitwise search with a block-wide count per bit took 28 us at d_ff = 14336. The list
+// is then written in ascending order: per-wave totals give each wave's base, and inside a wave
+// ballots over the lanes, slot j after slot j - 1. Equal scores at the
 // k-th value are taken lowest index first.
 template <int PER>
 __global__ __launch_bounds__(kTopkThreads) void griffin_topk_kernel(const float* __restrict__ scores,

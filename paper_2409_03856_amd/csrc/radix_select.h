@@ -1,10 +1,11 @@
 // Most-significant-digit radix select over 32-bit patterns held by a 1024-thread workgroup
 // (PER values per thread), shared by the per-token top-k cut and the prompt top-k of Griffin.
 // The patterns are those of non-negative floats (|a|, scores), whose bit order is their value
-// order. The bits that every candidate shares are settled first (a block minimum and maximum);
-// the digits, of at most 11 bits, start right below them, so values that crowd into a narrow
-// range (prompt scores share their exponent and leading mantissa bits) still spread over the
-// first digit's bins.
+// order. radix_common_bits settles the bits every candidate shares (a block minimum and
+// maximum), so that digits of at most 11 bits can start right below them: values that crowd
+// into a narrow range (prompt scores share their exponent and leading mantissa bits) then still
+// spread over the first digit's bins. Values spread over many exponents (gate activations) skip
+// it and start their digits at bit 30.
 #pragma once
 
 #include <hip/hip_runtime.h>
