@@ -183,7 +183,9 @@ int sirius_cats_calibrate(const float* x_cal, int N, const uint16_t* w_gate, int
  * keeps the k neurons of largest s (equal scores: lower index first) and
  * copies their rows of all three matrices into the condensed matrices.
  *   x_prompt [T, d_model] bf16 bits; products are exact and accumulate in
- *            fp32 on MFMA.
+ *            fp32 on MFMA; z in fp32 with SiLU through the hardware exp2
+ *            and reciprocal (each within about 1 ulp), squares summed in
+ *            fp64.
  *   sel_idx  [k] int32 out, ascending.
  *   scores   [d_ff] fp32 out (s), or NULL.
  *   w_*_c    [k, d_model] bf16 out: row j = row sel_idx[j] of w_*.

@@ -87,15 +87,23 @@ __device__ __forceinline__ void tile_of(int id, int ntn, int ntm, int* n_tile, i
   }
 }
 
+// SiLU of a gate product in griffin_z's epilogue: exp through v_exp_f32 and a v_rcp_f32
+// reciprocal (each within about 1 ulp) instead of the range-reduced expf and IEEE division
+__device__ __forceinline__ float z_silu(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f));
+}
+
 // Z tile (Z != nullptr) or, for the plain statistic, the tile's partial sums of z^2 over its
 // tokens per neuron (part[m_tile][n], fp64) without storing Z.
 //
-// Tile kZT tokens x kZN neurons. The weight rows of the tile are interleaved in blocks of 16:
-// block j holds gate rows n0 + 8j .. + 7, then up rows n0 + 8j .. + 7, so that one 16-column
-// MFMA block carries the gate and up products of 8 neurons, the up product of neuron 8j + p in
-// the lane 8 above the gate product's. Wave (wm, wn) multiplies token rows 64 wm .. + 63 by
-// weight blocks 7 wn .. + 6: 4 x 7 v_mfma_f32_16x16x32_bf16 per K stage into 112 fp32
-// accumulators per lane. The two waves of a SIMD take turns on its MFMA unit.
+// Tile kZT tokens x kZN neurons. The MFMAs take weight rows as the M side and tokens as the N
+// side, and the weight rows of the tile alternate gate and up: row 2p of block j (16 rows) is
+// the gate row of neuron n0 + 8j + p, row 2p + 1 its up row. A lane of a 16 x 16 result holds
+// four consecutive rows of one token column, so it holds the gate and up products of two
+// neurons side by side: every lane forms z from its own registers. Wave (wm, wn) multiplies
+// weight blocks 7 wn .. + 6 by token rows 64 wm .. + 63: 7 x 4 v_mfma_f32_16x16x32_bf16 per K
+// stage into 112 fp32 accumulators per lane. The two waves of a SIMD take turns on its MFMA
+// unit.
 //
 // K goes through a five-slot LDS ring of 32-wide stages (30 KiB each) filled by direct
 // global-to-LDS 16-byte loads (three or four per thread per stage, no staging registers): while
@@ -135,9 +143,9 @@ __global__ __launch_bounds__(kZThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
     if (r < kZT) {
       row = X + (size_t)min(t0 + r, T - 1) * d;
     } else {
-      const int w = r - kZT, j = w >> 4, p = w & 15;
-      const int n = min(n0 + 8 * j + (p & 7), F - 1);
-      row = (p < 8 ? Wg : Wu) + (size_t)n * d;
+      const int w = r - kZT;  // weight row: neuron w / 2 of the tile, gate (even) or up (odd)
+      const int n = min(n0 + (w >> 1), F - 1);
+      row = ((w & 1) ? Wu : Wg) + (size_t)n * d;
     }
     src[q] = row;
     chunk_k[q] = 8 * c;
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(kZThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
     }
   };
 
-  floatx4_t acc[kZMB][kZWB];
+  floatx4_t acc[kZMB][kZWB];  // [token block][weight block]: rows = weights, columns = tokens
 #pragma unroll
   for (int mt = 0; mt < kZMB; ++mt)
 #pragma unroll
@@ -207,7 +215,7 @@ __global__ __launch_bounds__(kZThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
     for (int nb = 0; nb < kZWB; ++nb)
 #pragma unroll
       for (int mt = 0; mt < kZMB; ++mt)
-        acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[mt], f.b[nb], acc[mt][nb], 0, 0, 0);
+        acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.b[nb], f.a[mt], acc[mt][nb], 0, 0, 0);
   };
 
   // iteration b: fragments of stage b are in `cur`, stage b lives in slot b % kZSlots. Wait for
@@ -240,46 +248,53 @@ __global__ __launch_bounds__(kZThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
   }
   if (b < nblk) step(f0, f1, b);
 
-  // C layout: lane l holds column l % 16 of each 16-column block (gate of neuron 8 nb + l % 16
-  // for l % 16 < 8, up of neuron 8 nb + l % 16 - 8 otherwise) and tokens 4 (l / 16) + i of each
-  // 16-token block; the up product of the gate lane's neuron sits 8 lanes above.
-  const bool gate_lane = (lane & 8) == 0;
+  // C layout of a 16 x 16 block: lane l holds token column l % 16 and weight rows 4 (l / 16) + i,
+  // i = 0..3: the gate and up products of neurons 8 nb + 2 (l / 16) (i = 0, 1) and
+  // 8 nb + 2 (l / 16) + 1 (i = 2, 3).
+  const int tcol = lane & 15, grp = lane >> 4;
   if (Z != nullptr) {
 #pragma unroll
     for (int nb = 0; nb < kZWB; ++nb) {
-      const int n = n0 + 8 * (kZWB * wn + nb) + (lane & 7);
+      const int n = n0 + 8 * (kZWB * wn + nb) + 2 * grp;
 #pragma unroll
-      for (int mt = 0; mt < kZMB; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float g = acc[mt][nb][i];
-          const float u = __shfl_xor(g, 8, kWave);
-          const int t = t0 + wm * kZWT + 16 * mt + 4 * fc + i;
-          if (gate_lane && t < T && n < F) Z[(size_t)t * F + n] = silu(g) * u;
-        }
+      for (int mt = 0; mt < kZMB; ++mt) {
+        const int t = t0 + wm * kZWT + 16 * mt + tcol;
+        const floatx4_t& c = acc[mt][nb];
+        if (t < T && n < F) Z[(size_t)t * F + n] = z_silu(c[0]) * c[1];
+        if (t < T && n + 1 < F) Z[(size_t)t * F + n + 1] = z_silu(c[2]) * c[3];
+      }
     }
     return;
   }
-  // sum of z^2 over this tile's tokens, per neuron, in a fixed order: the lane's 16 tokens, then
-  // the four lane groups, then the four token quarters of the tile. Tokens past T are left out.
+  // sum of z^2 over this tile's tokens, per neuron, in a fixed order: the lane's 4 tokens, then
+  // the 16 token columns (xor tree), then the four token quarters of the tile. Tokens past T
+  // are left out.
   __syncthreads();  // every wave is done with the ring: its first slot holds the wave sums
   double* s_part = reinterpret_cast<double*>(s_ring);  // [token quarter][kZN]
 #pragma unroll
   for (int nb = 0; nb < kZWB; ++nb) {
-    double sum = 0.0;
+    double s0 = 0.0, s1 = 0.0;
 #pragma unroll
-    for (int mt = 0; mt < kZMB; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float g = acc[mt][nb][i];
-        const float u = __shfl_xor(g, 8, kWave);
-        const int t = t0 + wm * kZWT + 16 * mt + 4 * fc + i;
-        const double z = (double)(silu(g) * u);
-        if (t < T) sum += z * z;
+    for (int mt = 0; mt < kZMB; ++mt) {
+      const int t = t0 + wm * kZWT + 16 * mt + tcol;
+      const floatx4_t& c = acc[mt][nb];
+      const double z0 = (double)(z_silu(c[0]) * c[1]);
+      const double z1 = (double)(z_silu(c[2]) * c[3]);
+      if (t < T) {
+        s0 += z0 * z0;
+        s1 += z1 * z1;
       }
-    sum += __shfl_xor(sum, 16, kWave);
-    sum += __shfl_xor(sum, 32, kWave);
-    if (lane < 8) s_part[wm * kZN + 8 * (kZWB * wn + nb) + lane] = sum;
+    }
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+      s0 += __shfl_xor(s0, m, kWave);
+      s1 += __shfl_xor(s1, m, kWave);
+    }
+    if (tcol == 0) {
+      const int nl = 8 * (kZWB * wn + nb) + 2 * grp;
+      s_part[wm * kZN + nl] = s0;
+      s_part[wm * kZN + nl + 1] = s1;
+    }
   }
   __syncthreads();
   if (tid < kZN && n0 + tid < F)
