@@ -17,8 +17,9 @@
 //                    compaction and the separate up phase drop out);
 //                  * W_down rows of the kept neurons: thread (p, c) owns the eight output
 //                    columns of 16-byte chunk c and the kept rows p, p + P, ... with eight
-//                    row chunks in flight; the P row groups are summed in a fixed order
-//                    into the segment's partial y.
+//                    row chunks in flight (dense: the first eight requested before the
+//                    barrier that completes h); the P row groups are summed in a fixed
+//                    order into the segment's partial y.
 //  reduce_kernel   (ffn_gemv.hip) y = resid + the segment partials in order, and the
 //                  ascending active list from the per-segment lists.
 //
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
     }
   }
   if (MODE == kModeAct) return;  // the activations are all this mode writes
-  __syncthreads();
+  if (!kFused) __syncthreads();
 
   // ---- ascending compaction of the kept rows: wave ballot + popcount, wave offsets in LDS
   int nk = nr;
@@ -231,22 +232,36 @@ __global__ __launch_bounds__(kThreads) void decode1_kernel(
       if (lane == 0) s_h[k1] = s_a[s_list[k1]] * u1;
     }
   }
+  const int P = kThreads / nch;  // row groups (nch <= 1024)
+  const int c = tid % nch, p = tid / nch;
+  // dense: the first W_down rows are known before h, so they are requested before the barrier
+  uint4 wpre[kDownUnroll];
+  if (kFused && p < P) {
+#pragma unroll
+    for (int u = 0; u < kDownUnroll; ++u) {
+      const int k = p + u * P;
+      wpre[u] = (k < nk) ? ld_stream(wd + (size_t)(r0 + k) * nch + c) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
   __syncthreads();  // s_h complete; x no longer needed
 
   // ---- W_down rows of the kept neurons: thread (p, c), rows p, p + P, ...
-  const int P = kThreads / nch;  // row groups (nch <= 1024)
-  const int c = tid % nch, p = tid / nch;
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
   if (p < P) {
     for (int k0 = p; k0 < nk; k0 += P * kDownUnroll) {
       uint4 w[kDownUnroll];
+      if (kFused && k0 == p) {
 #pragma unroll
-      for (int u = 0; u < kDownUnroll; ++u) {
-        const int k = k0 + u * P;
-        w[u] = (k < nk) ? ld_stream(wd + (size_t)(r0 + s_list[k]) * nch + c)
-                        : make_uint4(0u, 0u, 0u, 0u);
+        for (int u = 0; u < kDownUnroll; ++u) w[u] = wpre[u];
+      } else {
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+          const int k = k0 + u * P;
+          w[u] = (k < nk) ? ld_stream(wd + (size_t)(r0 + s_list[k]) * nch + c)
+                          : make_uint4(0u, 0u, 0u, 0u);
+        }
       }
 #pragma unroll
       for (int u = 0; u < kDownUnroll; ++u) {
