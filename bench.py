@@ -80,6 +80,7 @@ ATT_H, ATT_HKV, ATT_HD, ATT_L, ATT_P = 32, 8, 128, 4096, 2048
 N_LOGIT_BUFS = 4
 SWEEP = (0.0, 0.4, 0.5, 0.65, 0.8)
 SWEEP_CALLS = 40
+B2B_CALLS = 20             # back-to-back calls per row in the pass after the timed region
 BATCHED = (4, 16)          # batched threshold-sparse decode rows (tokens per call)
 TREE_TOKENS = 64           # the full model's pass over a drafted tree of kernel size 16 x width 4
 STACK8_LAYERS, STACK70_LAYERS = 32, 80
@@ -433,6 +434,54 @@ def main():
             kern[name] = {"avg_us": round(tot * 1e3 / n, 3), "launches": n}
     sr.sirius_profile_reset()
 
+    # ------------------------------------------------------------------ back-to-back pass
+    # Each stateless row's call repeated B2B_CALLS times in a row (layer copies rotated as in the
+    # step) between one pair of events: what the call sustains on its own. Its in-step time also
+    # carries what the row before it leaves behind (writes still draining to HBM, the row-boundary
+    # event markers). Counts go to a scratch tensor, so the step's logs stay as the timed region
+    # wrote them.
+    b2b_cnt = torch.zeros((1,), dtype=torch.int32, device=dev)
+    b2b_calls = {
+        "cats": lambda s: sr.sirius_ffn_cats(xs[s % N_DECODE:s % N_DECODE + 1], *layers[s % NCOPY],
+                                             thresholds[s % NCOPY], y=y, active_idx=act_idx, active_cnt=b2b_cnt),
+        "rmsnorm": lambda s: sr.sirius_rmsnorm(y, 1e-5, out=hn),
+        "griffin": lambda s: sr.sirius_griffin_select(prompt, *layers[(s + 2) % NCOPY], k_keep, want_scores=False,
+                                                      sel_idx=g_sel, w_gate_c=g_c[0], w_up_c=g_c[1], w_down_c=g_c[2]),
+        "condensed": lambda s: sr.sirius_ffn_condensed(xs[(s + 1) % N_DECODE:(s + 1) % N_DECODE + 1],
+                                                       *cond[(s + 4) % NCOPY], y=yc),
+        "dense": lambda s: sr.sirius_ffn_dense(xs[(s + 2) % N_DECODE:(s + 2) % N_DECODE + 1],
+                                               *layers[(s + 6) % NCOPY], y=yd),
+        "dense16": lambda s: sr.sirius_ffn_dense(x16, *layers[(s + 3) % NCOPY], y=y16),
+        "verify": lambda s: sr.sirius_verify_accept(logits[s % N_LOGIT_BUFS], drafted[s % N_LOGIT_BUFS], 0.1, 1.0,
+                                                    accept_len=acc, next_token=nxt, want_p=False),
+        "tree_build": lambda s: sr.sirius_tree_build_step(tb_logits[s % N_LOGIT_BUFS], TREE_W, tb_cum[s % N_LOGIT_BUFS],
+                                                          1.0, tokens=tb_out[0], parents=tb_out[1], cum_ll_out=tb_out[2]),
+        "tree_verify": lambda s: sr.sirius_tree_verify(tv_logits[s % N_LOGIT_BUFS], tv_tok[s % N_LOGIT_BUFS],
+                                                       tv_par[s % N_LOGIT_BUFS], 0.1, 1.0, bonus=True,
+                                                       best_leaf=tv_out[0], accept_len=tv_out[1],
+                                                       next_token=tv_out[2], want_q=False),
+        "topk": lambda s: sr.sirius_ffn_topk(xs[(s + 3) % N_DECODE:(s + 3) % N_DECODE + 1], *layers[(s + 5) % NCOPY],
+                                             k_keep, y=yt, active_idx=act_t, active_cnt=b2b_cnt),
+        "cats70b": lambda s: sr.sirius_ffn_cats(xs70[s % N_DECODE:s % N_DECODE + 1], *layers70[s % NCOPY70],
+                                                t70[s % NCOPY70], y=y70, active_idx=act70, active_cnt=b2b_cnt),
+        "dense64": lambda s: sr.sirius_ffn_dense(x64, *layers[(s + 7) % NCOPY], y=y64),
+    }
+    for j, bsz in enumerate(BATCHED):
+        b2b_calls[f"cats_b{bsz}"] = (lambda j_, b_: lambda s: sr.sirius_ffn_cats(
+            batched_window(b_, s), *layers[(s + 1 + j_) % NCOPY], thresholds[(s + 1 + j_) % NCOPY], y=yb[b_],
+            want_active=False))(j, bsz)
+    b2b_us = {}
+    for r, fn in b2b_calls.items():
+        for i in range(2):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(B2B_CALLS):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        b2b_us[r] = e0.elapsed_time(e1) * 1e3 / B2B_CALLS
+
     # sparsity sweep of the headline layer: per-token CATS decode at several calibrated
     # sparsities (0 = every neuron kept, through the same kernels), to check that the time of
     # the kept up and down rows scales with the density 1 - s while the dense gate stays fixed
@@ -555,6 +604,9 @@ def main():
         gbps = row_bytes[r] / (us * 1e-6) / 1e9
         rows_out[r] = {"us": round(us, 2), "alg_bytes": int(row_bytes[r]), "gbps": round(gbps, 1),
                        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        if r in b2b_us:
+            rows_out[r]["us_b2b"] = round(b2b_us[r], 2)
+            rows_out[r]["hbm_frac_b2b"] = round(row_bytes[r] / (b2b_us[r] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     for bsz in BATCHED:
         rows_out[f"cats_b{bsz}"].update(union[bsz])
         rows_out[f"cats_b{bsz}"]["us_per_token"] = round(rows_out[f"cats_b{bsz}"]["us"] / bsz, 2)
@@ -618,6 +670,9 @@ def main():
             "copy_ceiling_gbps": copy_gbps,
         },
         "rows": rows_out,
+        "rows_timing": "us: median over the timed steps of the row's own span between row-boundary events inside "
+                       "the step; us_b2b: the same call repeated B2B_CALLS times back to back (layer copies "
+                       "rotated) after the timed region, per call",
         "stacks": stacks,
         "acceptance": accept,
         "kernels": kern,
