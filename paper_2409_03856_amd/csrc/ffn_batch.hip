@@ -288,14 +288,17 @@ constexpr int ks_for(int rows, int lds) { return rows * 256 * 3 <= lds ? 128 : 6
 constexpr int kGuLds = 144 * 1024;
 constexpr int kCatsLds = 124 * 1024;
 
-template <int TB>
+// NPM: neurons per segment at most (kSegN, or kSegSmall for short segments, whose smaller slots
+// leave room for a deeper ring)
+constexpr int kSegSmall = 32;
+template <int TB, int NPM>
 struct GuGeom {
-  static constexpr int kRowsData = 2 * kSegN + TB;
+  static constexpr int kRowsData = 2 * NPM + TB;
   using G = RingGeom<kRowsData, ks_for(kRowsData, kGuLds), kGuLds>;
 };
-template <int TB>
+template <int TB, int NPM>
 struct CatsGeom {
-  static constexpr int kRowsData = kSegN + 3 * TB;
+  static constexpr int kRowsData = NPM + 3 * TB;
   using G = RingGeom<kRowsData, ks_for(kRowsData, kCatsLds), kCatsLds>;
 };
 
@@ -304,14 +307,14 @@ struct CatsGeom {
 // TB token rows (zeros past B). Wave w: 16-neuron tile w / 2 of the gate (w even) or up (w odd)
 // rows; its A operand for tile mt reads token row min(16 mt + r, TB - 1), so a tile's padding
 // tokens (never stored) repeat a loaded row instead of occupying slot rows.
-template <int TB>
+template <int TB, int NPM>
 __global__ __launch_bounds__(kBT) void gu_ring_kernel(const uint16_t* __restrict__ xp, int B,
                                                       const uint16_t* __restrict__ wg,
                                                       const uint16_t* __restrict__ wu, int d,
                                                       int F, int hs, int np, int sp,
                                                       uint16_t* __restrict__ hhi,
                                                       uint16_t* __restrict__ hlo) {
-  using G = typename GuGeom<TB>::G;
+  using G = typename GuGeom<TB, NPM>::G;
   constexpr int MT = (TB + 15) / 16, KS = G::kRowBytes / 2;
   extern __shared__ __attribute__((aligned(16))) unsigned char ring[];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
@@ -394,14 +397,14 @@ constexpr int kModeThr = 0, kModeAct = 1, kModeKeyed = 2, kModeAll = 3;
 // (kModeAll keeps every neuron: the dense and condensed FFN of small batches on the exact input,
 // through the same kernels, and so the same sums, as the threshold path with t < 0.)
 
-template <int TB, int MODE>
+template <int TB, int MODE, int NPM>
 __global__ __launch_bounds__(kBT) void cats_ring_kernel(
     const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
     const uint16_t* __restrict__ wu, int d, int F, int np, float t, float* __restrict__ act,
     const unsigned long long* __restrict__ cut, uint16_t* __restrict__ hhi,
     uint16_t* __restrict__ hlo, int hs, int sp, int32_t* __restrict__ uidx,
     int32_t* __restrict__ ucnt, int32_t* __restrict__ bidx, int32_t* __restrict__ bcnt) {
-  using G = typename CatsGeom<TB>::G;
+  using G = typename CatsGeom<TB, NPM>::G;
   constexpr int MT = (TB + 15) / 16, KS = G::kRowBytes / 2;
   constexpr int kMpad = 16 * MT;
   extern __shared__ __attribute__((aligned(16))) unsigned char ring[];
@@ -434,7 +437,9 @@ __global__ __launch_bounds__(kBT) void cats_ring_kernel(
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     const int wrow = 16 * tau + fr;  // past np: never stored
+    const bool active = 16 * tau < np;  // a tile past the segment's rows skips its MFMAs
     run_ring<G>(ring, rg, nblk, d, np, [&](const unsigned char* slot) {
+      if (!active) return;
       bf16x8_t bw[kHalf], ax[kHalf][3][MT];
 #pragma unroll
       for (int i2 = 0; i2 < kHalf; ++i2) {  // every operand of the block first, then the MFMAs
@@ -770,30 +775,51 @@ hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
   return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
+template <int TB, int NPM>
+hipError_t launch_gu_np(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                        const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
+                        uint16_t* hlo) {
+  using G = typename GuGeom<TB, NPM>::G;
+  static const hipError_t attr =
+      allow_dynamic_lds(reinterpret_cast<const void*>(gu_ring_kernel<TB, NPM>), kGuLds);
+  if (attr != hipSuccess) return attr;
+  klaunch(gu_ring_kernel<TB, NPM>, L.nseg, kBT, (uint32_t)(G::kSlots * G::kSlotBytes), stream, xp, B,
+          wg, wu, d, F, L.hs, L.np, L.sp, hhi, hlo);
+  return hipGetLastError();
+}
+// short segments (np <= kSegSmall) of the small token classes take the deeper ring
 template <int TB>
 hipError_t launch_gu(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
                      const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
                      uint16_t* hlo) {
-  using G = typename GuGeom<TB>::G;
-  static const hipError_t attr = allow_dynamic_lds(reinterpret_cast<const void*>(gu_ring_kernel<TB>), kGuLds);
-  if (attr != hipSuccess) return attr;
-  klaunch(gu_ring_kernel<TB>, L.nseg, kBT, (uint32_t)(G::kSlots * G::kSlotBytes), stream, xp, B, wg,
-          wu, d, F, L.hs, L.np, L.sp, hhi, hlo);
-  return hipGetLastError();
+  if (TB <= 16 && L.np <= kSegSmall)
+    return launch_gu_np<TB, (TB <= 16 ? kSegSmall : kSegN)>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
+  return launch_gu_np<TB, kSegN>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
 }
 
+template <int TB, int MODE, int NPM>
+hipError_t launch_cats_np(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                          const uint16_t* wg, const uint16_t* wu, int d, int F, float t, float* act,
+                          const unsigned long long* cut, uint16_t* hhi, uint16_t* hlo,
+                          int32_t* uidx, int32_t* ucnt, int32_t* bidx, int32_t* bcnt) {
+  using G = typename CatsGeom<TB, NPM>::G;
+  static const hipError_t attr =
+      allow_dynamic_lds(reinterpret_cast<const void*>(cats_ring_kernel<TB, MODE, NPM>), kCatsLds);
+  if (attr != hipSuccess) return attr;
+  klaunch(cats_ring_kernel<TB, MODE, NPM>, L.nseg, kBT, (uint32_t)(G::kSlots * G::kSlotBytes), stream,
+          xp, B, wg, wu, d, F, L.np, t, act, cut, hhi, hlo, L.hs, L.sp, uidx, ucnt, bidx, bcnt);
+  return hipGetLastError();
+}
 template <int TB, int MODE>
 hipError_t launch_cats(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
                        const uint16_t* wg, const uint16_t* wu, int d, int F, float t, float* act,
                        const unsigned long long* cut, uint16_t* hhi, uint16_t* hlo,
                        int32_t* uidx, int32_t* ucnt, int32_t* bidx, int32_t* bcnt) {
-  using G = typename CatsGeom<TB>::G;
-  static const hipError_t attr =
-      allow_dynamic_lds(reinterpret_cast<const void*>(cats_ring_kernel<TB, MODE>), kCatsLds);
-  if (attr != hipSuccess) return attr;
-  klaunch(cats_ring_kernel<TB, MODE>, L.nseg, kBT, (uint32_t)(G::kSlots * G::kSlotBytes), stream,
-          xp, B, wg, wu, d, F, L.np, t, act, cut, hhi, hlo, L.hs, L.sp, uidx, ucnt, bidx, bcnt);
-  return hipGetLastError();
+  if (TB <= 16 && L.np <= kSegSmall)
+    return launch_cats_np<TB, MODE, (TB <= 16 ? kSegSmall : kSegN)>(L, stream, xp, B, wg, wu, d, F, t, act,
+                                                                     cut, hhi, hlo, uidx, ucnt, bidx, bcnt);
+  return launch_cats_np<TB, MODE, kSegN>(L, stream, xp, B, wg, wu, d, F, t, act, cut, hhi, hlo, uidx,
+                                         ucnt, bidx, bcnt);
 }
 
 hipError_t launch_gu_tb(int B, const BatchLayout& L, hipStream_t stream, const uint16_t* xp,
