@@ -301,6 +301,11 @@ struct CatsGeom {
   static constexpr int kRowsData = NPM + 3 * TB;
   using G = RingGeom<kRowsData, ks_for(kRowsData, kCatsLds), kCatsLds>;
 };
+template <int TB, int NPM>
+struct AllGeom {
+  static constexpr int kRowsData = 2 * NPM + 3 * TB;
+  using G = RingGeom<kRowsData, ks_for(kRowsData, kCatsLds), kCatsLds>;
+};
 
 // ---- dense gate/up on the bf16-rounded input: one workgroup per segment of np neurons over
 // F16 rows (rows past d_ff give h = 0). Slot rows: gate rows [0, np), up rows [np, 2 np), then
@@ -386,6 +391,112 @@ __global__ __launch_bounds__(kBT) void gu_ring_kernel(const uint16_t* __restrict
     }
   }
   if (blockIdx.x == gridDim.x - 1) zero_h_tail(hhi, hlo, hs, gridDim.x * sp, 16 * MT);
+}
+
+// ---- every neuron kept (the dense and condensed FFN of small batches on the exact input) in one
+// ring pass over the segment's gate rows [0, np), up rows [np, 2 np) and the token rows (piece p,
+// token m) at 2 np + p TB + m. Wave w keeps the gate and up sums of 16-neuron tile w & 3 over the
+// K steps of half w >> 2 of each block, in the order in which the two-phase segment kernel below
+// forms them (same K blocks, steps, pieces and token tiles; the halves added in the same order),
+// so its results are bitwise those of the threshold path with t < 0, with one pass over K instead
+// of two.
+template <int TB, int NPM>
+__global__ __launch_bounds__(kBT) void all_ring_kernel(
+    const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int np, uint16_t* __restrict__ hhi,
+    uint16_t* __restrict__ hlo, int hs, int sp, int32_t* __restrict__ uidx,
+    int32_t* __restrict__ ucnt) {
+  using G = typename AllGeom<TB, NPM>::G;
+  static_assert(G::kRowBytes == CatsGeom<TB, NPM>::G::kRowBytes,
+                "the K blocks of the two-phase kernel, and so its sums");
+  constexpr int MT = (TB + 15) / 16, KS = G::kRowBytes / 2;
+  constexpr int kMpad = 16 * MT;
+  extern __shared__ __attribute__((aligned(16))) unsigned char ring[];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int fr = lane & 15, grp = lane >> 4;
+  const int seg = blockIdx.x, nseg = gridDim.x;
+  const int r0 = seg * np;
+  const int nr = min(np, F - r0);  // neurons of this segment (>= 1)
+  const int nblk = (d + KS - 1) / KS;
+  const int tau = wave & 3, kap = wave >> 2;
+  constexpr int kSteps = KS / 32;
+  constexpr int kHalf = kSteps / 2;
+  const int x0 = 2 * np;  // first token row of a slot
+
+  Ring<G> rg(tid, wave, [&](int r) -> const uint16_t* {
+    if (r < np) return wg + (size_t)(r0 + min(r, nr - 1)) * d;
+    if (r < x0) return wu + (size_t)(r0 + min(r - np, nr - 1)) * d;
+    if (r < x0 + 3 * TB) {
+      const int p = (r - x0) / TB, m = (r - x0) % TB;
+      return m < B ? xp + ((size_t)p * kMpad + m) * d : nullptr;
+    }
+    return nullptr;
+  });
+  floatx4_t accg[MT], accu[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    accg[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    accu[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  const int wrow = 16 * tau + fr;  // past np: never stored
+  const bool active = 16 * tau < np;
+  run_ring<G>(ring, rg, nblk, d, x0, [&](const unsigned char* slot) {
+    if (!active) return;
+    bf16x8_t bg[kHalf], bu[kHalf], ax[kHalf][3][MT];
+#pragma unroll
+    for (int i2 = 0; i2 < kHalf; ++i2) {
+      const int c = 4 * (kap * kHalf + i2) + grp;
+      bg[i2] = *reinterpret_cast<const bf16x8_t*>(slot + wrow * G::kRowBytes + 16 * swz(wrow, c));
+      bu[i2] = *reinterpret_cast<const bf16x8_t*>(slot + (np + wrow) * G::kRowBytes + 16 * swz(np + wrow, c));
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int xr = x0 + p * TB + min(16 * mt + fr, TB - 1);
+          ax[i2][p][mt] = *reinterpret_cast<const bf16x8_t*>(slot + xr * G::kRowBytes + 16 * swz(xr, c));
+        }
+    }
+#pragma unroll
+    for (int i2 = 0; i2 < kHalf; ++i2)
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          accg[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ax[i2][p][mt], bg[i2], accg[mt], 0, 0, 0);
+          accu[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ax[i2][p][mt], bu[i2], accu[mt], 0, 0, 0);
+        }
+  });
+  // the second K half hands its sums to the first through LDS
+  __syncthreads();
+  floatx4_t* s_h = reinterpret_cast<floatx4_t*>(ring);  // [gate 0..3 | up 4..7][mt][lane]
+  if (kap == 1) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      s_h[(tau * MT + mt) * kWave + lane] = accg[mt];
+      s_h[((4 + tau) * MT + mt) * kWave + lane] = accu[mt];
+    }
+  }
+  __syncthreads();
+  if (kap == 0) {
+    const int k = 16 * tau + fr;  // position = neuron r0 + k
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const floatx4_t og = s_h[(tau * MT + mt) * kWave + lane];
+      const floatx4_t ou = s_h[((4 + tau) * MT + mt) * kWave + lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        accg[mt][r] += og[r];
+        accu[mt][r] += ou[r];
+        const int m = 16 * mt + 4 * grp + r;  // C layout: neuron fr, tokens 4 (lane / 16) + r
+        const float h = (k < nr && m < B) ? silu(accg[mt][r]) * accu[mt][r] : 0.f;
+        if (k < sp) store_h(hhi, hlo, (size_t)m * hs + seg * sp + k, h);
+      }
+    }
+  }
+  // the kept list of every neuron, as the two-phase kernel writes it for t < 0
+  if (tid < nr) uidx[seg * sp + tid] = r0 + tid;
+  if (tid == 0) ucnt[seg] = nr;
+  if (seg == nseg - 1) zero_h_tail(hhi, hlo, hs, nseg * sp, kMpad);
 }
 
 // ---- per-token sparse gate/up over one segment (threshold, top-k gate pass, top-k keyed pass,
@@ -822,6 +933,19 @@ hipError_t launch_cats(const BatchLayout& L, hipStream_t stream, const uint16_t*
                                          ucnt, bidx, bcnt);
 }
 
+template <int TB, int NPM>
+hipError_t launch_all_np(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                         const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
+                         uint16_t* hlo, int32_t* uidx, int32_t* ucnt) {
+  using G = typename AllGeom<TB, NPM>::G;
+  static const hipError_t attr =
+      allow_dynamic_lds(reinterpret_cast<const void*>(all_ring_kernel<TB, NPM>), kCatsLds);
+  if (attr != hipSuccess) return attr;
+  klaunch(all_ring_kernel<TB, NPM>, L.nseg, kBT, (uint32_t)(G::kSlots * G::kSlotBytes), stream, xp, B,
+          wg, wu, d, F, L.np, hhi, hlo, L.hs, L.sp, uidx, ucnt);
+  return hipGetLastError();
+}
+
 hipError_t launch_gu_tb(int B, const BatchLayout& L, hipStream_t stream, const uint16_t* xp,
                         const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
                         uint16_t* hlo) {
@@ -901,6 +1025,10 @@ hipError_t launch_ffn_batch(const float* x, int B, const uint16_t* wg, const uin
     } else if (topk) {
       e = launch_cats_tb<kModeKeyed>(B, L, stream, xp, wg, wu, d, F, 0.f, const_cast<float*>(act),
                                      cut, hhi, hlo, uidx, ucnt, bidx, bcnt);
+    } else if (token_class(B) <= 8 && L.np <= kSegSmall) {  // every neuron kept: one pass
+      e = token_class(B) == 4
+              ? launch_all_np<4, kSegSmall>(L, stream, xp, B, wg, wu, d, F, hhi, hlo, uidx, ucnt)
+              : launch_all_np<8, kSegSmall>(L, stream, xp, B, wg, wu, d, F, hhi, hlo, uidx, ucnt);
     } else {
       e = launch_cats_tb<kModeAll>(B, L, stream, xp, wg, wu, d, F, 0.f, nullptr, nullptr, hhi, hlo,
                                    uidx, ucnt, bidx, bcnt);
