@@ -217,6 +217,12 @@ hipError_t launch_embed(const int32_t* tokens, int n, const uint16_t* E, int d, 
                         hipStream_t s);
 // y[i][j] = x[i] . W[j] (+ resid[i][j]) for i < n, j < N; W [N][K] bf16; K % 8 == 0 and
 // K <= 16384. With y_bf16 the rows are written as bf16 instead (resid and y unused).
+// RMSNorm (unit weight, bit for bit rmsnorm_vec_kernel's result) of n rows of x [n][K] as they
+// are staged, then q = xn Wq^T [n][Nq] fp32 and, for Nkv > 0, k = xn Wk^T, v = xn Wv^T [n][Nkv]
+// bf16 in one launch per 16 rows. K % 8 == 0, K <= 8192, 16-byte aligned rows.
+hipError_t launch_norm_qkv(const float* x, int n, int K, float eps, const uint16_t* Wq, int Nq,
+                           const uint16_t* Wk, const uint16_t* Wv, int Nkv, float* yq,
+                           uint16_t* yk, uint16_t* yv, hipStream_t s);
 hipError_t launch_linear(const float* x, int n, const uint16_t* W, int K, int N,
                          const float* resid, float* y, uint16_t* y_bf16, hipStream_t s);
 // seq[slot] = argmax of the V logits (lowest index on ties); cache_pos[0] += pos_delta;

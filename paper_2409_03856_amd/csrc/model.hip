@@ -5,6 +5,11 @@
 //  linear_kernel<NB>   y[i][j] = x[i] . W[j] (+ resid[i][j]) for up to NB rows of x staged in
 //                      LDS; one wave per output row (W row-major [N][K] bf16), fp32 or bf16
 //                      output (round to nearest even)
+//  norm_qkv_kernel<NB> RMSNorm of the rows as they are staged (the same sums, in the same order,
+//                      as rmsnorm_vec_kernel, so bit for bit its result), then the products of
+//                      up to three matrices in one launch: q = xn Wq^T (fp32), k = xn Wk^T and
+//                      v = xn Wv^T (bf16) -- a layer's attention inputs, or the final norm and
+//                      the LM head (q only)
 //  draft_tail_kernel   the sparse model's greedy draft: argmax of one logit row (lowest index
 //                      on ties) into the chunk buffer, and the cache position advanced by one
 //                      (wound back by n - 1 after the last draft, so the full model's pass
@@ -79,6 +84,88 @@ __global__ __launch_bounds__(kLinThreads) void linear_kernel(const float* __rest
           } else {
             y[o] = (resid != nullptr) ? resid[o] + s : s;
           }
+        }
+      }
+    }
+  }
+}
+
+// Output rows j of the three products in one range: [0, Nq) of Wq into yq (fp32), then
+// [Nq, Nq + Nkv) of Wk and [Nq + Nkv, Nq + 2 Nkv) of Wv into yk, yv (bf16). The rows of x are
+// normalised while staged: each thread sums the squares of its float4s tid + 256 u as
+// rmsnorm_vec_kernel does, the wave sums go through LDS, and after one barrier each thread scales
+// the elements it staged.
+template <int NB>
+__global__ __launch_bounds__(kLinThreads) void norm_qkv_kernel(
+    const float* __restrict__ x, int n, int K, float eps, const uint4* __restrict__ Wq, int Nq,
+    const uint4* __restrict__ Wk, const uint4* __restrict__ Wv, int Nkv, float* __restrict__ yq,
+    uint16_t* __restrict__ yk, uint16_t* __restrict__ yv) {
+  static_assert(kLinThreads == 256, "the norm's sums follow rmsnorm_vec_kernel's 256-thread layout");
+  constexpr int kPer = 8;  // K <= 8192
+  __shared__ float4 s_x4[kLinLds / 4];
+  __shared__ float s_w[NB][kLinWaves];
+  const float* xs = reinterpret_cast<const float*>(s_x4);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int k4 = K >> 2, k8 = K >> 3;
+  const float4* x4 = reinterpret_cast<const float4*>(x);
+  for (int i = 0; i < n; ++i) {
+    float4 v[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + kLinThreads * u;
+      v[u] = (e < k4) ? x4[(size_t)i * k4 + e] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      ss = fmaf(v[u].x, v[u].x, ss);
+      ss = fmaf(v[u].y, v[u].y, ss);
+      ss = fmaf(v[u].z, v[u].z, ss);
+      ss = fmaf(v[u].w, v[u].w, ss);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) s_w[i][wave] = ss;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + kLinThreads * u;
+      if (e < k4) s_x4[i * k4 + e] = v[u];
+    }
+  }
+  __syncthreads();
+  for (int i = 0; i < n; ++i) {
+    const float tot = ((s_w[i][0] + s_w[i][1]) + s_w[i][2]) + s_w[i][3];
+    const float inv = 1.0f / sqrtf(tot / (float)K + eps);
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + kLinThreads * u;
+      if (e < k4) {
+        const float4 t = s_x4[i * k4 + e];
+        s_x4[i * k4 + e] = make_float4(t.x * inv, t.y * inv, t.z * inv, t.w * inv);
+      }
+    }
+  }
+  __syncthreads();
+  const int N = Nq + 2 * Nkv;
+  for (int j = blockIdx.x * kLinWaves + wave; j < N; j += gridDim.x * kLinWaves) {
+    const int part = j < Nq ? 0 : (j < Nq + Nkv ? 1 : 2);  // uniform over the wave
+    const int jr = part == 0 ? j : (part == 1 ? j - Nq : j - Nq - Nkv);
+    const uint4* wr = (part == 0 ? Wq : (part == 1 ? Wk : Wv)) + (size_t)jr * k8;
+    float acc[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) acc[i] = 0.f;
+    for (int c = lane; c < k8; c += kWave) {
+      const uint4 w = wr[c];
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        if (i < n) acc[i] = dot8(w, xs + (size_t)i * K + 8 * c, acc[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (i < n) {  // n is uniform over the wave
+        const float s = wave_sum(acc[i]);
+        if (lane == i) {
+          if (part == 0) yq[(size_t)i * Nq + jr] = s;
+          else (part == 1 ? yk : yv)[(size_t)i * Nkv + jr] = (uint16_t)f32_to_bf16(s);
         }
       }
     }
@@ -188,6 +275,39 @@ hipError_t launch_embed(const int32_t* tokens, int n, const uint16_t* E, int d, 
   ProfScope prof("embed", s);
   klaunch(embed_kernel, n, 256, 0, s, tokens, n, reinterpret_cast<const uint4*>(E), d / 8, V, out);
   return hipGetLastError();
+}
+
+hipError_t launch_norm_qkv(const float* x, int n, int K, float eps, const uint16_t* Wq, int Nq,
+                           const uint16_t* Wk, const uint16_t* Wv, int Nkv, float* yq,
+                           uint16_t* yk, uint16_t* yv, hipStream_t s) {
+  if ((K & 7) != 0 || K > 8192 || n < 1 || Nq < 1 || Nkv < 0 ||
+      (Nkv > 0 && (Wk == nullptr || Wv == nullptr || yk == nullptr || yv == nullptr)))
+    return hipErrorInvalidValue;
+  ProfScope prof("norm_qkv", s);
+  const int nb = std::min(16, kLinLds / K);
+  for (int i0 = 0; i0 < n; i0 += nb) {
+    const int m = std::min(nb, n - i0);
+    const int grid = std::min(ceil_div(Nq + 2 * Nkv, kLinWaves), 2048);
+    const float* xi = x + (size_t)i0 * K;
+    float* qi = yq + (size_t)i0 * Nq;
+    uint16_t* ki = Nkv > 0 ? yk + (size_t)i0 * Nkv : nullptr;
+    uint16_t* vi = Nkv > 0 ? yv + (size_t)i0 * Nkv : nullptr;
+    const uint4* q4 = reinterpret_cast<const uint4*>(Wq);
+    const uint4* k4 = reinterpret_cast<const uint4*>(Wk);
+    const uint4* v4 = reinterpret_cast<const uint4*>(Wv);
+#define SIRIUS_NQKV(NBV)                                                                          \
+  if (m <= NBV) {                                                                                 \
+    klaunch(norm_qkv_kernel<NBV>, grid, kLinThreads, 0, s, xi, m, K, eps, q4, Nq, k4, v4, Nkv, qi, ki, vi); \
+    hipError_t e = hipGetLastError();                                                             \
+    if (e != hipSuccess) return e;                                                                \
+    continue;                                                                                     \
+  }
+    SIRIUS_NQKV(1)
+    SIRIUS_NQKV(4)
+    SIRIUS_NQKV(16)
+#undef SIRIUS_NQKV
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_linear(const float* x, int n, const uint16_t* W, int K, int N,

@@ -137,12 +137,21 @@ hipError_t forward(const sirius_model* m, const int32_t* tokens, int n, const in
   float* att = reinterpret_cast<float*>(ws + L.att);
   char* sub = ws + L.sub;
   hipError_t e;
+  // the norm folds into the projections' launch when the rows take the vectorised norm (the
+  // same sums, so the same bits); otherwise the separate norm and one launch per product
+  const bool fused = (d & 3) == 0 && d <= 8192 && (reinterpret_cast<uintptr_t>(h) & 15) == 0;
   if ((e = sirius::launch_embed(tokens, n, m->embed, d, m->vocab, h, s)) != hipSuccess) return e;
   for (int l = 0; l < m->n_layers; ++l) {
-    if ((e = sirius::launch_rmsnorm(h, n, d, m->norm_eps, xn, s)) != hipSuccess) return e;
-    if ((e = sirius::launch_linear(xn, n, m->wq + l * st.q, d, hq, nullptr, q, nullptr, s)) != hipSuccess) return e;
-    if ((e = sirius::launch_linear(xn, n, m->wk + l * st.kv, d, hkv, nullptr, nullptr, kb, s)) != hipSuccess) return e;
-    if ((e = sirius::launch_linear(xn, n, m->wv + l * st.kv, d, hkv, nullptr, nullptr, vb, s)) != hipSuccess) return e;
+    if (fused) {
+      if ((e = sirius::launch_norm_qkv(h, n, d, m->norm_eps, m->wq + l * st.q, hq, m->wk + l * st.kv,
+                                       m->wv + l * st.kv, hkv, q, kb, vb, s)) != hipSuccess)
+        return e;
+    } else {
+      if ((e = sirius::launch_rmsnorm(h, n, d, m->norm_eps, xn, s)) != hipSuccess) return e;
+      if ((e = sirius::launch_linear(xn, n, m->wq + l * st.q, d, hq, nullptr, q, nullptr, s)) != hipSuccess) return e;
+      if ((e = sirius::launch_linear(xn, n, m->wk + l * st.kv, d, hkv, nullptr, nullptr, kb, s)) != hipSuccess) return e;
+      if ((e = sirius::launch_linear(xn, n, m->wv + l * st.kv, d, hkv, nullptr, nullptr, vb, s)) != hipSuccess) return e;
+    }
     const sirius::AttnLayout AL = sirius::attn_layout(1, n, H, Hkv, hd, m->max_len);
     if ((e = sirius::launch_attn_kv(q, kb, vb, m->k_cache + l * st.cache, m->v_cache + l * st.cache,
                                     cache_pos, 1, n, H, Hkv, hd, m->max_len, att, sub, AL, s)) != hipSuccess)
@@ -154,6 +163,9 @@ hipError_t forward(const sirius_model* m, const int32_t* tokens, int n, const in
                      acnt ? acnt + l * c_lstride : nullptr, sub, s)) != hipSuccess)
       return e;
   }
+  if (fused)
+    return sirius::launch_norm_qkv(h, n, d, m->norm_eps, m->lm_head, m->vocab, nullptr, nullptr, 0,
+                                   logits, nullptr, nullptr, s);
   if ((e = sirius::launch_rmsnorm(h, n, d, m->norm_eps, xn, s)) != hipSuccess) return e;
   return sirius::launch_linear(xn, n, m->lm_head, d, m->vocab, nullptr, logits, nullptr, s);
 }
