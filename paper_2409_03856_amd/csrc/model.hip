@@ -92,9 +92,9 @@ __global__ __launch_bounds__(kLinThreads) void linear_kernel(const float* __rest
 
 // Output rows j of the three products in one range: [0, Nq) of Wq into yq (fp32), then
 // [Nq, Nq + Nkv) of Wk and [Nq + Nkv, Nq + 2 Nkv) of Wv into yk, yv (bf16). The rows of x are
-// normalised while staged: each thread sums the squares of its float4s tid + 256 u as
-// rmsnorm_vec_kernel does, the wave sums go through LDS, and after one barrier each thread scales
-// the elements it staged.
+// staged in LDS (every load in flight at once), then normalised there: each thread sums the
+// squares of its float4s tid + 256 u of a row as rmsnorm_vec_kernel does, the wave sums go through
+// LDS, and after one barrier each thread scales its float4s.
 template <int NB>
 __global__ __launch_bounds__(kLinThreads) void norm_qkv_kernel(
     const float* __restrict__ x, int n, int K, float eps, const uint4* __restrict__ Wq, int Nq,
@@ -108,28 +108,21 @@ __global__ __launch_bounds__(kLinThreads) void norm_qkv_kernel(
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int k4 = K >> 2, k8 = K >> 3;
   const float4* x4 = reinterpret_cast<const float4*>(x);
+  for (int e = tid; e < n * k4; e += kLinThreads) s_x4[e] = x4[e];  // every row's loads in flight
+  __syncthreads();
   for (int i = 0; i < n; ++i) {
-    float4 v[kPer];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int e = tid + kLinThreads * u;
-      v[u] = (e < k4) ? x4[(size_t)i * k4 + e] : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
     float ss = 0.f;
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
-      ss = fmaf(v[u].x, v[u].x, ss);
-      ss = fmaf(v[u].y, v[u].y, ss);
-      ss = fmaf(v[u].z, v[u].z, ss);
-      ss = fmaf(v[u].w, v[u].w, ss);
+      const int e = tid + kLinThreads * u;
+      const float4 v = (e < k4) ? s_x4[i * k4 + e] : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss = fmaf(v.x, v.x, ss);
+      ss = fmaf(v.y, v.y, ss);
+      ss = fmaf(v.z, v.z, ss);
+      ss = fmaf(v.w, v.w, ss);
     }
     ss = wave_sum(ss);
     if (lane == 0) s_w[i][wave] = ss;
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int e = tid + kLinThreads * u;
-      if (e < k4) s_x4[i * k4 + e] = v[u];
-    }
   }
   __syncthreads();
   for (int i = 0; i < n; ++i) {
