@@ -96,10 +96,36 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     }
     return;
   }
-  // the direct rewrite: the new rows of this chunk go into the cache
+  // the direct rewrite: the new rows of this chunk go into the cache; the thread's first new-row
+  // chunk and its first query chunk are requested together, so the two take one round trip
+  const int w0 = max(c0, p);
+  const int ncw = rg == 0 ? (c1 - w0) * hd8 : 0;  // 16-byte chunks of new rows to write
+  {
+    uint4 kw0 = make_uint4(0u, 0u, 0u, 0u), vw0 = kw0;
+    size_t dst0 = 0;
+    if (tid < ncw) {
+      const int j = tid / hd8, c = tid - j * hd8, pos = w0 + j;
+      const size_t src = (((size_t)b * n + (pos - p)) * Hkv + kvh) * hd8 + c;
+      dst0 = (((size_t)b * Lmax + pos) * Hkv + kvh) * hd8 + c;
+      kw0 = k_new[src];
+      vw0 = v_new[src];
+    }
+    float4 qv = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int qr = tid / hd4, qd4 = tid - qr * hd4;
+    if (tid < nr4 * hd4 && qr < nr) {
+      const int rr = r0 + qr, i = rr / G, h = kvh * G + (rr - i * G);
+      qv = reinterpret_cast<const float4*>(q + (((size_t)b * n + i) * H + h) * hd)[qd4];
+    }
+    if (tid < ncw) {
+      k_cache[dst0] = kw0;
+      v_cache[dst0] = vw0;
+    }
+    if (tid < nr4 * hd4)
+      *reinterpret_cast<float4*>(&s_q[qr * kPitch + 4 * qd4]) =
+          make_float4(qv.x * scale, qv.y * scale, qv.z * scale, qv.w * scale);
+  }
   if (rg == 0) {
-    const int w0 = max(c0, p);
-    for (int e = tid; e < (c1 - w0) * hd8; e += kAttnThreads) {
+    for (int e = tid + kAttnThreads; e < ncw; e += kAttnThreads) {
       const int j = e / hd8, c = e - j * hd8, pos = w0 + j;
       const size_t src = (((size_t)b * n + (pos - p)) * Hkv + kvh) * hd8 + c;
       const size_t dst = (((size_t)b * Lmax + pos) * Hkv + kvh) * hd8 + c;
@@ -108,7 +134,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     }
   }
   // query rows (row r = token i * G + head g), scaled; padding rows are zero
-  for (int e = tid; e < nr4 * hd4; e += kAttnThreads) {
+  for (int e = tid + kAttnThreads; e < nr4 * hd4; e += kAttnThreads) {
     const int r = e / hd4, d4 = e - r * hd4;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (r < nr) {
@@ -270,16 +296,18 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       }
     }
     __syncthreads();
-    // ---- online softmax: four lanes per row, 16 positions each
+    // ---- online softmax: LPR lanes per row (4 for up to 64 rows, 16 for up to 16), the tile's
+    // positions split evenly over them
     {
-      const int r = tid >> 2, part = tid & 3;
+      constexpr int LPR = BIG ? 4 : 16, PPL = kTile / LPR;
+      const int r = tid / LPR, part = tid % LPR;
       float mx = -INFINITY;
       if (r < nr) {
 #pragma unroll
-        for (int jj = 0; jj < kTile / 4; ++jj) mx = fmaxf(mx, s_p[(part * (kTile / 4) + jj) * kPPitch + r]);
+        for (int jj = 0; jj < PPL; ++jj) mx = fmaxf(mx, s_p[(part * PPL + jj) * kPPitch + r]);
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 2, kWave));
+#pragma unroll
+      for (int m = 1; m < LPR; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, kWave));
       float m_old = -INFINITY, m_new = -INFINITY;
       if (r < nr) {
         m_old = s_m[r];
@@ -288,15 +316,15 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       float sum = 0.f;
       if (r < nr) {
 #pragma unroll
-        for (int jj = 0; jj < kTile / 4; ++jj) {
-          float* sp = &s_p[(part * (kTile / 4) + jj) * kPPitch + r];
+        for (int jj = 0; jj < PPL; ++jj) {
+          float* sp = &s_p[(part * PPL + jj) * kPPitch + r];
           const float e = (*sp > -INFINITY) ? expf(*sp - m_new) : 0.f;
           *sp = e;
           sum += e;
         }
       }
-      sum += __shfl_xor(sum, 1, kWave);
-      sum += __shfl_xor(sum, 2, kWave);
+#pragma unroll
+      for (int m = 1; m < LPR; m <<= 1) sum += __shfl_xor(sum, m, kWave);
       if (r < nr && part == 0) {
         const float alpha = (m_old > -INFINITY) ? expf(m_old - m_new) : 0.f;
         s_alpha[r] = alpha;
@@ -322,6 +350,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
           acc[u][rr].w *= al;
         }
         const int span = kTile / jg, j0 = (BIG ? 0 : jgrp) * span, j1 = min(j0 + span, tn);
+#pragma unroll 4
         for (int j = j0; j < j1; ++j) {
           const float4 pv = *reinterpret_cast<const float4*>(&s_p[j * kPPitch + 4 * rb]);
           const uint2 vw = *reinterpret_cast<const uint2*>(&s_v16[j * kKVPitch8 * 8 + 4 * d4]);
@@ -377,6 +406,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         float4 t = s_red[tid * 4 + rr];
+#pragma unroll 4
         for (int g2 = 1; g2 < jg; ++g2) {
           const float4 o = s_red[(g2 * nob + tid) * 4 + rr];
           t.x += o.x;
