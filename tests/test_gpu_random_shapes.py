@@ -1,7 +1,8 @@
 """GPU parity over seeded random shapes: the dense, threshold-sparse (CATS) and per-token top-k FFN
 calls through the one FFN dispatcher -- the batch-1 decode kernel, the batched MFMA engine at every
-token class and at short and long segments (d_model % 256 == 0, 2..64 tokens), the small-batch
-kernels of other widths -- with and without RMSNorm and residual, against the fp64 oracle."""
+token class and at short and long segments (d_model % 256 == 0, 2..64 tokens, d_ff up to 14336),
+the small-batch kernels of other widths -- with and without RMSNorm and residual, against the fp64
+oracle."""
 
 import numpy as np
 import pytest
@@ -22,7 +23,8 @@ def _cases(n=18, seed=2409):
     out = []
     for i in range(n):
         d = int(rng.choice(_WIDTHS))
-        f = int(rng.integers(1, 4201))
+        # even cases: short segments (d_ff <= 4200: at most 20 neurons); odd: up to 56 neurons
+        f = int(rng.integers(1, 4201)) if i % 2 == 0 else int(rng.integers(7200, 14337))
         b = int(rng.choice(_BATCHES))
         out.append((i, d, f, b, bool(rng.integers(0, 2))))
     return out
