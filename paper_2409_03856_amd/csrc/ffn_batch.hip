@@ -16,6 +16,10 @@
 //                      token tile move into an LDS ring by direct global-to-LDS loads, two to
 //                      four K blocks in flight; wave (tile, product) multiplies with
 //                      v_mfma_f32_16x16x32_bf16.
+//  gu_unit_kernel      the same for 8..16 tokens with d_model a multiple of 2048: the weights
+//                      move through LDS in units of 16 rows x 2048 columns, each row's 4 KiB
+//                      requested by one wave with consecutive 1 KiB direct loads (the order in
+//                      which HBM streams a row fastest), x held in registers.
 //  cats_ring_kernel    per-token sparsity over one segment: the gate rows alone through the ring
 //                      (threshold mode and the top-k gate pass), SiLU, the per-token keep
 //                      decision (|a| > t, or the top-k key against the token's cut), the union of
@@ -391,6 +395,129 @@ __global__ __launch_bounds__(kBT) void gu_ring_kernel(const uint16_t* __restrict
     }
   }
   if (blockIdx.x == gridDim.x - 1) zero_h_tail(hhi, hlo, hs, gridDim.x * sp, 16 * MT);
+}
+
+// ---- dense gate/up of 8..16 tokens on the bf16-rounded input with d_model a multiple of 2048.
+// HBM streams a weight row fastest when its bytes are requested close together in time: one wave
+// reading a row's aligned 4 KiB with consecutive 1 KiB loads moves about 6.8 TB/s over the chip,
+// the same bytes requested 256 or 512 bytes per row per instruction, or spread over later
+// instructions, 5.0-6.0. The ring kernel above requests each row 256 bytes per K block; this one
+// moves the weights through LDS in units of 16 rows x 2048 columns, wave w requesting row w of
+// the unit with four consecutive 1 KiB direct loads, two unit buffers (128.5 KiB of LDS).
+// Segment rows: gate rows [0, np), up rows [np, 2 np), padded to whole 16-row tiles with zero
+// rows; units go tile by tile with the K spans inner, so a row's spans are requested in
+// consecutive units. Wave w multiplies K steps 4 w .. 4 w + 3 of every unit (x in registers for
+// the whole call, the weights from LDS) into one partial per tile; the 16 partials are summed in
+// wave order at the end, so the result does not depend on timing.
+constexpr int kUnitThreads = 1024;                  // 16 waves: one row of a unit each
+constexpr int kUnitWaves = kUnitThreads / kWave;
+constexpr int kUnitK = 2048;                        // columns per unit (4 KiB of a row)
+constexpr int kUnitRowBytes = kUnitK * 2 + 16;      // LDS row stride: the 16 rows of an MFMA
+                                                    // operand read lie in distinct banks
+constexpr int kUnitBytes = 16 * kUnitRowBytes;      // 65792
+constexpr int kUnitLds = 2 * kUnitBytes;            // 131584
+constexpr int kUnitTiles = (2 * kSegN + 15) / 16;   // 16-row tiles per segment at most (7)
+constexpr int kUnitLoads = kUnitK * 2 / 1024;       // 1 KiB loads per wave per unit (4)
+constexpr int kUnitSteps = kUnitK / 32 / kUnitWaves;  // 32-wide K steps per wave per unit (4)
+static_assert(kUnitWaves * kUnitTiles * kWave * 16 + kUnitTiles * 16 * 16 * 4 <= kUnitLds,
+              "the end-of-call reduction fits in the unit buffers");
+__device__ __align__(16) uint16_t g_zero_row[kUnitK];  // source of the padding rows
+
+template <int NSPAN>  // d_model / 2048
+__global__ __launch_bounds__(kUnitThreads) void gu_unit_kernel(
+    const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int hs, int np, int sp,
+    uint16_t* __restrict__ hhi, uint16_t* __restrict__ hlo) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_u[];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int fr = lane & 15, grp = lane >> 4;
+  const int n0 = blockIdx.x * np;
+  const int T = (2 * np + 15) >> 4;  // tiles of the segment's rows
+  const int U = T * NSPAN;           // units
+
+  // x operand (A: token rows; rows past B are zero in xp) of this wave's K steps in every span
+  bf16x8_t xa[NSPAN][kUnitSteps];
+#pragma unroll
+  for (int s = 0; s < NSPAN; ++s)
+#pragma unroll
+    for (int j = 0; j < kUnitSteps; ++j)
+      xa[s][j] = as_bf16x8(*reinterpret_cast<const uint4*>(
+          xp + (size_t)fr * d + s * kUnitK + 32 * (kUnitSteps * wave + j) + 8 * grp));
+
+  // unit u = (tile u / NSPAN, span u % NSPAN) into buffer u & 1: wave w requests row w of the tile
+  auto issue = [&](int u) {
+    const int t = u / NSPAN, s = u - t * NSPAN;
+    const int r = __builtin_amdgcn_readfirstlane(16 * t + wave);  // wave-uniform
+    const uint16_t* src = r < np       ? wg + (size_t)min(n0 + r, F - 1) * d + s * kUnitK
+                          : r < 2 * np ? wu + (size_t)min(n0 + r - np, F - 1) * d + s * kUnitK
+                                       : g_zero_row;
+    unsigned char* row = lds_u + (u & 1) * kUnitBytes + wave * kUnitRowBytes;
+#pragma unroll
+    for (int q = 0; q < kUnitLoads; ++q) {
+      auto* lp = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<size_t>(row + q * 1024));  // lane l lands at + 16 l
+      __builtin_amdgcn_global_load_lds(src + q * 512 + 8 * lane, lp, 16, 0, 2);
+    }
+  };
+
+  floatx4_t acc[kUnitTiles];
+#pragma unroll
+  for (int t = 0; t < kUnitTiles; ++t) acc[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  issue(0);
+  if (U > 1) issue(1);
+#pragma unroll
+  for (int t = 0; t < kUnitTiles; ++t) {
+    if (t >= T) break;  // uniform
+#pragma unroll
+    for (int s = 0; s < NSPAN; ++s) {
+      const int u = t * NSPAN + s;
+      // this wave's loads of unit u have landed (unit u + 1 still in flight), then every wave's
+      if (u + 1 < U) wait_vm<kUnitLoads>();
+      else wait_vm<0>();
+      ring_barrier();
+      const unsigned char* buf = lds_u + (u & 1) * kUnitBytes;
+      bf16x8_t bw[kUnitSteps];  // B operand: weight row fr of the tile
+#pragma unroll
+      for (int j = 0; j < kUnitSteps; ++j)
+        bw[j] = *reinterpret_cast<const bf16x8_t*>(
+            buf + fr * kUnitRowBytes + 2 * (32 * (kUnitSteps * wave + j) + 8 * grp));
+#pragma unroll
+      for (int j = 0; j < kUnitSteps; ++j)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[s][j], bw[j], acc[t], 0, 0, 0);
+      if (u + 2 < U) {
+        ring_barrier();  // every wave is done reading buffer u & 1
+        issue(u + 2);
+      }
+    }
+  }
+
+  // the waves' partials summed in wave order (red[w][t][lane]) into res[row][token]
+  __syncthreads();
+  floatx4_t* red = reinterpret_cast<floatx4_t*>(lds_u);
+  float* res = reinterpret_cast<float*>(lds_u + kUnitWaves * kUnitTiles * kWave * 16);
+#pragma unroll
+  for (int t = 0; t < kUnitTiles; ++t)
+    if (t < T) red[(wave * kUnitTiles + t) * kWave + lane] = acc[t];
+  __syncthreads();
+  if (tid < T * kWave) {
+    const int t = tid >> 6, l = tid & (kWave - 1);
+    floatx4_t v = red[t * kWave + l];
+#pragma unroll
+    for (int w = 1; w < kUnitWaves; ++w) v += red[(w * kUnitTiles + t) * kWave + l];
+    // C layout: lane l holds weight row (l & 15) of the tile and tokens 4 (l >> 4) + e
+#pragma unroll
+    for (int e = 0; e < 4; ++e) res[(16 * t + (l & 15)) * 16 + 4 * (l >> 4) + e] = v[e];
+  }
+  __syncthreads();
+  // h at the segment's positions [0, sp), as the ring kernel writes it: neuron n0 + j, zero past
+  // the segment's rows, past d_ff and for the padding tokens
+  for (int i = tid; i < 16 * sp; i += kUnitThreads) {
+    const int m = i / sp, j = i - m * sp;
+    const bool real = j < np && n0 + j < F && m < B;
+    store_h(hhi, hlo, (size_t)m * hs + (size_t)blockIdx.x * sp + j,
+            real ? silu(res[j * 16 + m]) * res[(np + j) * 16 + m] : 0.f);
+  }
+  if (blockIdx.x == gridDim.x - 1) zero_h_tail(hhi, hlo, hs, gridDim.x * sp, 16);
 }
 
 // ---- every neuron kept (the dense and condensed FFN of small batches on the exact input) in one
@@ -898,6 +1025,30 @@ hipError_t launch_gu_np(const BatchLayout& L, hipStream_t stream, const uint16_t
           wg, wu, d, F, L.hs, L.np, L.sp, hhi, hlo);
   return hipGetLastError();
 }
+template <int NSPAN>
+hipError_t launch_gu_unit_n(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                            const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
+                            uint16_t* hlo) {
+  static const hipError_t attr =
+      allow_dynamic_lds(reinterpret_cast<const void*>(gu_unit_kernel<NSPAN>), kUnitLds);
+  if (attr != hipSuccess) return attr;
+  klaunch(gu_unit_kernel<NSPAN>, L.nseg, kUnitThreads, (uint32_t)kUnitLds, stream, xp, B, wg, wu, d,
+          F, L.hs, L.np, L.sp, hhi, hlo);
+  return hipGetLastError();
+}
+// the unit kernel takes one 16-token tile and d_model = 2048, 4096, 6144 or 8192
+bool gu_unit_ok(int B, int d) { return B <= 16 && d % kUnitK == 0 && d <= 4 * kUnitK; }
+hipError_t launch_gu_unit(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                          const uint16_t* wg, const uint16_t* wu, int d, int F, uint16_t* hhi,
+                          uint16_t* hlo) {
+  switch (d / kUnitK) {
+    case 1: return launch_gu_unit_n<1>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
+    case 2: return launch_gu_unit_n<2>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
+    case 3: return launch_gu_unit_n<3>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
+    case 4: return launch_gu_unit_n<4>(L, stream, xp, B, wg, wu, d, F, hhi, hlo);
+    default: return hipErrorInvalidValue;
+  }
+}
 // short segments (np <= kSegSmall) of the small token classes take the deeper ring
 template <int TB>
 hipError_t launch_gu(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
@@ -1018,7 +1169,8 @@ hipError_t launch_ffn_batch(const float* x, int B, const uint16_t* wg, const uin
   {
     ProfScope prof(pfx_gu, stream);
     if (!exact) {
-      e = launch_gu_tb(B, L, stream, xp, wg, wu, d, F, hhi, hlo);
+      e = gu_unit_ok(B, d) ? launch_gu_unit(L, stream, xp, B, wg, wu, d, F, hhi, hlo)
+                           : launch_gu_tb(B, L, stream, xp, wg, wu, d, F, hhi, hlo);
     } else if (thr) {
       e = launch_cats_tb<kModeThr>(B, L, stream, xp, wg, wu, d, F, t, nullptr, nullptr, hhi, hlo,
                                    uidx, ucnt, bidx, bcnt);

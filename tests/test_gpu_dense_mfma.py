@@ -38,7 +38,11 @@ def _layer(seed, d, f, std):
                                      # one 16-token tile with d_model % 128 == 0: the LDS-ring gate/up
                                      # kernel (ragged d_ff, partial last segments, a single K block)
                                      (1024, 5000, 16), (4096, 14000, 13), (128, 8, 8), (256, 1000, 10),
-                                     (4096, 40, 16)])
+                                     (4096, 40, 16),
+                                     # d_model a multiple of 2048 and at most 16 tokens: the gate/up
+                                     # kernel on 16-row x 2048-column units (one, three and four K
+                                     # spans, one and seven tiles per segment, rows past d_ff)
+                                     (2048, 3000, 8), (6144, 777, 11), (2048, 90, 9), (8192, 3000, 16)])
 def test_ragged_batches(sr, d, f, bsz):
     say(f"dense mfma d={d} f={f} B={bsz}")
     (wg, wu, wd), W = _layer(500 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
@@ -121,7 +125,7 @@ def test_llama3_8b_tree_pass(sr, bsz):
     assert rel_err(y - res, oracle.ffn_dense(xn, wg, wu, wd)) <= METHOD_TOL
 
 
-@pytest.mark.parametrize("d,f", [(256, 1000), (256, 97), (512, 3100)])
+@pytest.mark.parametrize("d,f", [(256, 1000), (256, 97), (512, 3100), (2048, 1000)])
 @pytest.mark.parametrize("bsz,mode", [(4, "dense"), (16, "dense"), (64, "dense"), (16, "cats")])
 def test_segment_tail_on_dirty_workspace(sr, d, f, bsz, mode):
     """Batched calls whose segment layout ends inside a 64-position down block (250 segments of
