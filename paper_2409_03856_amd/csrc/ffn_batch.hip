@@ -20,6 +20,9 @@
 //                      move through LDS in units of 16 rows x 2048 columns, each row's 4 KiB
 //                      requested by one wave with consecutive 1 KiB direct loads (the order in
 //                      which HBM streams a row fastest), x held in registers.
+//  cats_unit_kernel    the same modes as cats_ring_kernel for at most 4 tokens with d_model a
+//                      multiple of 2048 on the unit layout: the three pieces of the four tokens
+//                      are the 12 rows of one MFMA operand tile, held in registers.
 //  cats_ring_kernel    per-token sparsity over one segment: the gate rows alone through the ring
 //                      (threshold mode and the top-k gate pass), SiLU, the per-token keep
 //                      decision (|a| > t, or the top-k key against the token's cut), the union of
@@ -423,50 +426,54 @@ static_assert(kUnitWaves * kUnitTiles * kWave * 16 + kUnitTiles * 16 * 16 * 4 <=
               "the end-of-call reduction fits in the unit buffers");
 __device__ __align__(16) uint16_t g_zero_row[kUnitK];  // source of the padding rows
 
-template <int NSPAN>  // d_model / 2048
-__global__ __launch_bounds__(kUnitThreads) void gu_unit_kernel(
-    const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
-    const uint16_t* __restrict__ wu, int d, int F, int hs, int np, int sp,
-    uint16_t* __restrict__ hhi, uint16_t* __restrict__ hlo) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char lds_u[];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  const int fr = lane & 15, grp = lane >> 4;
-  const int n0 = blockIdx.x * np;
-  const int T = (2 * np + 15) >> 4;  // tiles of the segment's rows
-  const int U = T * NSPAN;           // units
-
-  // x operand (A: token rows; rows past B are zero in xp) of this wave's K steps in every span
-  bf16x8_t xa[NSPAN][kUnitSteps];
+// x operand (A) of this wave's K steps in every span: row fr of the tile from `row` (16 rows of
+// d columns), zero where `ok` is false (the load is issued anyway, from row 0, so every wave's
+// load count is the same)
+template <int NSPAN>
+__device__ __forceinline__ void unit_x(bf16x8_t (&xa)[NSPAN][kUnitSteps], const uint16_t* row,
+                                       bool ok) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6, grp = lane >> 4;
 #pragma unroll
   for (int s = 0; s < NSPAN; ++s)
 #pragma unroll
-    for (int j = 0; j < kUnitSteps; ++j)
-      xa[s][j] = as_bf16x8(*reinterpret_cast<const uint4*>(
-          xp + (size_t)fr * d + s * kUnitK + 32 * (kUnitSteps * wave + j) + 8 * grp));
+    for (int j = 0; j < kUnitSteps; ++j) {
+      uint4 v = *reinterpret_cast<const uint4*>(row + s * kUnitK + 32 * (kUnitSteps * wave + j) + 8 * grp);
+      if (!ok) v = make_uint4(0u, 0u, 0u, 0u);
+      xa[s][j] = as_bf16x8(v);
+    }
+}
 
-  // unit u = (tile u / NSPAN, span u % NSPAN) into buffer u & 1: wave w requests row w of the tile
+// The unit pipeline: T (<= TMAX) tiles of 16 rows, row r of the sequence from row_of(r) (wave-
+// uniform; nullptr: a zero row), units (tile u / NSPAN, span u % NSPAN) in two LDS buffers, wave w
+// requesting row w of every unit; acc[t] = this wave's K steps of tile t. Then the waves'
+// partials are summed in wave order into res[16 t + row][x row] (fp32, in LDS past the partials),
+// and the unit buffers are free again. A row's result does not depend on its place in the
+// sequence: the same loads, steps and sums give it wherever it sits.
+template <int NSPAN, int TMAX, class RowOf>
+__device__ __forceinline__ float* unit_pass(unsigned char* lds_u, int T, RowOf row_of,
+                                            const bf16x8_t (&xa)[NSPAN][kUnitSteps]) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int fr = lane & 15, grp = lane >> 4;
+  const int U = T * NSPAN;
   auto issue = [&](int u) {
-    const int t = u / NSPAN, s = u - t * NSPAN;
-    const int r = __builtin_amdgcn_readfirstlane(16 * t + wave);  // wave-uniform
-    const uint16_t* src = r < np       ? wg + (size_t)min(n0 + r, F - 1) * d + s * kUnitK
-                          : r < 2 * np ? wu + (size_t)min(n0 + r - np, F - 1) * d + s * kUnitK
-                                       : g_zero_row;
-    unsigned char* row = lds_u + (u & 1) * kUnitBytes + wave * kUnitRowBytes;
+    const int t = u / NSPAN, sp_ = u - t * NSPAN;
+    const uint16_t* row = row_of(__builtin_amdgcn_readfirstlane(16 * t + wave));  // wave-uniform
+    const uint16_t* src = row != nullptr ? row + sp_ * kUnitK : g_zero_row;
+    unsigned char* dst = lds_u + (u & 1) * kUnitBytes + wave * kUnitRowBytes;
 #pragma unroll
     for (int q = 0; q < kUnitLoads; ++q) {
       auto* lp = reinterpret_cast<__attribute__((address_space(3))) void*>(
-          reinterpret_cast<size_t>(row + q * 1024));  // lane l lands at + 16 l
+          reinterpret_cast<size_t>(dst + q * 1024));  // lane l lands at + 16 l
       __builtin_amdgcn_global_load_lds(src + q * 512 + 8 * lane, lp, 16, 0, 2);
     }
   };
-
-  floatx4_t acc[kUnitTiles];
+  floatx4_t acc[TMAX];
 #pragma unroll
-  for (int t = 0; t < kUnitTiles; ++t) acc[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < TMAX; ++t) acc[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   issue(0);
   if (U > 1) issue(1);
 #pragma unroll
-  for (int t = 0; t < kUnitTiles; ++t) {
+  for (int t = 0; t < TMAX; ++t) {
     if (t >= T) break;  // uniform
 #pragma unroll
     for (int s = 0; s < NSPAN; ++s) {
@@ -490,25 +497,46 @@ __global__ __launch_bounds__(kUnitThreads) void gu_unit_kernel(
       }
     }
   }
-
-  // the waves' partials summed in wave order (red[w][t][lane]) into res[row][token]
+  // the waves' partials summed in wave order: red[w][t][lane], then res
   __syncthreads();
   floatx4_t* red = reinterpret_cast<floatx4_t*>(lds_u);
-  float* res = reinterpret_cast<float*>(lds_u + kUnitWaves * kUnitTiles * kWave * 16);
+  float* res = reinterpret_cast<float*>(lds_u + kUnitWaves * TMAX * kWave * 16);
 #pragma unroll
-  for (int t = 0; t < kUnitTiles; ++t)
-    if (t < T) red[(wave * kUnitTiles + t) * kWave + lane] = acc[t];
+  for (int t = 0; t < TMAX; ++t)
+    if (t < T) red[(wave * TMAX + t) * kWave + lane] = acc[t];
   __syncthreads();
   if (tid < T * kWave) {
     const int t = tid >> 6, l = tid & (kWave - 1);
     floatx4_t v = red[t * kWave + l];
 #pragma unroll
-    for (int w = 1; w < kUnitWaves; ++w) v += red[(w * kUnitTiles + t) * kWave + l];
-    // C layout: lane l holds weight row (l & 15) of the tile and tokens 4 (l >> 4) + e
+    for (int w = 1; w < kUnitWaves; ++w) v += red[(w * TMAX + t) * kWave + l];
+    // C layout: lane l holds weight row (l & 15) of the tile and x rows 4 (l >> 4) + e
 #pragma unroll
     for (int e = 0; e < 4; ++e) res[(16 * t + (l & 15)) * 16 + 4 * (l >> 4) + e] = v[e];
   }
   __syncthreads();
+  return res;
+}
+
+template <int NSPAN>  // d_model / 2048
+__global__ __launch_bounds__(kUnitThreads) void gu_unit_kernel(
+    const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int hs, int np, int sp,
+    uint16_t* __restrict__ hhi, uint16_t* __restrict__ hlo) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_u[];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int n0 = blockIdx.x * np;
+  // x operand: token rows (rows past B are zero in xp)
+  bf16x8_t xa[NSPAN][kUnitSteps];
+  unit_x<NSPAN>(xa, xp + (size_t)(lane & 15) * d, true);
+  const float* res = unit_pass<NSPAN, kUnitTiles>(
+      lds_u, (2 * np + 15) >> 4,
+      [&](int r) -> const uint16_t* {
+        return r < np       ? wg + (size_t)min(n0 + r, F - 1) * d
+               : r < 2 * np ? wu + (size_t)min(n0 + r - np, F - 1) * d
+                            : nullptr;
+      },
+      xa);
   // h at the segment's positions [0, sp), as the ring kernel writes it: neuron n0 + j, zero past
   // the segment's rows, past d_ff and for the padding tokens
   for (int i = tid; i < 16 * sp; i += kUnitThreads) {
@@ -518,6 +546,151 @@ __global__ __launch_bounds__(kUnitThreads) void gu_unit_kernel(
             real ? silu(res[j * 16 + m]) * res[(np + j) * 16 + m] : 0.f);
   }
   if (blockIdx.x == gridDim.x - 1) zero_h_tail(hhi, hlo, hs, gridDim.x * sp, 16);
+}
+
+// ---- per-token sparse gate/up of at most 4 tokens on the exact input (threshold, top-k gate pass,
+// top-k keyed pass, every neuron kept), d_model a multiple of 2048, on the unit pipeline: the
+// three bf16 pieces of the four tokens are the 12 rows of one MFMA operand tile (row 4 p + m), so
+// the whole input stays in registers. Phase A streams the segment's gate rows, phase B the up rows
+// of the tokens' union; keep decisions, lists and h as cats_ring_kernel forms them. A row's sum is
+// its three pieces' sums added in piece order. With every neuron kept the gate and up rows go in
+// one pass (each row's result is the same wherever it sits in the sequence), so a threshold below
+// 0 still gives the dense result bit for bit.
+constexpr int kCatsUnitTokens = 4;
+constexpr int kCatsUnitTiles = (kSegN + 15) / 16;  // 16-row tiles of one phase (4)
+constexpr int kModeThr = 0, kModeAct = 1, kModeKeyed = 2, kModeAll = 3;
+
+__device__ __forceinline__ float piece_sum(const float* res, int row, int m) {
+  return (res[row * 16 + m] + res[row * 16 + 4 + m]) + res[row * 16 + 8 + m];
+}
+
+template <int NSPAN, int MODE>
+__global__ __launch_bounds__(kUnitThreads) void cats_unit_kernel(
+    const uint16_t* __restrict__ xp, int B, const uint16_t* __restrict__ wg,
+    const uint16_t* __restrict__ wu, int d, int F, int np, float t, float* __restrict__ act,
+    const unsigned long long* __restrict__ cut, uint16_t* __restrict__ hhi,
+    uint16_t* __restrict__ hlo, int hs, int sp, int32_t* __restrict__ uidx,
+    int32_t* __restrict__ ucnt, int32_t* __restrict__ bidx, int32_t* __restrict__ bcnt) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_u[];
+  __shared__ float s_a[kCatsUnitTokens][kSegPad];         // a = SiLU(g) per token and position
+  __shared__ unsigned long long s_keep[kCatsUnitTokens];  // kept positions per token
+  __shared__ int s_u[kSegPad];                            // union positions, ascending
+  __shared__ int s_nu;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int seg = blockIdx.x, nseg = gridDim.x;
+  const int r0 = seg * np;
+  const int nr = min(np, F - r0);  // neurons of this segment (>= 1)
+  constexpr int kMpad = 16;        // rows of xp per piece and of h
+
+  // x operand: row 4 p + m = piece p of token m (rows 12..15 and tokens past B: zero)
+  bf16x8_t xa[NSPAN][kUnitSteps];
+  {
+    const int fr = lane & 15, pc = fr >> 2, m = fr & 3;
+    const bool ok = fr < 12 && m < B;
+    unit_x<NSPAN>(xa, xp + ((size_t)(ok ? pc : 0) * kMpad + (ok ? m : 0)) * d, ok);
+  }
+
+  if (MODE == kModeAll) {  // gate rows [0, np), up rows [np, 2 np) in one pass
+    const float* res = unit_pass<NSPAN, kUnitTiles>(
+        lds_u, (2 * np + 15) >> 4,
+        [&](int r) -> const uint16_t* {
+          return r < np       ? wg + (size_t)(r0 + min(r, nr - 1)) * d
+                 : r < 2 * np ? wu + (size_t)(r0 + min(r - np, nr - 1)) * d
+                              : nullptr;
+        },
+        xa);
+    for (int i = tid; i < kMpad * sp; i += kUnitThreads) {
+      const int m = i / sp, k = i - m * sp;
+      const float h = (m < B && k < nr) ? silu(piece_sum(res, k, m)) * piece_sum(res, np + k, m) : 0.f;
+      store_h(hhi, hlo, (size_t)m * hs + (size_t)seg * sp + k, h);
+    }
+    // the kept list of every neuron, as the threshold path writes it for t < 0
+    if (tid < nr) uidx[seg * sp + tid] = r0 + tid;
+    if (tid == 0) ucnt[seg] = nr;
+    if (seg == nseg - 1) zero_h_tail(hhi, hlo, hs, nseg * sp, kMpad);
+    return;
+  }
+
+  // ---- phase A: the gate (threshold mode and the top-k gate pass) or the stored activations
+  if (MODE != kModeKeyed) {
+    const float* res = unit_pass<NSPAN, kCatsUnitTiles>(
+        lds_u, (np + 15) >> 4,
+        [&](int r) -> const uint16_t* {
+          return r < np ? wg + (size_t)(r0 + min(r, nr - 1)) * d : nullptr;
+        },
+        xa);
+    for (int i = tid; i < kCatsUnitTokens * kSegPad; i += kUnitThreads) {
+      const int m = i / kSegPad, j = i - m * kSegPad;
+      if (j < np) {
+        const float a = silu(piece_sum(res, j, m));
+        if (MODE == kModeAct) {
+          if (m < B && j < nr) act[(size_t)m * F + r0 + j] = a;
+        } else {
+          s_a[m][j] = a;
+        }
+      }
+    }
+    if (MODE == kModeAct) return;  // uniform
+  } else {
+    for (int i = tid; i < kCatsUnitTokens * kSegPad; i += kUnitThreads) {
+      const int m = i / kSegPad, j = i - m * kSegPad;
+      s_a[m][j] = (m < B && j < nr) ? act[(size_t)m * F + r0 + j] : 0.f;
+    }
+  }
+  __syncthreads();
+
+  // ---- keep decisions per token (a wave ballot over the segment's positions), per-token lists
+  if (wave < kCatsUnitTokens) {
+    const int m = wave;
+    const float a = s_a[m][lane];
+    bool keep = false;
+    if (m < B && lane < nr) {
+      if (MODE == kModeKeyed) keep = topk_key(a, r0 + lane) >= cut[m];
+      else keep = fabsf(a) > t;
+    }
+    const unsigned long long mk = __ballot(keep);
+    if (lane == 0) s_keep[m] = mk;
+    if (m < B && bidx != nullptr) {
+      if (keep) bidx[((size_t)m * nseg + seg) * kSegPad + __popcll(mk & ((1ull << lane) - 1ull))] = r0 + lane;
+      if (lane == 0) bcnt[m * nseg + seg] = __popcll(mk);
+    }
+  }
+  __syncthreads();
+  // ---- union of the tokens' kept positions, ascending
+  if (wave == 0) {
+    unsigned long long un = 0ull;
+    for (int m = 0; m < B && m < kCatsUnitTokens; ++m) un |= s_keep[m];
+    const bool in = (un >> lane) & 1ull;
+    const int pos = __popcll(un & ((1ull << lane) - 1ull));
+    if (in) {
+      s_u[pos] = lane;
+      uidx[seg * sp + pos] = r0 + lane;
+    }
+    if (lane == 0) {
+      s_nu = __popcll(un);
+      ucnt[seg] = __popcll(un);
+    }
+  }
+  __syncthreads();
+  const int nu = s_nu;
+
+  // ---- phase B: the up rows of the union only; h = a u where the token keeps the neuron
+  const float* res = nullptr;
+  if (nu > 0)  // uniform
+    res = unit_pass<NSPAN, kCatsUnitTiles>(
+        lds_u, (nu + 15) >> 4,
+        [&](int k) -> const uint16_t* { return k < nu ? wu + (size_t)(r0 + s_u[k]) * d : nullptr; },
+        xa);
+  for (int i = tid; i < kMpad * sp; i += kUnitThreads) {
+    const int m = i / sp, k = i - m * sp;
+    float h = 0.f;
+    if (m < B && k < nu) {
+      const int j = s_u[k];
+      if ((s_keep[m] >> j) & 1ull) h = s_a[m][j] * piece_sum(res, k, m);
+    }
+    store_h(hhi, hlo, (size_t)m * hs + (size_t)seg * sp + k, h);  // 0 past nu
+  }
+  if (seg == nseg - 1) zero_h_tail(hhi, hlo, hs, nseg * sp, kMpad);
 }
 
 // ---- every neuron kept (the dense and condensed FFN of small batches on the exact input) in one
@@ -631,9 +804,9 @@ __global__ __launch_bounds__(kBT) void all_ring_kernel(
 // (phase B) rows [0, np), then the token rows (piece p, token m) at np + p TB + m (zeros past B).
 // Wave w: 16-neuron tile w & 3, K steps of half w >> 2 of each block; the halves are added in a
 // fixed order. The A operand for piece p and tile mt reads token row min(16 mt + r, TB - 1).
-constexpr int kModeThr = 0, kModeAct = 1, kModeKeyed = 2, kModeAll = 3;
-// (kModeAll keeps every neuron: the dense and condensed FFN of small batches on the exact input,
-// through the same kernels, and so the same sums, as the threshold path with t < 0.)
+// (The modes are those of cats_unit_kernel above. kModeAll keeps every neuron: the dense and
+// condensed FFN of small batches on the exact input, through the same kernels, and so the same
+// sums, as the threshold path with t < 0.)
 
 template <int TB, int MODE, int NPM>
 __global__ __launch_bounds__(kBT) void cats_ring_kernel(
@@ -1110,11 +1283,49 @@ hipError_t launch_gu_tb(int B, const BatchLayout& L, hipStream_t stream, const u
   }
 }
 
+// the unit kernel of the exact-input modes: at most 4 tokens, d_model = 2048, 4096, 6144 or 8192
+bool cats_unit_ok(int B, int d) {
+  return B <= kCatsUnitTokens && d % kUnitK == 0 && d <= 4 * kUnitK;
+}
+template <int NSPAN, int MODE>
+hipError_t launch_cats_unit_n(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                              const uint16_t* wg, const uint16_t* wu, int d, int F, float t,
+                              float* act, const unsigned long long* cut, uint16_t* hhi,
+                              uint16_t* hlo, int32_t* uidx, int32_t* ucnt, int32_t* bidx,
+                              int32_t* bcnt) {
+  static const hipError_t attr =
+      allow_dynamic_lds(reinterpret_cast<const void*>(cats_unit_kernel<NSPAN, MODE>), kUnitLds);
+  if (attr != hipSuccess) return attr;
+  klaunch(cats_unit_kernel<NSPAN, MODE>, L.nseg, kUnitThreads, (uint32_t)kUnitLds, stream, xp, B, wg,
+          wu, d, F, L.np, t, act, cut, hhi, hlo, L.hs, L.sp, uidx, ucnt, bidx, bcnt);
+  return hipGetLastError();
+}
+template <int MODE>
+hipError_t launch_cats_unit(const BatchLayout& L, hipStream_t stream, const uint16_t* xp, int B,
+                            const uint16_t* wg, const uint16_t* wu, int d, int F, float t,
+                            float* act, const unsigned long long* cut, uint16_t* hhi,
+                            uint16_t* hlo, int32_t* uidx, int32_t* ucnt, int32_t* bidx,
+                            int32_t* bcnt) {
+#define SIRIUS_CATS_UNIT(NS)                                                                   \
+  case NS:                                                                                     \
+    return launch_cats_unit_n<NS, MODE>(L, stream, xp, B, wg, wu, d, F, t, act, cut, hhi, hlo, \
+                                        uidx, ucnt, bidx, bcnt);
+  switch (d / kUnitK) {
+    SIRIUS_CATS_UNIT(1) SIRIUS_CATS_UNIT(2) SIRIUS_CATS_UNIT(3) SIRIUS_CATS_UNIT(4)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef SIRIUS_CATS_UNIT
+}
+
 template <int MODE>
 hipError_t launch_cats_tb(int B, const BatchLayout& L, hipStream_t stream, const uint16_t* xp,
                           const uint16_t* wg, const uint16_t* wu, int d, int F, float t,
                           float* act, const unsigned long long* cut, uint16_t* hhi, uint16_t* hlo,
                           int32_t* uidx, int32_t* ucnt, int32_t* bidx, int32_t* bcnt) {
+  if (cats_unit_ok(B, d))
+    return launch_cats_unit<MODE>(L, stream, xp, B, wg, wu, d, F, t, act, cut, hhi, hlo, uidx, ucnt,
+                                  bidx, bcnt);
 #define SIRIUS_CATS_TB(TBV)                                                                     \
   case TBV:                                                                                     \
     return launch_cats<TBV, MODE>(L, stream, xp, B, wg, wu, d, F, t, act, cut, hhi, hlo, uidx,  \
@@ -1177,7 +1388,7 @@ hipError_t launch_ffn_batch(const float* x, int B, const uint16_t* wg, const uin
     } else if (topk) {
       e = launch_cats_tb<kModeKeyed>(B, L, stream, xp, wg, wu, d, F, 0.f, const_cast<float*>(act),
                                      cut, hhi, hlo, uidx, ucnt, bidx, bcnt);
-    } else if (token_class(B) <= 8 && L.np <= kSegSmall) {  // every neuron kept: one pass
+    } else if (token_class(B) <= 8 && L.np <= kSegSmall && !cats_unit_ok(B, d)) {  // every neuron kept: one ring pass
       e = token_class(B) == 4
               ? launch_all_np<4, kSegSmall>(L, stream, xp, B, wg, wu, d, F, hhi, hlo, uidx, ucnt)
               : launch_all_np<8, kSegSmall>(L, stream, xp, B, wg, wu, d, F, hhi, hlo, uidx, ucnt);

@@ -5,7 +5,7 @@ import pytest
 
 import oracle
 from synth import ffn_weights, decode_inputs, calibration_inputs, TINY, LLAMA3_8B
-from gpu_util import (say, dev_bf16, dev_f32, host, check_cats_sets, check_ffn)
+from gpu_util import (say, dev_bf16, dev_f32, host, check_cats_sets, check_topk_sets, check_ffn)
 
 pytestmark = pytest.mark.gpu
 
@@ -84,6 +84,34 @@ def test_negative_threshold_is_dense(sr, bsz):
     check_ffn(host(y), ref)
     yd = sr.sirius_ffn_dense(dev_f32(x), *W)
     assert np.array_equal(host(yd), host(y))  # same kernels, same order: bitwise
+
+
+@pytest.mark.parametrize("d,f,bsz,norm", [(2048, 3000, 2, False), (4096, 1000, 4, True), (6144, 777, 3, False),
+                                          (2048, 14000, 4, True), (8192, 3000, 3, True)])
+def test_wide_small_batches_every_mode(sr, d, f, bsz, norm):
+    """At most 4 tokens with d_model a multiple of 2048 (one to four K spans; one to seven row
+    tiles per segment): threshold sets and outputs, a threshold below 0 equal to the dense call
+    bit for bit, the dense call against the oracle, and per-token top-k, with and without RMSNorm
+    and residual."""
+    say(f"wide small batch d={d} f={f} B={bsz} norm={norm}")
+    (wg, wu, wd), W = _layer(1200 + d + f + bsz, d, f, 1.0 / np.sqrt(d))
+    x = decode_inputs(1300 + bsz, bsz, d) * (3.0 if norm else 1.0)
+    res = decode_inputs(1400 + bsz, bsz, d) if norm else None
+    xn = oracle.rmsnorm(x, 1e-5) if norm else x
+    kw = dict(norm_eps=1e-5, resid=dev_f32(res)) if norm else {}
+    t = float(np.median(np.abs(oracle.gate_activations(xn, wg))))
+    y, idx, cnt = sr.sirius_ffn_cats(dev_f32(x), *W, t, **kw)
+    sets, _ = check_cats_sets(xn, wg, t, host(idx), host(cnt))
+    check_ffn(host(y), oracle.ffn_masked(xn, wg, wu, wd, sets), resid=res)
+    yneg, _, cneg = sr.sirius_ffn_cats(dev_f32(x), *W, -1.0, **kw)
+    assert np.all(host(cneg) == f)
+    yd = sr.sirius_ffn_dense(dev_f32(x), *W, **kw)
+    assert np.array_equal(host(yd), host(yneg))  # same kernel, same sums: bitwise
+    check_ffn(host(yd), oracle.ffn_dense(xn, wg, wu, wd), resid=res)
+    k = max(1, f // 3)
+    y, idx, cnt = sr.sirius_ffn_topk(dev_f32(x), *W, k, **kw)
+    sets, _ = check_topk_sets(xn, wg, k, host(idx), host(cnt))
+    check_ffn(host(y), oracle.ffn_masked(xn, wg, wu, wd, sets), resid=res)
 
 
 def test_infinite_threshold_is_residual(sr):
