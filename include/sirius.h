@@ -447,9 +447,14 @@ int sirius_fill_normal_bf16(uint16_t* out, size_t n, uint64_t seed, float mean, 
  * the events of one kernel name and returns the summed duration in
  * milliseconds and the number of launches (0 and 0 for an unknown name).
  * Kernel names: "cats_decode", "cats_reduce", "dense_decode", "dense_reduce",
- * "topk_decode", "topk_reduce" (batch 1); "cats_gate", "cats_down",
- * "dense_gate", "dense_down", "topk_up", "topk_down" (batches 2..8);
- * "ffn_mfma_prep", "ffn_mfma_gate_up", "ffn_mfma_down", "ffn_mfma_reduce";
+ * "topk_decode", "topk_reduce" (batch 1); "batch_prep", "batch_gate_up",
+ * "batch_seg_gate_up", "batch_cats_up", "batch_topk_prep", "batch_topk_gate",
+ * "batch_topk_up", "batch_down", "batch_reduce" (2..64 tokens with d_model a
+ * multiple of 256); "cats_gate", "cats_down", "dense_gate", "dense_down",
+ * "topk_up", "topk_down" (small batches at other shapes); "ffn_mfma_prep",
+ * "ffn_mfma_gate_up", "ffn_mfma_down", "ffn_mfma_reduce" (8 or more tokens
+ * at other shapes); "embed", "norm_qkv", "linear", "draft_tail",
+ * "period_tail" (the small decoder);
  * "calib_gate", "select_init", "select_hist", "select_pick"; "topk_gate",
  * "topk_cut"; "verify_stats", "verify_scan", "tree_stats", "tree_scan",
  * "tree_topw", "tree_select"; "griffin_z", "griffin_rownorm", "griffin_score",
