@@ -26,8 +26,9 @@
 //                fixed order into one partial per workgroup. (Owning columns instead, to
 //                avoid partials, means 32-byte reads per row, and the per-CU limit on
 //                outstanding line requests then caps useful bandwidth near a quarter.)
-//  reduce_kernel y = resid + the row-range partials summed in order; extra blocks build the
-//                per-token ascending active lists.
+//  reduce_kernel y = resid + the row-range partials summed in order (one output per thread with
+//                every row in flight for at most 16 rows and 256K outputs or more); extra
+//                blocks build the per-token ascending active lists.
 
 
 
@@ -396,6 +397,13 @@ __global__ __launch_bounds__(256) void down_kernel(
   }
 }
 
+// The one-output-per-thread form of the sums (below) when there are at most 16 partial rows and
+// enough outputs for 256 workgroups; with fewer outputs the grouped form keeps more workgroups
+// busy. Both give the same bits.
+__host__ __device__ constexpr bool red_wide(int gr, int n) {
+  return gr <= kRedGroups && n >= 4 * 256 * 256;
+}
+
 // y = resid + sum over the gr row-range partials in order (bitwise reproducible); the blocks
 // past the reduction build the per-token ascending active lists.
 __global__ __launch_bounds__(256) void reduce_kernel(
@@ -405,6 +413,36 @@ __global__ __launch_bounds__(256) void reduce_kernel(
   __shared__ float4 s_red[kRedGroups][kRedOut4];
   __shared__ int s_tmp[4];
   const int tid = threadIdx.x;
+  if ((int)blockIdx.x < nred && red_wide(gr, n)) {
+    // at most 16 partial rows: one float4 output per thread with every row's load in flight
+    // (each row read 4 KiB contiguous per block), added in the order of the grouped sum below,
+    // whose group g then holds 0 + row g: the same bits
+    const int o4 = blockIdx.x * 256 + tid;
+    if (4 * o4 >= n) return;
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    const size_t stride4 = (size_t)(n >> 2);
+    float4 v[kRedGroups];
+#pragma unroll
+    for (int r = 0; r < kRedGroups; ++r)
+      v[r] = r < gr ? p4[(size_t)r * stride4 + o4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 s = make_float4(0.f + v[0].x, 0.f + v[0].y, 0.f + v[0].z, 0.f + v[0].w);
+#pragma unroll
+    for (int r = 1; r < kRedGroups; ++r) {
+      s.x += 0.f + v[r].x;
+      s.y += 0.f + v[r].y;
+      s.z += 0.f + v[r].z;
+      s.w += 0.f + v[r].w;
+    }
+    if (resid != nullptr) {
+      const float4 rv = reinterpret_cast<const float4*>(resid)[o4];
+      s.x = rv.x + s.x;
+      s.y = rv.y + s.y;
+      s.z = rv.z + s.z;
+      s.w = rv.w + s.w;
+    }
+    reinterpret_cast<float4*>(y)[o4] = s;
+    return;
+  }
   if ((int)blockIdx.x < nred) {
     // kRedOut4 float4 outputs per block; thread (o, g) sums partial rows g, g + 16, ... of
     // output o with kRedUnroll loads in flight; the 16 groups are then added in order
@@ -609,7 +647,7 @@ hipError_t launch_ffn_gemv(const float* x, int B, const uint16_t* wg, const uint
       return e;
   }
   const int n = B * d;
-  const int nred = ceil_div(n, 4 * kRedOut4);
+  const int nred = ceil_div(n, 4 * (red_wide(L.gr, n) ? 256 : kRedOut4));  // blocks of the sums
   ProfScope prof(topk ? "topk_reduce" : (thr ? "cats_reduce" : "dense_reduce"), stream);
   klaunch(reduce_kernel, nred + (lists ? B * kListBlocks : 0), 256, 0, stream, 
       part, L.gr, n, resid, y, nred, B, F, L.ntiles, L.rmax, bidx, bcnt, active_idx, active_cnt);
@@ -644,7 +682,7 @@ hipError_t launch_reduce(const float* part, int gr, int B, int d, const float* r
                          hipStream_t stream, int F, int nseg, int rmax, const int32_t* bidx,
                          const int32_t* bcnt, int32_t* active_idx, int32_t* active_cnt) {
   const int n = B * d;
-  const int nred = ceil_div(n, 4 * kRedOut4);
+  const int nred = ceil_div(n, 4 * (red_wide(gr, n) ? 256 : kRedOut4));  // blocks of the sums
   const bool lists = active_idx != nullptr;
   if (lists && nseg > kListSegs) return hipErrorInvalidValue;
   klaunch(reduce_kernel, nred + (lists ? B * kListBlocks : 0), 256, 0, stream, 
