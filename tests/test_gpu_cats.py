@@ -114,6 +114,55 @@ def test_wide_small_batches_every_mode(sr, d, f, bsz, norm):
     check_ffn(host(y), oracle.ffn_masked(xn, wg, wu, wd, sets), resid=res)
 
 
+@pytest.mark.parametrize("mode,bsz", [("dense", 16), ("cats", 4), ("dense", 4), ("dense", 64)])
+def test_batched_calls_under_graph_capture(sr, mode, bsz):
+    """Batched calls at a width the unit kernels take (the 16-token gate/up kernel, the exact-input
+    kernel of at most 4 tokens in threshold and every-neuron-kept mode, and the 64-token pass with
+    its one-output-per-thread reduce) record into a HIP graph; every replay, with eager calls in
+    between, equals the eager result bit for bit (kept lists included)."""
+    import torch
+    d, f = 2048, 3000
+    (wg, wu, wd), W = _layer(1500 + bsz, d, f, 1.0 / np.sqrt(d))
+    x = dev_f32(decode_inputs(1600 + bsz, bsz, d))
+    res = dev_f32(decode_inputs(1700 + bsz, bsz, d))
+    op = sr.OP_FFN_DENSE if mode == "dense" else sr.OP_FFN_CATS
+    ws = torch.empty((int(sr.lib().sirius_workspace_size(op, bsz, d, f, 0, 0)),), dtype=torch.uint8,
+                     device="cuda")
+    y = torch.empty_like(x)
+    idx = torch.empty((bsz, f), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((bsz,), dtype=torch.int32, device="cuda")
+    t = 0.02
+
+    def call():
+        if mode == "dense":
+            sr.sirius_ffn_dense(x, *W, norm_eps=1e-5, resid=res, y=y, ws=ws)
+        else:
+            sr.sirius_ffn_cats(x, *W, t, norm_eps=1e-5, resid=res, y=y, active_idx=idx, active_cnt=cnt,
+                               ws=ws)
+
+    say(f"graph capture {mode} B={bsz}")
+    call()
+    torch.cuda.synchronize()
+    want, want_cnt = host(y).copy(), host(cnt).copy()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            call()
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(3):
+        y.fill_(float("nan"))
+        cnt.fill_(-1)
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(y), want), f"replay {rep}"
+        if mode == "cats":
+            assert np.array_equal(host(cnt), want_cnt), f"replay {rep} counts"
+        call()  # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_infinite_threshold_is_residual(sr):
     (wg, wu, wd), W = _layer(400, TINY.d_model, TINY.d_ff, TINY.weight_std)
     x = decode_inputs(400, 2, TINY.d_model)
